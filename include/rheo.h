@@ -1,0 +1,175 @@
+/*
+ * rheo.h -- C ABI of the RheoSampling hot path on AMD Instinct MI355X (gfx950).
+ *
+ * RheoSampling (arXiv 2609.21827) builds a speculative-decoding draft tree by
+ * EAGLE's expand-then-rerank (Sec. 2.1) with one stochastic slot per candidate
+ * pool: the top-m draft tokens, then one token Y sampled from the tail
+ * distribution q~, then the highest-ranked remaining tokens (Sec. 3.2, "Hybrid
+ * sampling mechanism"; App. C.1).  Y competes in expansion and pruning with
+ * the proxy probability min{q(x_m), z} and is verified with its true
+ * probability q~(Y) (Sec. 3.2, "Dual treatment").  The tree is pruned globally
+ * to R nodes by path score with a fixed tie-break (App. C.1) and verified
+ * layer by layer by RheoVerification (Algorithm 1; Thm. 1).
+ *
+ * One decoding step for B independent sequences is
+ *     rheo_begin_step
+ *     rheo_expand_level  x depth     (draft logits of the current frontier)
+ *     rheo_prune
+ *     rheo_verify                    (target logits of the pruned tree)
+ * and the caller runs its draft / target model between the calls, using
+ * rheo_frontier and rheo_pruned_view to learn which rows to compute.
+ *
+ * Conventions
+ *   - All data pointers are device pointers (HBM) unless marked "host".
+ *     The caller owns every logit and output buffer; the tree handle owns its
+ *     own device state, sized at rheo_create.
+ *   - Every call that takes a stream enqueues work on that HIP stream
+ *     (hipStream_t, passed as void*; NULL = the default stream) and returns
+ *     without synchronising.  A handle must not be used from two streams at
+ *     once; calls on one handle must follow the step order above.
+ *   - Return value: RHEO_OK or a negative error code; rheo_last_error()
+ *     gives a message for the calling thread's last failure.  Arguments are
+ *     validated on the host before anything is enqueued, so an error leaves
+ *     the device state as it was.
+ *   - Logit rows: dtype RHEO_F32 or RHEO_BF16, V contiguous elements per row,
+ *     consecutive rows row_stride elements apart, base pointer 16-byte aligned
+ *     and row_stride a multiple of 16 bytes.  Logits must be finite.
+ *   - Decisions are exact: each probability is an integer weight (a
+ *     fixed-point softmax numerator evaluated by a fixed fp32 operation
+ *     sequence), sums are exact 64-bit integers and every sampling or
+ *     acceptance decision is an exact integer comparison, so results do not
+ *     depend on launch shapes or reduction order.  Random draws are
+ *     Philox4x64-10 (Salmon et al., SC'11) blocks keyed by rng_key with the
+ *     counter (index, sequence, purpose, 0), purposes 1 = the sampled token
+ *     of the node with uid index, 2 = acceptance test 32*level + j (j = 0 for
+ *     the sampled child, else the candidate's slot), 3 = the final sample of
+ *     a level.
+ */
+#ifndef RHEO_H
+#define RHEO_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct rheo_tree rheo_tree;
+
+enum {
+    RHEO_OK = 0,
+    RHEO_EINVAL = -1,   /* invalid argument or configuration             */
+    RHEO_ENOMEM = -2,   /* device allocation failed                      */
+    RHEO_EHIP = -3,     /* a HIP runtime call failed (message attached)  */
+    RHEO_ESTATE = -4    /* call out of the step order                    */
+};
+
+enum { RHEO_F32 = 0, RHEO_BF16 = 1 };
+
+typedef struct rheo_config {
+    int32_t batch;               /* B >= 1 independent sequences                      */
+    int32_t vocab;               /* V, 2 <= V <= 262143                               */
+    int32_t pool;                /* K slots per candidate pool, sampled slot included
+                                    (Sec. 3.2); 1 <= K <= 15                           */
+    int32_t leads;               /* m deterministic lead tokens, 0 <= m <= K-1          */
+    int32_t depth;               /* D expansion levels, 1 <= D <= 15                   */
+    int32_t n_expand;            /* parents expanded per level below the root,
+                                    1..K (EAGLE expands K, Sec. 2.1); 0 means K         */
+    int32_t support;             /* S: draft logits truncated to their top-S entries
+                                    before the softmax (Sec. 3.2, sparse draft; the
+                                    paper uses 128, App. B).  K <= S <= 1024; S >= V
+                                    keeps the whole vocabulary                          */
+    int32_t construct_tempered;  /* 0: tree built on untempered q (Sec. 5.4);
+                                    1: on the tempered q_T                              */
+    int32_t dtype;               /* RHEO_F32 or RHEO_BF16                               */
+    int32_t reserved;            /* must be 0                                           */
+    int64_t row_stride;          /* elements between consecutive logit rows (>= V)     */
+    double eps_m0;               /* epsilon of the m = 0 proxy q(x_1) + eps (Sec. 3.2);
+                                    0 selects 2^-40                                     */
+} rheo_config;
+
+/* Allocates a tree for cfg (host pointer, copied).  *out receives the handle.
+ * Node capacity per sequence: 1 + K + (D-1) * n_expand * K. */
+int rheo_create(const rheo_config* cfg, rheo_tree** out);
+
+/* Frees the handle and its device memory (synchronises the device). */
+int rheo_destroy(rheo_tree* tree);
+
+/* Starts a new step: the next rheo_expand_level builds level 0 from the root. */
+int rheo_begin_step(rheo_tree* tree);
+
+/* Expands the current frontier by one level (Sec. 2.1 with the pools of
+ * Sec. 3.2 / App. C.1).
+ *   draft_logits  [B][P][row_stride] of cfg.dtype, P = 1 at level 0 (the
+ *                 root) and n_expand afterwards; row (b, j) holds the draft
+ *                 model's logits at frontier node j of sequence b.
+ *   T             sampling temperature (> 0, finite): Y ~ q~_T.
+ *   rng_key       key of the step's Philox draws.
+ * Writes K children per frontier node (token, proxy, true probability,
+ * path score) and, below the last level, selects the n_expand children with
+ * the highest path scores as the next frontier.  With support S, the
+ * truncated distribution is kept in the tree for verification, so the
+ * draft buffer may be reused as soon as this call's work has run. */
+int rheo_expand_level(rheo_tree* tree, const void* draft_logits, float T,
+                      uint64_t rng_key, void* stream);
+
+/* The frontier chosen by the last rheo_expand_level, in rank order:
+ *   parent_index  [B][n_expand] int32: index of the node's parent in the
+ *                 previous frontier (0 at level 1)
+ *   token         [B][n_expand] int32: the node's token
+ * (device pointers; either may be NULL). */
+int rheo_frontier(rheo_tree* tree, int32_t* parent_index, int32_t* token,
+                  void* stream);
+
+/* Keeps the budget R best non-root nodes (1 <= R <= K + (D-1) n_expand K) by
+ * path score, ties by depth (shallower first) then left-to-right sibling
+ * order (App. C.1); the root does not count towards R. */
+int rheo_prune(rheo_tree* tree, int32_t budget, void* stream);
+
+/* The pruned tree in rank order, index 0 = root:
+ *   parent  [B][R+1] int32 (pruned index of the parent, -1 for the root)
+ *   token   [B][R+1] int32 (-1 for the root)
+ * Row i of the target buffer given to rheo_verify must hold the target
+ * model's logits at pruned node i. */
+int rheo_pruned_view(rheo_tree* tree, int32_t* parent, int32_t* token,
+                     void* stream);
+
+/* RheoVerification (Algorithm 1) applied layer by layer from the root
+ * (Thm. 1), with p = softmax(target / T) over the whole vocabulary.
+ *   target_logits [B][R+1][row_stride] of cfg.dtype (pruned-node order)
+ *   accepted      [B][depth] int32: accepted draft tokens, -1 after the end
+ *   accept_len    [B] int32: number of accepted draft tokens
+ *   final_token   [B] int32: the token emitted after them (residual sample,
+ *                 or a sample of p below an accepted leaf)
+ * The output of a step is accepted[0..accept_len) followed by final_token. */
+int rheo_verify(rheo_tree* tree, const void* target_logits, float T,
+                uint64_t rng_key, int32_t* accepted, int32_t* accept_len,
+                int32_t* final_token, void* stream);
+
+/* Copies the unpruned tree of the current step (uid order, [B][N], N =
+ * 1 + K + (D-1) n_expand K, uid 0 = root; children of a level are numbered
+ * in frontier order, then slot order).  Any pointer may be NULL.
+ *   kind: 0 lead, 1 sampled, 2 fill; qtrue: q~(Y) for the sampled slot,
+ *   q(x) for the others; score: product of proxies from the root. */
+int rheo_read_nodes(rheo_tree* tree, int32_t* token, int32_t* parent,
+                    int32_t* depth, int32_t* slot, int32_t* kind,
+                    double* proxy, double* qtrue, double* score, void* stream);
+
+/* Synchronises the device and copies the tree's sticky device error flag to
+ * *host_flag (0 = no error; bit 0: no sampled token found, bit 1: pruned
+ * tree not ancestor-closed, bit 2: sampled child missing from its parent's
+ * tail, bit 3: residual sample out of range, bit 4: corrupt frontier,
+ * bit 5: corrupt verification walk).  Diagnostic only. */
+int rheo_device_error(rheo_tree* tree, int32_t* host_flag);
+
+/* Nodes per sequence of the unpruned tree (root included). */
+int32_t rheo_node_count(const rheo_tree* tree);
+
+/* Message of the calling thread's last failed call ("" if none). */
+const char* rheo_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RHEO_H */

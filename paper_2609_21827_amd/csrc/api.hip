@@ -1,0 +1,304 @@
+// Host side of the C ABI declared in include/rheo.h: validation, device
+// state, step order and kernel launches.  Nothing here synchronises except
+// rheo_destroy and rheo_device_error.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <string>
+
+#include "rheo.h"
+#include "rheo_state.h"
+
+using namespace rheo;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+    return fail(RHEO_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+enum State { CREATED, EXPANDING, EXPANDED, PRUNED, VERIFIED };
+
+constexpr int kCap = 1024;       // candidate capacity of the expand kernel
+constexpr int kMaxV = 262143;
+
+float k_of_T(float T) { return (float)(1.4426950408889634 / (double)T); }
+
+}  // namespace
+
+struct rheo_tree {
+    rheo_config cfg;
+    TreeDev dev;
+    State state = CREATED;
+    int level = 0;
+    int R = 0;
+    int variant = 0;
+    int min_blocks = 1024;
+    float T_expand = 1.0f;
+    void* blocks[32] = {};
+    int nblocks = 0;
+};
+
+namespace {
+
+template <typename T>
+int dalloc(rheo_tree* t, T** p, size_t count) {
+    const size_t bytes = count * sizeof(T) ? count * sizeof(T) : 16;
+    void* q = nullptr;
+    const hipError_t e = hipMalloc(&q, bytes);
+    if (e != hipSuccess) return fail(RHEO_ENOMEM, "hipMalloc(%zu): %s", bytes, hipGetErrorString(e));
+    t->blocks[t->nblocks++] = q;
+    *p = (T*)q;
+    return RHEO_OK;
+}
+
+void free_all(rheo_tree* t) {
+    for (int i = 0; i < t->nblocks; ++i) (void)hipFree(t->blocks[i]);
+    t->nblocks = 0;
+}
+
+int check_ptr(const void* p, const char* name) {
+    if (!p) return fail(RHEO_EINVAL, "%s is NULL", name);
+    if ((uintptr_t)p % 16) return fail(RHEO_EINVAL, "%s is not 16-byte aligned", name);
+    return RHEO_OK;
+}
+
+int check_T(float T) {
+    if (!(T > 0.0f) || !std::isfinite(T)) return fail(RHEO_EINVAL, "temperature must be finite and > 0");
+    if (!std::isfinite(k_of_T(T))) return fail(RHEO_EINVAL, "temperature too small");
+    return RHEO_OK;
+}
+
+// Segment layout of one level's expand launch.
+void level_shape(const rheo_tree* t, int rows, int* G, int* seg_len) {
+    const TreeDev& d = t->dev;
+    const ExpandVariant v = expand_variant(d.dtype, t->variant);
+    const int vec = d.dtype ? 8 : 4;
+    const int cap = v.nt * v.ept;
+    const int gmax = kCap / d.S;
+    int g = (d.V + cap - 1) / cap;
+    // more segments while the launch is small (fills the 256 compute units),
+    // keeping every segment at least 4 S elements long
+    while (g < gmax && rows * g < t->min_blocks && d.V / (g + 1) >= 4 * d.S) ++g;
+    int len = (d.V + g - 1) / g;
+    len = (len + vec - 1) / vec * vec;
+    *G = g;
+    *seg_len = len;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* rheo_last_error(void) { return g_err.c_str(); }
+
+int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
+    if (!cfg_in || !out) return fail(RHEO_EINVAL, "NULL argument");
+    rheo_config c = *cfg_in;
+    if (c.n_expand == 0) c.n_expand = c.pool;
+    if (c.eps_m0 == 0.0) c.eps_m0 = std::ldexp(1.0, -40);
+    if (c.batch < 1) return fail(RHEO_EINVAL, "batch must be >= 1");
+    if (c.vocab < 2 || c.vocab > kMaxV) return fail(RHEO_EINVAL, "vocab must be in [2, %d]", kMaxV);
+    if (c.pool < 1 || c.pool > 15) return fail(RHEO_EINVAL, "pool K must be in [1, 15]");
+    if (c.leads < 0 || c.leads > c.pool - 1) return fail(RHEO_EINVAL, "leads m must be in [0, K-1]");
+    if (c.depth < 1 || c.depth > 15) return fail(RHEO_EINVAL, "depth must be in [1, 15]");
+    if (c.n_expand < 1 || c.n_expand > c.pool) return fail(RHEO_EINVAL, "n_expand must be in [1, K]");
+    if (c.dtype != RHEO_F32 && c.dtype != RHEO_BF16) return fail(RHEO_EINVAL, "unknown dtype");
+    if (c.reserved != 0) return fail(RHEO_EINVAL, "reserved field must be 0");
+    if (c.support <= 0) return fail(RHEO_EINVAL, "support S must be >= K (dense mode is not available)");
+    const int S = c.support < c.vocab ? c.support : c.vocab;
+    if (S < c.pool) return fail(RHEO_EINVAL, "support must be >= pool K");
+    if (S > 1024) return fail(RHEO_EINVAL, "support must be <= 1024");
+    if (S <= c.leads) return fail(RHEO_EINVAL, "support must exceed leads m");
+    if (c.row_stride < c.vocab) return fail(RHEO_EINVAL, "row_stride must be >= vocab");
+    const int esz = c.dtype == RHEO_BF16 ? 2 : 4;
+    if ((c.row_stride * esz) % 16) return fail(RHEO_EINVAL, "row_stride must be a multiple of 16 bytes");
+    if (!(c.eps_m0 > 0.0) || !std::isfinite(c.eps_m0)) return fail(RHEO_EINVAL, "eps_m0 must be > 0");
+
+    rheo_tree* t = new rheo_tree();
+    t->cfg = c;
+    TreeDev& d = t->dev;
+    d.B = c.batch; d.V = c.vocab; d.K = c.pool; d.m = c.leads; d.D = c.depth;
+    d.NE = c.n_expand; d.S = S; d.dtype = c.dtype; d.stride = c.row_stride;
+    d.eps = c.eps_m0;
+    d.NN = 1 + c.pool + (c.depth - 1) * c.n_expand * c.pool;
+    d.E = 1 + (c.depth - 1) * c.n_expand;
+    if (2 * 8 * (size_t)(d.NN - 1) > 64 * 1024) {
+        delete t;
+        return fail(RHEO_EINVAL, "tree too large (%d nodes per sequence)", d.NN);
+    }
+    const char* env = getenv("RHEO_EXPAND_VARIANT");
+    t->variant = env ? atoi(env) : 0;
+    if (t->variant < 0 || t->variant >= expand_variant_count(c.dtype)) t->variant = 0;
+    env = getenv("RHEO_EXPAND_MIN_BLOCKS");
+    if (env) t->min_blocks = atoi(env);
+
+    const size_t B = d.B, NN = d.NN, E = d.E;
+    const size_t rows_max = B * (size_t)d.NE;
+    int rc = RHEO_OK;
+    rc = rc ? rc : dalloc(t, &d.tok, B * NN);
+    rc = rc ? rc : dalloc(t, &d.par, B * NN);
+    rc = rc ? rc : dalloc(t, &d.meta, B * NN);
+    rc = rc ? rc : dalloc(t, &d.proxy, B * NN);
+    rc = rc ? rc : dalloc(t, &d.qtrue, B * NN);
+    rc = rc ? rc : dalloc(t, &d.score, B * NN);
+    rc = rc ? rc : dalloc(t, &d.path, B * NN);
+    rc = rc ? rc : dalloc(t, &d.first_child, B * NN);
+    rc = rc ? rc : dalloc(t, &d.exp_of, B * NN);
+    rc = rc ? rc : dalloc(t, &d.tail_id, B * E * S);
+    rc = rc ? rc : dalloc(t, &d.tail_q, B * E * S);
+    rc = rc ? rc : dalloc(t, &d.zq, B * E);
+    rc = rc ? rc : dalloc(t, &d.frontier, B * d.NE);
+    rc = rc ? rc : dalloc(t, &d.fr_parent, B * d.NE);
+    rc = rc ? rc : dalloc(t, &d.fr_token, B * d.NE);
+    rc = rc ? rc : dalloc(t, &d.pidx, B * NN);
+    rc = rc ? rc : dalloc(t, &d.porder, B * NN);
+    rc = rc ? rc : dalloc(t, &d.seg_keys, rows_max * (kCap / S) * S);
+    rc = rc ? rc : dalloc(t, &d.row_cnt, rows_max);
+    rc = rc ? rc : dalloc(t, &d.seq_cnt, B);
+    rc = rc ? rc : dalloc(t, &d.err, 1);
+    if (rc) {
+        free_all(t);
+        delete t;
+        return rc;
+    }
+    hipError_t e = hipMemset(d.row_cnt, 0, rows_max * sizeof(uint32_t));
+    if (e == hipSuccess) e = hipMemset(d.seq_cnt, 0, B * sizeof(uint32_t));
+    if (e == hipSuccess) e = hipMemset(d.err, 0, sizeof(int32_t));
+    if (e == hipSuccess) e = hipMemset(d.pidx, 0xFF, B * NN * sizeof(int32_t));
+    if (e == hipSuccess) e = hipMemset(d.frontier, 0, B * d.NE * sizeof(int32_t));
+    if (e == hipSuccess) e = hipMemset(d.first_child, 0xFF, B * NN * sizeof(int32_t));
+    if (e == hipSuccess) e = hipDeviceSynchronize();
+    if (e != hipSuccess) {
+        free_all(t);
+        delete t;
+        return hip_fail(e, "initialising tree state");
+    }
+    *out = t;
+    return RHEO_OK;
+}
+
+int rheo_destroy(rheo_tree* t) {
+    if (!t) return RHEO_OK;
+    (void)hipDeviceSynchronize();
+    free_all(t);
+    delete t;
+    return RHEO_OK;
+}
+
+int32_t rheo_node_count(const rheo_tree* t) { return t ? t->dev.NN : 0; }
+
+int rheo_begin_step(rheo_tree* t) {
+    if (!t) return fail(RHEO_EINVAL, "NULL tree");
+    t->state = EXPANDING;
+    t->level = 0;
+    t->R = 0;
+    return RHEO_OK;
+}
+
+int rheo_expand_level(rheo_tree* t, const void* logits, float T, uint64_t key, void* stream) {
+    if (!t) return fail(RHEO_EINVAL, "NULL tree");
+    if (t->state != EXPANDING) return fail(RHEO_ESTATE, "rheo_expand_level needs rheo_begin_step first");
+    int rc = check_ptr(logits, "draft_logits");
+    if (rc) return rc;
+    if ((rc = check_T(T))) return rc;
+    LevelArgs a;
+    a.logits = logits;
+    a.level = t->level;
+    a.P = t->level == 0 ? 1 : t->dev.NE;
+    level_shape(t, t->dev.B * a.P, &a.G, &a.seg_len);
+    a.k1 = k_of_T(t->cfg.construct_tempered ? T : 1.0f);
+    a.kT = k_of_T(T);
+    a.rng_key = key;
+    const hipError_t e = launch_expand(t->dev, a, t->variant, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "expand launch");
+    t->T_expand = T;
+    if (++t->level == t->dev.D) t->state = EXPANDED;
+    return RHEO_OK;
+}
+
+int rheo_frontier(rheo_tree* t, int32_t* parent_index, int32_t* token, void* stream) {
+    if (!t) return fail(RHEO_EINVAL, "NULL tree");
+    if (t->state != EXPANDING || t->level < 1)
+        return fail(RHEO_ESTATE, "no frontier: expand a level below the last first");
+    const size_t n = (size_t)t->dev.B * t->dev.NE * sizeof(int32_t);
+    hipError_t e = hipSuccess;
+    if (parent_index)
+        e = hipMemcpyAsync(parent_index, t->dev.fr_parent, n, hipMemcpyDeviceToDevice, (hipStream_t)stream);
+    if (e == hipSuccess && token)
+        e = hipMemcpyAsync(token, t->dev.fr_token, n, hipMemcpyDeviceToDevice, (hipStream_t)stream);
+    return e == hipSuccess ? RHEO_OK : hip_fail(e, "frontier copy");
+}
+
+int rheo_prune(rheo_tree* t, int32_t R, void* stream) {
+    if (!t) return fail(RHEO_EINVAL, "NULL tree");
+    if (t->state != EXPANDED) return fail(RHEO_ESTATE, "rheo_prune needs all depth levels expanded");
+    if (R < 1 || R > t->dev.NN - 1) return fail(RHEO_EINVAL, "budget must be in [1, %d]", t->dev.NN - 1);
+    const hipError_t e = launch_prune(t->dev, R, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "prune launch");
+    t->R = R;
+    t->state = PRUNED;
+    return RHEO_OK;
+}
+
+int rheo_pruned_view(rheo_tree* t, int32_t* parent, int32_t* token, void* stream) {
+    if (!t) return fail(RHEO_EINVAL, "NULL tree");
+    if (t->state != PRUNED && t->state != VERIFIED) return fail(RHEO_ESTATE, "no pruned tree");
+    const hipError_t e = launch_pruned_view(t->dev, t->R, parent, token, (hipStream_t)stream);
+    return e == hipSuccess ? RHEO_OK : hip_fail(e, "pruned view launch");
+}
+
+int rheo_verify(rheo_tree* t, const void* logits, float T, uint64_t key, int32_t* accepted,
+                int32_t* accept_len, int32_t* final_token, void* stream) {
+    if (!t) return fail(RHEO_EINVAL, "NULL tree");
+    if (t->state != PRUNED) return fail(RHEO_ESTATE, "rheo_verify needs rheo_prune first");
+    int rc = check_ptr(logits, "target_logits");
+    if (rc) return rc;
+    if ((rc = check_T(T))) return rc;
+    if (!accepted || !accept_len || !final_token) return fail(RHEO_EINVAL, "NULL output");
+    VerifyArgs a;
+    a.logits = logits;
+    a.R = t->R;
+    a.kT = k_of_T(T);
+    a.rng_key = key;
+    a.accepted = accepted;
+    a.accept_len = accept_len;
+    a.final_token = final_token;
+    const hipError_t e = launch_verify(t->dev, a, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "verify launch");
+    t->state = VERIFIED;
+    return RHEO_OK;
+}
+
+int rheo_read_nodes(rheo_tree* t, int32_t* token, int32_t* parent, int32_t* depth, int32_t* slot,
+                    int32_t* kind, double* proxy, double* qtrue, double* score, void* stream) {
+    if (!t) return fail(RHEO_EINVAL, "NULL tree");
+    if (t->state == CREATED || (t->state == EXPANDING && t->level == 0))
+        return fail(RHEO_ESTATE, "no tree built in this step");
+    const hipError_t e = launch_read_nodes(t->dev, token, parent, depth, slot, kind, proxy, qtrue,
+                                           score, (hipStream_t)stream);
+    return e == hipSuccess ? RHEO_OK : hip_fail(e, "read_nodes launch");
+}
+
+int rheo_device_error(rheo_tree* t, int32_t* host_flag) {
+    if (!t || !host_flag) return fail(RHEO_EINVAL, "NULL argument");
+    hipError_t e = hipDeviceSynchronize();
+    if (e == hipSuccess) e = hipMemcpy(host_flag, t->dev.err, sizeof(int32_t), hipMemcpyDeviceToHost);
+    return e == hipSuccess ? RHEO_OK : hip_fail(e, "reading the device error flag");
+}
+
+}  // extern "C"

@@ -1,0 +1,175 @@
+// Device-side building blocks of the RheoSampling hot path (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace rheo {
+
+typedef unsigned __int128 u128;
+
+constexpr int WAVE = 64;
+
+enum Kind { LEAD = 0, SAMPLED = 1, FILL = 2 };
+enum Purpose { P_DRAFT = 1, P_VERIFY = 2, P_FINAL = 3 };
+
+// ---------------------------------------------------------------------------
+// Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds of two
+// 64x64->128 multiplies with the round multipliers, the high halves xored
+// into the odd words with the key, key bumped by the Weyl constants.
+// ---------------------------------------------------------------------------
+__device__ inline uint64_t philox_draw(uint64_t key, uint64_t purpose,
+                                       uint64_t seq, uint64_t index) {
+    uint64_t x0 = index, x1 = seq, x2 = purpose, x3 = 0;
+    uint64_t k0 = key, k1 = 0;
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        if (r) {
+            k0 += 0x9E3779B97F4A7C15ull;
+            k1 += 0xBB67AE8584CAA73Bull;
+        }
+        const uint64_t lo0 = 0xD2E7470EE14C6C93ull * x0;
+        const uint64_t hi0 = __umul64hi(0xD2E7470EE14C6C93ull, x0);
+        const uint64_t lo1 = 0xCA5A826395121157ull * x2;
+        const uint64_t hi1 = __umul64hi(0xCA5A826395121157ull, x2);
+        const uint64_t n0 = hi1 ^ x1 ^ k0;
+        const uint64_t n2 = hi0 ^ x3 ^ k1;
+        x0 = n0; x1 = lo1; x2 = n2; x3 = lo0;
+    }
+    return x0;
+}
+
+// ---------------------------------------------------------------------------
+// Canonical integer weight of a logit: floor(2^30 * 2^t) with
+// t = fl(fl(l - ref) * kT), kT = fl32(log2(e) / T), t clamped to <= 0 and
+// weight 0 below t = -31.  2^t = 2^n * P(f), n = rint(t), f = t - n, P the
+// degree-6 Taylor polynomial of 2^f with coefficients (ln 2)^k / k! * 2^30
+// rounded to fp32, evaluated in Horner form with separately rounded
+// products and sums.  Result: (uint32)(2^30 P) >> -n.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint32_t cweight(float l, float ref, float kT) {
+    float t = __fmul_rn(__fsub_rn(l, ref), kT);
+    t = fminf(t, 0.0f);
+    if (t < -31.0f) return 0u;
+    const float n = rintf(t);
+    const float f = __fsub_rn(t, n);
+    float p = 0x1.430912p+17f;
+    p = __fadd_rn(__fmul_rn(p, f), 0x1.5d87fep+20f);
+    p = __fadd_rn(__fmul_rn(p, f), 0x1.3b2ab6p+23f);
+    p = __fadd_rn(__fmul_rn(p, f), 0x1.c6b08ep+25f);
+    p = __fadd_rn(__fmul_rn(p, f), 0x1.ebfbe0p+27f);
+    p = __fadd_rn(__fmul_rn(p, f), 0x1.62e430p+29f);
+    p = __fadd_rn(__fmul_rn(p, f), 0x1.000000p+30f);
+    const uint32_t u = (uint32_t)p;
+    return u >> (uint32_t)(-(int)n);
+}
+
+// Order-preserving map of an fp32 value to uint32 (-0 folded onto +0).
+__device__ __forceinline__ uint32_t ord32(float f) {
+    uint32_t b = __float_as_uint(f);
+    if (b == 0x80000000u) b = 0u;
+    return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+__device__ __forceinline__ float unord32(uint32_t k) {
+    const uint32_t b = (k & 0x80000000u) ? (k & 0x7fffffffu) : ~k;
+    return __uint_as_float(b);
+}
+// Selection key of a logit: larger key = (larger logit, then smaller id).
+__device__ __forceinline__ uint64_t logit_key(float v, uint32_t id) {
+    return ((uint64_t)ord32(v) << 32) | (uint64_t)(0xFFFFFFFFu - id);
+}
+__device__ __forceinline__ float key_value(uint64_t k) { return unord32((uint32_t)(k >> 32)); }
+__device__ __forceinline__ int key_id(uint64_t k) { return (int)(0xFFFFFFFFu - (uint32_t)k); }
+
+// Priority of a tree node (App. C.1): score descending, depth ascending,
+// slot path ascending -- as a 128-bit key where larger = better.  Scores
+// are non-negative, so their IEEE bits are already order-preserving.
+__device__ __forceinline__ void prio_key(double score, int depth, uint64_t path,
+                                         uint64_t& hi, uint64_t& lo) {
+    hi = (uint64_t)__double_as_longlong(score);
+    lo = ((uint64_t)(15 - depth) << 60) | (0x0FFFFFFFFFFFFFFFull - path);
+}
+
+// bf16 pairs packed in a uint32: low and high element as fp32 (exact).
+__device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// High 128 bits of a (64 x 128)-bit product, b < 2^96.
+__device__ __forceinline__ u128 mulhi_64x128(uint64_t a, u128 b) {
+    const uint64_t blo = (uint64_t)b;
+    const uint64_t bhi = (uint64_t)(b >> 64);
+    const u128 plo = (u128)a * blo;
+    return (u128)a * bhi + (plo >> 64);
+}
+
+// ---------------------------------------------------------------------------
+// wave / block reductions (wave64)
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+    return v;
+}
+__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    return v;
+}
+__device__ __forceinline__ int wave_sum_i32(int v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    return v;
+}
+
+template <int NT>
+__device__ float block_max(float v, float* sh) {
+    v = wave_max(v);
+    const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE;
+    __syncthreads();
+    if (l == 0) sh[w] = v;
+    __syncthreads();
+    float r = sh[0];
+#pragma unroll
+    for (int i = 1; i < NT / WAVE; ++i) r = fmaxf(r, sh[i]);
+    return r;
+}
+
+template <int NT>
+__device__ uint64_t block_sum_u64(uint64_t v, uint64_t* sh) {
+    v = wave_sum_u64(v);
+    const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE;
+    __syncthreads();
+    if (l == 0) sh[w] = v;
+    __syncthreads();
+    uint64_t r = 0;
+#pragma unroll
+    for (int i = 0; i < NT / WAVE; ++i) r += sh[i];
+    return r;
+}
+
+template <int NT>
+__device__ int block_sum_i32(int v, int* sh) {
+    v = wave_sum_i32(v);
+    const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE;
+    __syncthreads();
+    if (l == 0) sh[w] = v;
+    __syncthreads();
+    int r = 0;
+#pragma unroll
+    for (int i = 0; i < NT / WAVE; ++i) r += sh[i];
+    return r;
+}
+
+// Exclusive prefix of v over the wave (lane order).
+__device__ __forceinline__ int wave_excl_scan(int v) {
+    const int l = threadIdx.x % WAVE;
+    int x = v;
+#pragma unroll
+    for (int o = 1; o < WAVE; o <<= 1) {
+        const int y = __shfl_up(x, o);
+        if (l >= o) x += y;
+    }
+    return x - v;
+}
+
+}  // namespace rheo

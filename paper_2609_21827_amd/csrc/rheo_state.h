@@ -1,0 +1,86 @@
+// Device state of one tree handle and the kernel launch entry points.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace rheo {
+
+// Everything a kernel needs to find the tree arrays.  Node arrays are
+// [B][NN] in uid order (uid 0 = root); expanded-node arrays are [B][E] with
+// expanded index e = 0 for the root and 1 + (d-1) * NE + j for frontier
+// node j of level d >= 1.
+struct TreeDev {
+    int B, V, K, m, D, NE, S;      // S = effective support (min(S, V))
+    int NN, E;                      // nodes / expanded nodes per sequence
+    int dtype;
+    int64_t stride;
+    double eps;
+    // unpruned tree, [B][NN]
+    int32_t* tok;
+    int32_t* par;
+    int32_t* meta;                 // depth | slot << 8 | kind << 16
+    double* proxy;
+    double* qtrue;
+    double* score;
+    uint64_t* path;                // slot path, 4 bits per level from bit 59 down
+    int32_t* first_child;          // uid of slot-1 child, -1 if not expanded
+    int32_t* exp_of;               // expanded index, -1 if not expanded
+    // truncated tail distribution q~ of each expanded node, sorted by id
+    int32_t* tail_id;              // [B][E][S]
+    uint32_t* tail_q;              // [B][E][S]
+    uint64_t* zq;                  // [B][E]
+    // frontier of the last expanded level, [B][NE]
+    int32_t* frontier;
+    int32_t* fr_parent;
+    int32_t* fr_token;
+    // pruned tree
+    int32_t* pidx;                 // [B][NN]: pruned index, -1 if pruned away
+    int32_t* porder;               // [B][NN]: uid of each pruned index
+    // in-kernel coordination and scratch
+    uint64_t* seg_keys;            // [rows][G][S] segment selections
+    uint32_t* row_cnt;             // [rows] arrival counters
+    uint32_t* seq_cnt;             // [B] arrival counters
+    int32_t* err;                  // sticky device error flag
+};
+
+struct LevelArgs {
+    const void* logits;
+    int level;                     // 0..D-1
+    int P;                         // parents per sequence at this level
+    int G;                         // segments per row
+    int seg_len;                   // elements per segment (multiple of 8)
+    float k1;                      // construction kT (untempered unless asked)
+    float kT;                      // sampling kT
+    uint64_t rng_key;
+};
+
+struct VerifyArgs {
+    const void* logits;
+    int R;
+    float kT;
+    uint64_t rng_key;
+    int32_t* accepted;
+    int32_t* accept_len;
+    int32_t* final_token;
+};
+
+hipError_t launch_expand(const TreeDev& t, const LevelArgs& a, int variant,
+                         hipStream_t s);
+hipError_t launch_prune(const TreeDev& t, int R, hipStream_t s);
+hipError_t launch_verify(const TreeDev& t, const VerifyArgs& a, hipStream_t s);
+
+// expand kernel variants: elements per thread x threads per block
+struct ExpandVariant { int nt, ept; };
+int expand_variant_count(int dtype);
+ExpandVariant expand_variant(int dtype, int v);
+
+}  // namespace rheo
+
+namespace rheo {
+hipError_t launch_read_nodes(const TreeDev& t, int32_t* token, int32_t* parent,
+                             int32_t* depth, int32_t* slot, int32_t* kind, double* proxy,
+                             double* qtrue, double* score, hipStream_t s);
+hipError_t launch_pruned_view(const TreeDev& t, int R, int32_t* parent, int32_t* token,
+                              hipStream_t s);
+}  // namespace rheo

@@ -19,6 +19,8 @@ fp32 row):
           token order) and s = 1.1
   zipf_t3 as zipf with Student-t(3) noise; 5% of nodes get +12 on one keyed
           token (near one-hot peaks)
+  flat    all logits 0 (uniform distributions; every comparison a tie)
+  quantum > 0 rounds every logit to a multiple of it (massive ties)
   target  = draft row of the same node + sigma_t * N'_v (an independent
           noise stream of the same node key), rounded like the draft
 Noise variates come from 65536-entry quantile tables indexed by a 16-bit
@@ -66,6 +68,7 @@ class Workload:
     sigma: float = 1.5          # draft noise scale (zipf recipes)
     sigma_t: float = 0.7        # target divergence (fixed)
     sigma_t_range: tuple = None  # per-sequence U(lo, hi) divergence
+    quantum: float = 0.0        # > 0: logits rounded to multiples of it (ties)
     seed: int = 0x5EED0000
     n_expand: int = None
     construct_tempered: bool = False
@@ -213,10 +216,19 @@ def _perm_params(keys, V):
     return a_s, c_s
 
 
+def _quantise(w, rows):
+    if w.quantum:
+        q = float(w.quantum)
+        return torch.round(rows * (1.0 / q)) * q
+    return rows
+
+
 def _draft_fp32(w, keys, device):
     """fp32 draft rows for node keys (before dtype rounding)."""
     normal, t3 = _tables(device)
     V = w.V
+    if w.recipe == "flat":
+        return torch.zeros((len(keys), V), dtype=torch.float32, device=device)
     v = torch.arange(V, dtype=torch.int64, device=device).view(1, -1)
     lo, hi = _key_words(keys, 0x1111, device)
     idx = _noise_index(lo, hi, v)
@@ -250,7 +262,7 @@ def draft_rows(w, keys, device="cpu", chunk=256):
     """Draft logits [len(keys), V] for the given node keys."""
     out = []
     for i in range(0, len(keys), chunk):
-        out.append(_round(w, _draft_fp32(w, keys[i:i + chunk], device)))
+        out.append(_round(w, _quantise(w, _draft_fp32(w, keys[i:i + chunk], device))))
     return torch.cat(out, 0) if out else torch.empty(
         (0, w.V), dtype=torch.bfloat16 if w.dtype == "bf16" else torch.float32,
         device=device)
@@ -269,7 +281,10 @@ def target_rows(w, keys, sigmas, device="cpu", chunk=256):
         idx = _noise_index(lo, hi, v)
         sg = torch.tensor([np.float32(s) for s in sigmas[i:i + chunk]],
                           dtype=torch.float32, device=device).view(-1, 1)
-        out.append(_round(w, base + normal[idx] * sg))
+        if w.recipe == "flat":
+            out.append(_round(w, base))
+        else:
+            out.append(_round(w, _quantise(w, base + normal[idx] * sg)))
     return torch.cat(out, 0)
 
 

@@ -1,0 +1,181 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Both sides see the same seeded synthetic logits (``synth``), generated from
+the node path keys each side derives from its *own* tree, so a divergence
+anywhere shows up as different rows as well as different records.  The bar
+(set by the target): tree topology, token ids, slot kinds, pruned set,
+accepted tokens and final tokens bit-exact; probabilities within 1e-5
+relative -- they are in fact compared bit-exactly, since both sides evaluate
+the same fp32 / integer / correctly rounded fp64 operation sequence.
+"""
+
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle.harness import node_table, oracle_step
+
+pytestmark = pytest.mark.gpu
+
+INT_FIELDS = ("token", "parent", "depth", "slot", "kind")
+FP_FIELDS = ("proxy", "qtrue", "score")
+
+
+@pytest.fixture(scope="module")
+def dev():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2609_21827_amd import binding
+    binding.load_library()
+    return "cuda"
+
+
+def _check_seq(w, tree_nodes, ppar, ptok, acc, alen, fin, b, step, T):
+    print(f"  oracle {w.name} b={b} step={step} T={T}", flush=True)
+    nodes, pt, oacc, ou = oracle_step(w, b, step, T=T)
+    tab = node_table(nodes)
+    for k in INT_FIELDS:
+        got = tree_nodes[k][b]
+        assert np.array_equal(got, tab[k]), (k, b, np.nonzero(got != tab[k])[0][:10])
+    for k in FP_FIELDS:
+        got = tree_nodes[k][b]
+        want = tab[k]
+        rel = np.abs(got - want) / np.maximum(np.abs(want), 1e-300)
+        assert np.all(rel <= 1e-5), (k, b, float(rel.max()))
+        assert np.array_equal(got, want), (k, b, float(rel.max()))
+    R = len(pt.order) - 1
+    assert list(ptok[b][:R + 1]) == [-1] + [nodes[u].token for u in pt.order[1:]]
+    assert list(ppar[b][:R + 1]) == list(pt.parent)
+    n = int(alen[b])
+    assert list(acc[b][:n]) == list(oacc), (b, list(acc[b][:n]), oacc)
+    assert all(x == -1 for x in acc[b][n:])
+    assert int(fin[b]) == ou
+
+
+def run_parity(w, steps, seqs, T=None, dev="cuda", tree_kw=None):
+    from paper_2609_21827_amd.driver import make_tree, run_step
+    T = w.T if T is None else T
+    tree = make_tree(w, device=dev, **(tree_kw or {}))
+    try:
+        for step in steps:
+            print(f"gpu step {w.name} step={step} T={T}", flush=True)
+            acc, alen, fin = run_step(tree, w, step, T=T, device=dev)
+            nodes = {k: v.cpu().numpy() for k, v in tree.read_nodes().items()}
+            ppar, ptok = (x.cpu().numpy() for x in tree.pruned_view())
+            torch.cuda.synchronize()
+            assert tree.device_error() == 0
+            for b in seqs:
+                _check_seq(w, nodes, ppar, ptok, acc.numpy(), alen.numpy(), fin.numpy(),
+                           b, step, T)
+    finally:
+        tree.close()
+
+
+W = synth.WORKLOADS
+
+
+def test_tiny_many_steps(dev):
+    run_parity(W["tiny"], range(120), [0], dev=dev)
+
+
+@pytest.mark.parametrize("over", [
+    dict(m=0), dict(m=2), dict(K=1, m=0, R=3), dict(depth=1, R=3), dict(R=1), dict(R=21),
+    dict(construct_tempered=True, T=0.6), dict(T=2.0), dict(n_expand=2, R=7),
+    dict(B=3), dict(eps_m0=2.0 ** -20, m=0),
+])
+def test_tiny_variants(dev, over):
+    w = W["tiny"].with_(**over)
+    run_parity(w, range(25), list(range(w.B)), dev=dev)
+
+
+@pytest.mark.parametrize("over", [
+    dict(V=1001, dtype="f32", recipe="zipf", support=128, K=5, depth=4, R=20),
+    dict(V=1003, dtype="bf16", recipe="zipf", support=128, K=5, depth=4, R=20),
+    dict(V=200, dtype="bf16", recipe="zipf", support=1024, K=6, depth=3, R=15),
+    dict(V=300, dtype="bf16", recipe="flat", support=128, K=4, depth=3, R=12),
+    dict(V=5000, dtype="bf16", recipe="zipf", quantum=0.5, support=128, K=4, depth=3, R=12),
+    dict(V=32000, dtype="f32", recipe="zipf", support=1024, K=8, depth=3, R=30),
+    dict(V=4099, dtype="f32", recipe="zipf_t3", support=64, K=6, depth=5, R=40, B=2),
+])
+def test_edge_shapes(dev, over):
+    w = W["tiny"].with_(name="edge", sigma=1.5, sigma_t=0.8, **over)
+    tree_kw = {}
+    if w.V % 8:
+        tree_kw["row_stride"] = (w.V + 7) // 8 * 8
+    run_parity(w, range(3), list(range(w.B)), dev=dev, tree_kw=tree_kw)
+
+
+def test_llama2(dev):
+    run_parity(W["llama2"], range(3), [0], dev=dev)
+
+
+@pytest.mark.parametrize("T", [0.6, 1.0])
+def test_llama3_sparse(dev, T):
+    run_parity(W["llama3"], range(2), [0], T=T, dev=dev)
+
+
+def test_batched(dev):
+    run_parity(W["batched"], [0], [0, 17, 42, 63], dev=dev)
+
+
+def test_large(dev):
+    run_parity(W["large"], [0], [0, 77, 127], dev=dev)
+
+
+def test_headline(dev):
+    run_parity(W["headline"], [0, 1], [0, 31, 63], dev=dev)
+
+
+def test_launch_shape_independence(dev):
+    """Results do not depend on how rows are split into segments."""
+    from paper_2609_21827_amd.driver import make_tree, run_step
+    w = W["llama3"].with_(B=4)
+    outs = []
+    for variant, minb in (("0", "1"), ("0", "4096"), ("2", "64")):
+        os.environ["RHEO_EXPAND_VARIANT"] = variant
+        os.environ["RHEO_EXPAND_MIN_BLOCKS"] = minb
+        try:
+            tree = make_tree(w, device=dev)
+        finally:
+            del os.environ["RHEO_EXPAND_VARIANT"], os.environ["RHEO_EXPAND_MIN_BLOCKS"]
+        acc, alen, fin = run_step(tree, w, 0, device=dev)
+        nodes = tree.read_nodes()
+        outs.append((acc, alen, fin, {k: v.cpu() for k, v in nodes.items()}))
+        tree.close()
+    for o in outs[1:]:
+        assert torch.equal(o[0], outs[0][0]) and torch.equal(o[1], outs[0][1])
+        assert torch.equal(o[2], outs[0][2])
+        for k in o[3]:
+            assert torch.equal(o[3][k], outs[0][3][k]), k
+
+
+def test_step_order_enforced(dev):
+    from paper_2609_21827_amd.binding import RheoError, RHEO_ESTATE
+    from paper_2609_21827_amd.driver import make_tree
+    w = W["tiny"]
+    tree = make_tree(w, device=dev)
+    rows = torch.zeros((1, 1, w.V), dtype=torch.float32, device=dev)
+    with pytest.raises(RheoError) as e:
+        tree.expand_level(rows, 1.0, 1)
+    assert e.value.code == RHEO_ESTATE
+    tree.begin_step()
+    with pytest.raises(RheoError):
+        tree.prune(3)
+    with pytest.raises(RheoError):
+        tree.expand_level(rows, 0.0, 1)
+    tree.close()
+
+
+def test_generator_cpu_gpu_identical(dev):
+    for name in ("llama2", "large", "tiny"):
+        w = W[name]
+        keys = [synth.root_key(w, b, 3) for b in range(3)]
+        a = synth.draft_rows(w, keys, device="cpu")
+        g = synth.draft_rows(w, keys, device=dev).cpu()
+        assert torch.equal(a.view(torch.int16) if a.dtype == torch.bfloat16 else a,
+                           g.view(torch.int16) if g.dtype == torch.bfloat16 else g)
+        ta = synth.target_rows(w, keys, [0.9] * 3, device="cpu")
+        tg = synth.target_rows(w, keys, [0.9] * 3, device=dev).cpu()
+        assert torch.equal(ta.float(), tg.float())
