@@ -141,9 +141,26 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
         delete t;
         return fail(RHEO_EINVAL, "tree too large (%d nodes per sequence)", d.NN);
     }
+    // expand variant: the segments of a row must fit the candidate capacity
+    // of the merge (G * S <= kCap), so the segment capacity must reach V / G
+    const int gmax = kCap / S;
+    auto fits = [&](int v) {
+        const ExpandVariant ev = expand_variant(c.dtype, v);
+        return (int64_t)ev.nt * ev.ept * gmax >= c.vocab;
+    };
     const char* env = getenv("RHEO_EXPAND_VARIANT");
     t->variant = env ? atoi(env) : 0;
     if (t->variant < 0 || t->variant >= expand_variant_count(c.dtype)) t->variant = 0;
+    if (!fits(t->variant)) {
+        int best = -1;
+        for (int v = 0; v < expand_variant_count(c.dtype); ++v)
+            if (fits(v) && best < 0) best = v;
+        if (best < 0) {
+            delete t;
+            return fail(RHEO_EINVAL, "vocab %d too large for support %d", c.vocab, S);
+        }
+        t->variant = best;
+    }
     env = getenv("RHEO_EXPAND_MIN_BLOCKS");
     if (env) t->min_blocks = atoi(env);
 

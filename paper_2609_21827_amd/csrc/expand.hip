@@ -207,6 +207,10 @@ __global__ __launch_bounds__(NT) void k_expand(TreeDev t, LevelArgs a) {
     __syncthreads();
 
     // ---- merge the segments of the row ----------------------------------
+    if (a.G * S > CAP) {                 // excluded by the host's launch shape
+        if (tid == 0) atomicOr(t.err, 64);
+        return;
+    }
     if (a.G > 1) {
         uint64_t* out = t.seg_keys + ((int64_t)row * a.G + seg) * S;
         for (int i = tid; i < S; i += NT) out[i] = (i < ns) ? s_top[i] : 0ull;

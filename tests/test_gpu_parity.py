@@ -81,7 +81,7 @@ def test_tiny_many_steps(dev):
 
 
 @pytest.mark.parametrize("over", [
-    dict(m=0), dict(m=2), dict(K=1, m=0, R=3), dict(depth=1, R=3), dict(R=1), dict(R=21),
+    dict(m=0), dict(m=2), dict(K=1, m=0, R=3, n_expand=1), dict(depth=1, R=3), dict(R=1), dict(R=21),
     dict(construct_tempered=True, T=0.6), dict(T=2.0), dict(n_expand=2, R=7),
     dict(B=3), dict(eps_m0=2.0 ** -20, m=0),
 ])
