@@ -1,0 +1,200 @@
+"""Throughput of the RheoSampling hot path on one MI355X.
+
+A *step* is one full draft+verify pass of the tree machinery for a batch of
+B sequences: depth x rheo_expand_level, rheo_prune, rheo_verify (every row of
+the hot path) on synthetic logits that are already resident in HBM.
+
+Protocol
+  1. discovery: run_step() generates each level's draft rows from the
+     frontier the library picks and the target rows of the pruned tree, and
+     records them (several distinct steps, so the timed loop does not re-read
+     one step's rows from cache).
+  2. timed replay: W warm-up steps, then K steps of the library calls only,
+     cycling over the recorded steps, bracketed by torch.cuda.synchronize();
+     every replay must reproduce the discovery outputs bit for bit.
+  3. HIP events around each rheo_expand_level call (on the stream it launches
+     on) give the dominant kernel's average duration; its algorithmic bytes
+     are the draft rows it must read (rows x V x 2 bytes).
+  4. cpu_baseline: the CPU oracle timed on a bounded sample of the same
+     workload (one step of a few sequences, rows pre-generated).
+Prints one JSON line on stdout.
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "tree draft+verify steps/sec at V=128k batch 64; achieved HBM GB/s vs peak"
+PEAK_HBM_GBPS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="headline")
+    ap.add_argument("--distinct", type=int, default=4, help="recorded steps cycled over")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"))
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for {args.gpus}); "
+              "the hot path's multi-GPU sharding is a design, not a build", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import synth
+    from paper_2609_21827_amd.driver import make_tree, run_step
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = "cuda"
+    w = synth.WORKLOADS[args.workload]
+    esz = w.elem_bytes
+    tree = make_tree(w, device=dev)
+
+    # ---- 1. discovery ------------------------------------------------------
+    recs, outs = [], []
+    for s in range(args.distinct):
+        rec = {}
+        acc, alen, fin = run_step(tree, w, s, device=dev, record=rec)
+        recs.append(rec)
+        outs.append((acc, alen, fin))
+        log(f"discovery step {s}: mean accepted {alen.float().mean().item():.3f}")
+    torch.cuda.synchronize()
+    assert tree.device_error() == 0
+
+    stream = torch.cuda.current_stream()
+    out_bufs = [tuple(torch.empty_like(x, device=dev) for x in o) for o in outs]
+    fr_buf = tuple(torch.empty((w.B, w.n_expand), dtype=torch.int32, device=dev) for _ in range(2))
+    pv_buf = tuple(torch.empty((w.B, w.R + 1), dtype=torch.int32, device=dev) for _ in range(2))
+
+    def replay(i, events=None):
+        # the calls a serving loop makes: expand, frontier (which rows the
+        # draft model computes next), ..., prune, pruned view (which rows the
+        # target model computes), verify
+        rec = recs[i % len(recs)]
+        ob = out_bufs[i % len(recs)]
+        tree.begin_step()
+        for d, rows in enumerate(rec["draft"]):
+            if events is not None:
+                events[d][0].record(stream)
+            tree.expand_level(rows, rec["T"], rec["rng_key"], stream=stream)
+            if events is not None:
+                events[d][1].record(stream)
+            if d + 1 < w.depth:
+                tree.frontier(out=fr_buf, stream=stream)
+        tree.prune(w.R, stream=stream)
+        tree.pruned_view(out=pv_buf, stream=stream)
+        tree.verify(rec["target"], rec["T"], rec["rng_key"], out=ob, stream=stream)
+
+    # ---- 2. timed replay ---------------------------------------------------
+    for i in range(args.warmup):
+        replay(i)
+    torch.cuda.synchronize()
+    for i in range(len(recs)):
+        for a, b in zip(out_bufs[i], outs[i]):
+            assert torch.equal(a.cpu(), b), "replay differs from discovery"
+    ev = [[[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)]
+           for _ in range(w.depth)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        replay(i, ev[i])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms = (t1 - t0) * 1e3 / args.steps
+    steps_per_s = args.steps / (t1 - t0)
+
+    # algorithmic bytes: every draft row once, the target rows on each walk
+    rows_per_level = [w.B] + [w.B * w.n_expand] * (w.depth - 1)
+    draft_bytes = sum(rows_per_level) * w.V * esz
+    walk_rows = [int((o[1] + 1).sum()) for o in outs]
+    target_bytes = [r * w.V * esz for r in walk_rows]
+    step_bytes = [draft_bytes + tb for tb in target_bytes]
+    mean_step_bytes = sum(step_bytes[i % len(recs)] for i in range(args.steps)) / args.steps
+    tokens_per_step = sum(walk_rows) / len(walk_rows)
+
+    exp_ms = [[e[0].elapsed_time(e[1]) for e in ev[i]] for i in range(args.steps)]
+    tot_ms = sum(sum(x) for x in exp_ms)
+    n_launch = args.steps * w.depth
+    avg_launch_us = tot_ms * 1e3 / n_launch
+    bytes_per_launch = draft_bytes / w.depth
+    achieved = bytes_per_launch / (avg_launch_us * 1e-6) / 1e9
+    lvl_us = [sum(exp_ms[i][d] for i in range(args.steps)) * 1e3 / args.steps
+              for d in range(w.depth)]
+
+    traffic = None
+    if os.path.exists(args.traffic):
+        with open(args.traffic) as f:
+            tr = json.load(f)
+        if tr.get("workload") == w.name:
+            traffic = tr.get("bytes_per_launch")
+
+    # ---- 4. CPU oracle baseline --------------------------------------------
+    cpu = None
+    if not args.no_cpu:
+        from oracle.harness import oracle_step
+        cache = {}
+        seqs, t_cpu = 0, 0.0
+        budget = args.cpu_seconds
+        while t_cpu < budget and seqs < w.B:
+            oracle_step(w, seqs, 0, row_cache=cache)          # generate rows
+            c0 = time.perf_counter()
+            oracle_step(w, seqs, 0, row_cache=cache)          # timed: method only
+            t_cpu += time.perf_counter() - c0
+            seqs += 1
+        per_seq = t_cpu / seqs
+        cpu = {"value": 1.0 / (per_seq * w.B), "unit": "steps/s", "cores": 1,
+               "kind": "oracle",
+               "sample": f"{seqs} of {w.B} sequences of one {w.name} step "
+                         f"({t_cpu:.1f} s single-threaded, rows pre-generated), "
+                         f"scaled to the whole batch"}
+
+    res = {
+        "metric": METRIC,
+        "value": round(steps_per_s, 3),
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}: B={w.B} V={w.V} K={w.K} m={w.m} depth={w.depth} "
+                               f"budget={w.R} T={w.T} sparse top-{w.support} {w.dtype}",
+                   "batch": w.B, "vocab": w.V, "K": w.K, "m": w.m, "depth": w.depth,
+                   "budget": w.R, "T": w.T, "support": w.support},
+        "roofline": {"bound": "hbm", "kernel": "k_expand",
+                     "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS,
+                     "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4),
+                     "traffic": traffic,
+                     "avg_launch_us": round(avg_launch_us, 2),
+                     "bytes_per_launch": int(bytes_per_launch)},
+        "cpu_baseline": cpu,
+        "step_hbm_GBps": round(mean_step_bytes / (ms * 1e-3) / 1e9, 1),
+        "step_hbm_frac": round(mean_step_bytes / (ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
+        "tokens_per_s": round(steps_per_s * tokens_per_step, 1),
+        "mean_accept_len": round(tokens_per_step / w.B - 1, 4),
+        "expand_level_us": [round(x, 2) for x in lvl_us],
+    }
+    print(json.dumps(res), flush=True)
+    tree.close()
+
+
+if __name__ == "__main__":
+    main()

@@ -31,17 +31,24 @@ def node_key(nodes, uid, root):
     return key
 
 
-def oracle_step(w, b, step, T=None, trace=None, model="canonical", cfg=None):
+def oracle_step(w, b, step, T=None, trace=None, model="canonical", cfg=None,
+                row_cache=None):
     """One step of sequence ``b`` of workload ``w`` under the oracle.
-    Returns (nodes, pruned tree, accepted tokens, final token)."""
+    Returns (nodes, pruned tree, accepted tokens, final token).
+    ``row_cache`` (a dict) memoises generated rows by node key, so that a
+    second run times the method without the synthetic-input generation."""
     T = w.T if T is None else T
     cfg = cfg or tree_config(w, model=model)
     root = synth.root_key(w, b, step)
     sig = synth.seq_sigma_t(w, b)
 
+    cache = {} if row_cache is None else row_cache
+
     def draft_dist(node, nodes):
         key = node_key(nodes, node.uid, root)
-        row = synth.as_fp32_numpy(synth.draft_rows(w, [key]))[0]
+        if ("d", key) not in cache:
+            cache[("d", key)] = synth.as_fp32_numpy(synth.draft_rows(w, [key]))[0]
+        row = cache[("d", key)]
         return rheo.node_dist_from_logits(row, cfg.m, T, cfg.support,
                                           cfg.construct_tempered, model)
 
@@ -50,7 +57,9 @@ def oracle_step(w, b, step, T=None, trace=None, model="canonical", cfg=None):
     def target_P(i):
         nodes, pt = holder["nodes"], holder["pt"]
         key = node_key(nodes, pt.order[i], root)
-        row = synth.as_fp32_numpy(synth.target_rows(w, [key], [sig]))[0]
+        if ("t", key) not in cache:
+            cache[("t", key)] = synth.as_fp32_numpy(synth.target_rows(w, [key], [sig]))[0]
+        row = cache[("t", key)]
         return rheo.target_weights(row, T, model)
 
     def process():

@@ -131,9 +131,11 @@ class Tree:
         _check(_LIB.rheo_expand_level(self._h, _ptr(draft_logits), float(T),
                                       int(rng_key) & (2 ** 64 - 1), _stream(stream)))
 
-    def frontier(self, stream=None):
-        par = torch.empty((self.B, self.NE), dtype=torch.int32, device=self.device)
-        tok = torch.empty_like(par)
+    def frontier(self, out=None, stream=None):
+        if out is None:
+            out = (torch.empty((self.B, self.NE), dtype=torch.int32, device=self.device),
+                   torch.empty((self.B, self.NE), dtype=torch.int32, device=self.device))
+        par, tok = out
         _check(_LIB.rheo_frontier(self._h, _ptr(par), _ptr(tok), _stream(stream)))
         return par, tok
 
@@ -141,9 +143,11 @@ class Tree:
         _check(_LIB.rheo_prune(self._h, int(budget), _stream(stream)))
         self.R = int(budget)
 
-    def pruned_view(self, stream=None):
-        par = torch.empty((self.B, self.R + 1), dtype=torch.int32, device=self.device)
-        tok = torch.empty_like(par)
+    def pruned_view(self, out=None, stream=None):
+        if out is None:
+            out = (torch.empty((self.B, self.R + 1), dtype=torch.int32, device=self.device),
+                   torch.empty((self.B, self.R + 1), dtype=torch.int32, device=self.device))
+        par, tok = out
         _check(_LIB.rheo_pruned_view(self._h, _ptr(par), _ptr(tok), _stream(stream)))
         return par, tok
 

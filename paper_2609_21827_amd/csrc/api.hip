@@ -33,7 +33,6 @@ int hip_fail(hipError_t e, const char* what) {
 
 enum State { CREATED, EXPANDING, EXPANDED, PRUNED, VERIFIED };
 
-constexpr int kCap = 1024;       // candidate capacity of the expand kernel
 constexpr int kMaxV = 262143;
 
 float k_of_T(float T) { return (float)(1.4426950408889634 / (double)T); }
@@ -47,7 +46,8 @@ struct rheo_tree {
     int level = 0;
     int R = 0;
     int variant = 0;
-    int min_blocks = 1024;
+    int vG = 1, v_nv = 0, v_grid = 1;    // verification team shape
+    uint32_t verify_calls = 0;
     float T_expand = 1.0f;
     void* blocks[32] = {};
     int nblocks = 0;
@@ -81,23 +81,6 @@ int check_T(float T) {
     if (!(T > 0.0f) || !std::isfinite(T)) return fail(RHEO_EINVAL, "temperature must be finite and > 0");
     if (!std::isfinite(k_of_T(T))) return fail(RHEO_EINVAL, "temperature too small");
     return RHEO_OK;
-}
-
-// Segment layout of one level's expand launch.
-void level_shape(const rheo_tree* t, int rows, int* G, int* seg_len) {
-    const TreeDev& d = t->dev;
-    const ExpandVariant v = expand_variant(d.dtype, t->variant);
-    const int vec = d.dtype ? 8 : 4;
-    const int cap = v.nt * v.ept;
-    const int gmax = kCap / d.S;
-    int g = (d.V + cap - 1) / cap;
-    // more segments while the launch is small (fills the 256 compute units),
-    // keeping every segment at least 4 S elements long
-    while (g < gmax && rows * g < t->min_blocks && d.V / (g + 1) >= 4 * d.S) ++g;
-    int len = (d.V + g - 1) / g;
-    len = (len + vec - 1) / vec * vec;
-    *G = g;
-    *seg_len = len;
 }
 
 }  // namespace
@@ -141,31 +124,25 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
         delete t;
         return fail(RHEO_EINVAL, "tree too large (%d nodes per sequence)", d.NN);
     }
-    // expand variant: the segments of a row must fit the candidate capacity
-    // of the merge (G * S <= kCap), so the segment capacity must reach V / G
-    const int gmax = kCap / S;
-    auto fits = [&](int v) {
+    // expand variant: the smallest register footprint that holds a whole row
+    t->variant = -1;
+    for (int v = 0; v < expand_variant_count(c.dtype); ++v) {
         const ExpandVariant ev = expand_variant(c.dtype, v);
-        return (int64_t)ev.nt * ev.ept * gmax >= c.vocab;
-    };
-    const char* env = getenv("RHEO_EXPAND_VARIANT");
-    t->variant = env ? atoi(env) : 0;
-    if (t->variant < 0 || t->variant >= expand_variant_count(c.dtype)) t->variant = 0;
-    if (!fits(t->variant)) {
-        int best = -1;
-        for (int v = 0; v < expand_variant_count(c.dtype); ++v)
-            if (fits(v) && best < 0) best = v;
-        if (best < 0) {
-            delete t;
-            return fail(RHEO_EINVAL, "vocab %d too large for support %d", c.vocab, S);
+        if ((int64_t)ev.nt * ev.ept >= c.vocab) {
+            t->variant = v;
+            break;
         }
-        t->variant = best;
     }
-    env = getenv("RHEO_EXPAND_MIN_BLOCKS");
-    if (env) t->min_blocks = atoi(env);
-
+    if (t->variant < 0) {
+        delete t;
+        return fail(RHEO_EINVAL, "vocab %d exceeds the largest row the expand kernel holds", c.vocab);
+    }
+    const char* env = getenv("RHEO_EXPAND_VARIANT");
+    if (env) {
+        const int v = atoi(env);
+        if (v >= t->variant && v < expand_variant_count(c.dtype)) t->variant = v;
+    }
     const size_t B = d.B, NN = d.NN, E = d.E;
-    const size_t rows_max = B * (size_t)d.NE;
     int rc = RHEO_OK;
     rc = rc ? rc : dalloc(t, &d.tok, B * NN);
     rc = rc ? rc : dalloc(t, &d.par, B * NN);
@@ -184,18 +161,18 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
     rc = rc ? rc : dalloc(t, &d.fr_token, B * d.NE);
     rc = rc ? rc : dalloc(t, &d.pidx, B * NN);
     rc = rc ? rc : dalloc(t, &d.porder, B * NN);
-    rc = rc ? rc : dalloc(t, &d.seg_keys, rows_max * (kCap / S) * S);
-    rc = rc ? rc : dalloc(t, &d.row_cnt, rows_max);
-    rc = rc ? rc : dalloc(t, &d.seq_cnt, B);
     rc = rc ? rc : dalloc(t, &d.err, 1);
+    rc = rc ? rc : dalloc(t, &d.team_flag, B * 64);
+    rc = rc ? rc : dalloc(t, &d.team_max, B * 64);
+    rc = rc ? rc : dalloc(t, &d.team_chunk, B * 1024);
+    rc = rc ? rc : dalloc(t, &d.team_sp, B * (1024 + 16));
     if (rc) {
         free_all(t);
         delete t;
         return rc;
     }
-    hipError_t e = hipMemset(d.row_cnt, 0, rows_max * sizeof(uint32_t));
-    if (e == hipSuccess) e = hipMemset(d.seq_cnt, 0, B * sizeof(uint32_t));
-    if (e == hipSuccess) e = hipMemset(d.err, 0, sizeof(int32_t));
+    hipError_t e = hipMemset(d.err, 0, sizeof(int32_t));
+    if (e == hipSuccess) e = hipMemset(d.team_flag, 0, B * 64 * sizeof(uint32_t));
     if (e == hipSuccess) e = hipMemset(d.pidx, 0xFF, B * NN * sizeof(int32_t));
     if (e == hipSuccess) e = hipMemset(d.frontier, 0, B * d.NE * sizeof(int32_t));
     if (e == hipSuccess) e = hipMemset(d.first_child, 0xFF, B * NN * sizeof(int32_t));
@@ -204,6 +181,12 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
         free_all(t);
         delete t;
         return hip_fail(e, "initialising tree state");
+    }
+    e = verify_shape(d, &t->vG, &t->v_nv, &t->v_grid);
+    if (e != hipSuccess) {
+        free_all(t);
+        delete t;
+        return hip_fail(e, "no co-resident verification team shape for this tree");
     }
     *out = t;
     return RHEO_OK;
@@ -237,7 +220,6 @@ int rheo_expand_level(rheo_tree* t, const void* logits, float T, uint64_t key, v
     a.logits = logits;
     a.level = t->level;
     a.P = t->level == 0 ? 1 : t->dev.NE;
-    level_shape(t, t->dev.B * a.P, &a.G, &a.seg_len);
     a.k1 = k_of_T(t->cfg.construct_tempered ? T : 1.0f);
     a.kT = k_of_T(T);
     a.rng_key = key;
@@ -252,13 +234,13 @@ int rheo_frontier(rheo_tree* t, int32_t* parent_index, int32_t* token, void* str
     if (!t) return fail(RHEO_EINVAL, "NULL tree");
     if (t->state != EXPANDING || t->level < 1)
         return fail(RHEO_ESTATE, "no frontier: expand a level below the last first");
-    const size_t n = (size_t)t->dev.B * t->dev.NE * sizeof(int32_t);
-    hipError_t e = hipSuccess;
-    if (parent_index)
-        e = hipMemcpyAsync(parent_index, t->dev.fr_parent, n, hipMemcpyDeviceToDevice, (hipStream_t)stream);
-    if (e == hipSuccess && token)
-        e = hipMemcpyAsync(token, t->dev.fr_token, n, hipMemcpyDeviceToDevice, (hipStream_t)stream);
-    return e == hipSuccess ? RHEO_OK : hip_fail(e, "frontier copy");
+    TreeDev d = t->dev;
+    // write straight into the caller's buffers (NULL: tree-owned scratch)
+    if (parent_index) d.fr_parent = parent_index;
+    if (token) d.fr_token = token;
+    const int level = t->level - 1;
+    const hipError_t e = launch_frontier(d, level, level == 0 ? 1 : d.NE, (hipStream_t)stream);
+    return e == hipSuccess ? RHEO_OK : hip_fail(e, "frontier launch");
 }
 
 int rheo_prune(rheo_tree* t, int32_t R, void* stream) {
@@ -295,7 +277,17 @@ int rheo_verify(rheo_tree* t, const void* logits, float T, uint64_t key, int32_t
     a.accepted = accepted;
     a.accept_len = accept_len;
     a.final_token = final_token;
-    const hipError_t e = launch_verify(t->dev, a, (hipStream_t)stream);
+    a.G = t->vG;
+    // team barrier epochs grow across calls; the flags restart on wrap-around
+    if (++t->verify_calls >= (1u << 26)) {
+        t->verify_calls = 1;
+        const hipError_t e0 = hipMemsetAsync(t->dev.team_flag, 0,
+                                             (size_t)t->dev.B * 64 * sizeof(uint32_t),
+                                             (hipStream_t)stream);
+        if (e0 != hipSuccess) return hip_fail(e0, "resetting verification flags");
+    }
+    a.epoch = t->verify_calls * 64u;
+    const hipError_t e = launch_verify(t->dev, a, t->v_nv, t->v_grid, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "verify launch");
     t->state = VERIFIED;
     return RHEO_OK;

@@ -1,30 +1,34 @@
-// Level expansion of the draft tree: top-S selection over each draft-logit
-// row, the node's distributions, the hybrid candidate pool with its proxy and
-// true probabilities, and the next frontier.
+// Level expansion of the draft tree: parent selection, top-S selection over
+// each draft-logit row, the node's distributions, the hybrid candidate pool
+// with its proxy and true probabilities.
 //
-// One block handles one segment of one row (rows = B * P frontier nodes).
-// Phase 1 (every block): stream the segment once into registers with 16-byte
-// loads, take each thread's maximum, and use the S-th largest per-thread
-// maximum as a threshold: at least S elements reach it, so the segment's
-// top-S are all among the (typically ~1.2 S) elements at or above it.  They
-// are collected in LDS and ranked exactly by (logit desc, id asc).
-// Phase 2 (last block of a row): merge the segments' top-S, then build the
-// pool (Sec. 3.2; App. C.1) from the truncated distribution (Sec. 3.2,
-// sparse draft): construction weights q (untempered, Sec. 5.4), rank by
-// (q desc, id asc), tail q~_T = q_T / z on the support minus the top-m,
-// Y ~ q~_T by inverse CDF over token ids, fills, proxies
-// (min{q(x_m), z}; q(x_1) + eps for m = 0), true probability q~(Y), path
-// scores (App. C.1).
-// Phase 3 (last row of a sequence): the n_expand children with the highest
-// priority become the next frontier (Sec. 2.1; App. C.4 "expands exactly
-// the K nodes with highest path scores").
+// One 1024-thread block handles one frontier row (rows = B * P), so no
+// block ever waits for another:
+//  * prologue (level >= 1): the block's parent is the j-th best child of the
+//    previous level by priority (Sec. 2.1; App. C.4 "expands exactly the K
+//    nodes with highest path scores"); it is ranked from the children records
+//    the previous launch wrote, while the row loads are in flight.
+//  * the row is streamed once from HBM into registers with 16-byte loads;
+//    each thread keeps its maximum.  Every wave sorts its 64 maxima; with
+//    c = ceil(S / waves), the smallest of the waves' c-th largest maxima is a
+//    threshold that at least S elements reach, so the row's top-S (logit
+//    desc, id asc) are among the elements at or above it (typically ~1.3 S).
+//    They are collected in LDS and ranked exactly.
+//  * the pool (Sec. 3.2; App. C.1) from the truncated distribution (Sec.
+//    3.2, sparse draft): construction weights q (untempered, Sec. 5.4),
+//    ranks by (q desc, id asc), tail q~_T = q_T / z on the support minus the
+//    top-m, Y ~ q~_T by inverse CDF over token ids, fills, proxies
+//    (min{q(x_m), z}; q(x_1) + eps for m = 0), true probability q~(Y), path
+//    scores (App. C.1).  The tail is stored id-sorted for verification.
 #include "rheo_device.h"
 #include "rheo_state.h"
 
 namespace rheo {
 
-constexpr int CAP = 1024;    // LDS candidate capacity (keys)
+constexpr int NT = 1024;
+constexpr int CAP = 1024;    // LDS candidate capacity
 constexpr int SMAX = 1024;   // largest support
+constexpr int NWAVE = NT / WAVE;
 
 template <int DT>
 __device__ __forceinline__ float elem(const uint4& v, int k) {
@@ -33,104 +37,133 @@ __device__ __forceinline__ float elem(const uint4& v, int k) {
     return __uint_as_float(w[k]);
 }
 
-// Number of keys in keys[0..n) strictly greater than k.
-__device__ __forceinline__ int count_greater(const uint64_t* keys, int n, uint64_t k) {
-    int r = 0;
-    for (int j = 0; j < n; ++j) r += keys[j] > k;
-    return r;
-}
-
-template <int NT>
-__device__ void bitonic_desc(float* s) {
-    for (int k = 2; k <= NT; k <<= 1) {
-        for (int j = k >> 1; j > 0; j >>= 1) {
-            const int i = threadIdx.x;
-            const int p = i ^ j;
-            if (p > i) {
-                const float x = s[i], y = s[p];
-                const bool desc = (i & k) == 0;
-                if (desc ? (x < y) : (x > y)) { s[i] = y; s[p] = x; }
-            }
-            __syncthreads();
+// Vector vi (VEC consecutive elements) of a row; elements past V read as -inf.
+template <int DT>
+__device__ __forceinline__ uint4 load_row_vec(const char* base, int vi, int V) {
+    constexpr int VEC = DT ? 8 : 4;
+    constexpr int ESZ = DT ? 2 : 4;
+    const int e = vi * VEC;
+    if (e + VEC <= V) return load_stream16(base + (int64_t)e * ESZ);
+    uint32_t w[4];
+    if (DT) {
+        const uint16_t* p16 = (const uint16_t*)base;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int e0 = e + 2 * q;
+            const uint32_t lo = (e0 < V) ? p16[e0] : 0xFF80u;
+            const uint32_t hi = (e0 + 1 < V) ? p16[e0 + 1] : 0xFF80u;
+            w[q] = lo | (hi << 16);
         }
+    } else {
+        const uint32_t* p32 = (const uint32_t*)base;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) w[q] = (e + q < V) ? p32[e + q] : 0xFF800000u;
     }
+    return make_uint4(w[0], w[1], w[2], w[3]);
 }
 
-template <int DT, int NT, int EPT>
+// Hides the register-resident row from the optimiser between passes, so
+// each pass unpacks bf16 pairs on the fly instead of keeping every element
+// unpacked (which would exceed the register budget of a 1024-thread block).
+template <int NV>
+__device__ __forceinline__ void opaque(uint4 (&r)[NV]) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i)
+        asm volatile("" : "+v"(r[i].x), "+v"(r[i].y), "+v"(r[i].z), "+v"(r[i].w));
+}
+
+template <int DT, int NV>
 __global__ __launch_bounds__(NT) void k_expand(TreeDev t, LevelArgs a) {
     constexpr int VEC = DT ? 8 : 4;
-    constexpr int NV = EPT / VEC;
     constexpr int ESZ = DT ? 2 : 4;
-    static_assert(EPT % VEC == 0, "EPT must be a multiple of the vector width");
 
     __shared__ uint64_t s_keys[CAP];
     __shared__ uint64_t s_top[SMAX];
-    __shared__ float s_sort[NT];
     __shared__ uint32_t s_w1[SMAX];
     __shared__ uint32_t s_q[SMAX];
-    __shared__ int16_t s_xs[SMAX];
     __shared__ int16_t s_rank[SMAX];
-    __shared__ uint64_t s_red[NT / WAVE];
-    __shared__ int s_redi[NT / WAVE];
-    __shared__ int s_cnt, s_last, s_y;
+    __shared__ int16_t s_wr[SMAX];     // support item -> rank by construction weight
+    __shared__ int16_t s_xs[SMAX];     // rank by construction weight -> support item
+    __shared__ float s_tau[NWAVE];
+    __shared__ uint64_t s_red[NWAVE];
+    __shared__ int s_redi[NWAVE];
+    __shared__ int s_cnt, s_y, s_pu;
     __shared__ uint64_t s_t;
 
     const int tid = threadIdx.x;
-    const int lane = tid % WAVE;
-    const int row = blockIdx.x / a.G;
-    const int seg = blockIdx.x % a.G;
+    const int lane = tid % WAVE, wid = tid / WAVE;
+    const int row = blockIdx.x;
     const int b = row / a.P;
     const int j = row % a.P;
     const int V = t.V, S = t.S, K = t.K, m = t.m;
-    const int s0 = seg * a.seg_len;
-    const int s1 = min(V, s0 + a.seg_len);
-    const char* base = (const char*)a.logits + ((int64_t)row * t.stride + s0) * ESZ;
+    const int level = a.level;
+    const int NE = t.NE, NN = t.NN;
+    const int64_t nb = (int64_t)b * NN;
+    const char* base = (const char*)a.logits + (int64_t)row * t.stride * ESZ;
 
-    // ---- phase 1: load the segment, per-thread maxima -------------------
+    // ---- stream the row into registers -------------------------------------
     uint4 r[NV];
+#pragma unroll
+    for (int i = 0; i < NV; ++i) r[i] = load_row_vec<DT>(base, i * NT + tid, V);
+
+    // ---- prologue: this row's parent (ranked while the loads are in flight)
+    if (tid == 0) {
+        s_cnt = 0;
+        s_pu = -1;
+    }
+    __syncthreads();
+    if (level == 0) {
+        if (tid == 0) s_pu = 0;
+    } else {
+        const int pcb = (level == 1) ? 1 : 1 + K + (level - 2) * NE * K;
+        const int n = ((level == 1) ? 1 : NE) * K;
+        uint64_t* s_hi = s_keys;
+        uint64_t* s_lo = s_top;
+        if (tid < n) {
+            const int64_t o = nb + pcb + tid;
+            uint64_t hi, lo;
+            prio_key(t.score[o], level, t.path[o], hi, lo);
+            s_hi[tid] = hi;
+            s_lo[tid] = lo;
+        }
+        __syncthreads();
+        if (tid < n) {
+            const uint64_t hi = s_hi[tid], lo = s_lo[tid];
+            int rk = 0;
+            for (int q = 0; q < n; ++q)
+                rk += (s_hi[q] > hi) || (s_hi[q] == hi && s_lo[q] > lo);
+            if (rk == j) s_pu = pcb + tid;
+        }
+    }
+
+    // ---- threshold from the per-thread maxima -------------------------------
     float tmax = -INFINITY;
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
-        const int e = (i * NT + tid) * VEC;
-        if (s0 + e + VEC <= s1) {
-            r[i] = *(const uint4*)(base + (int64_t)e * ESZ);
-        } else {
-            uint32_t w[4];
-            if (DT) {
-                const uint16_t* p16 = (const uint16_t*)base;
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const int e0 = e + 2 * q, e1 = e0 + 1;
-                    const uint32_t lo = (s0 + e0 < s1) ? p16[e0] : 0xFF80u;
-                    const uint32_t hi = (s0 + e1 < s1) ? p16[e1] : 0xFF80u;
-                    w[q] = lo | (hi << 16);
-                }
-            } else {
-                const uint32_t* p32 = (const uint32_t*)base;
-#pragma unroll
-                for (int q = 0; q < 4; ++q)
-                    w[q] = (s0 + e + q < s1) ? p32[e + q] : 0xFF800000u;
-            }
-            r[i] = make_uint4(w[0], w[1], w[2], w[3]);
-        }
 #pragma unroll
         for (int k = 0; k < VEC; ++k) tmax = fmaxf(tmax, elem<DT>(r[i], k));
     }
-
-    s_sort[tid] = tmax;
-    if (tid == 0) s_cnt = 0;
+    const int cth = (S + NWAVE - 1) / NWAVE;   // <= 64 since S <= 1024
+    const float srt = wave_sort_desc(tmax);
+    const float tw = __shfl(srt, cth - 1);
+    if (lane == 0) s_tau[wid] = tw;
     __syncthreads();
-    bitonic_desc<NT>(s_sort);
-    const float tau = (S <= NT) ? s_sort[S - 1] : -INFINITY;
+    float tau = s_tau[0];
+#pragma unroll
+    for (int i = 1; i < NWAVE; ++i) tau = fminf(tau, s_tau[i]);
+    if (V <= CAP) tau = -INFINITY;
 
-    // ---- collect the candidates >= tau (wave-aggregated append) ----------
+    // ---- collect the candidates >= tau (wave-aggregated append) -------------
+    opaque(r);
     int mine = 0;
+    if (tmax >= tau) {
 #pragma unroll
-    for (int i = 0; i < NV; ++i) {
+        for (int i = 0; i < NV; ++i) {
 #pragma unroll
-        for (int k = 0; k < VEC; ++k) {
-            const int id = s0 + (i * NT + tid) * VEC + k;
-            mine += (id < s1) && (elem<DT>(r[i], k) >= tau);
+            for (int k = 0; k < VEC; ++k) {
+                const int id = (i * NT + tid) * VEC + k;
+                mine += (id < V) && (elem<DT>(r[i], k) >= tau);
+            }
         }
     }
     {
@@ -139,15 +172,16 @@ __global__ __launch_bounds__(NT) void k_expand(TreeDev t, LevelArgs a) {
         int wb = 0;
         if (lane == 0 && tot) wb = atomicAdd(&s_cnt, tot);
         wb = __shfl(wb, 0);
+        opaque(r);
         if (mine) {
             int pos = wb + ex;
 #pragma unroll
             for (int i = 0; i < NV; ++i) {
 #pragma unroll
                 for (int k = 0; k < VEC; ++k) {
-                    const int id = s0 + (i * NT + tid) * VEC + k;
+                    const int id = (i * NT + tid) * VEC + k;
                     const float v = elem<DT>(r[i], k);
-                    if (id < s1 && v >= tau) {
+                    if (id < V && v >= tau) {
                         if (pos < CAP) s_keys[pos] = logit_key(v, (uint32_t)id);
                         ++pos;
                     }
@@ -159,18 +193,21 @@ __global__ __launch_bounds__(NT) void k_expand(TreeDev t, LevelArgs a) {
     int c = s_cnt;
 
     if (c > CAP) {
-        // Degenerate row (massive ties at the threshold): find the S-th
-        // largest selection key exactly by bisection on the 64-bit key.
+        // Degenerate row (massive ties at the threshold): the S-th largest
+        // selection key, exactly, by bisection on the 64-bit key.  Rare, so
+        // it re-reads the row from memory rather than holding more registers.
+        const int nvec = (V + VEC - 1) / VEC;
         uint64_t x = 0;
         for (int bit = 63; bit >= 0; --bit) {
             const uint64_t cand = x | (1ull << bit);
             int n = 0;
-#pragma unroll
-            for (int i = 0; i < NV; ++i) {
+#pragma unroll 1
+            for (int vi = tid; vi < nvec; vi += NT) {
+                const uint4 w = load_row_vec<DT>(base, vi, V);
 #pragma unroll
                 for (int k = 0; k < VEC; ++k) {
-                    const int id = s0 + (i * NT + tid) * VEC + k;
-                    n += (id < s1) && (logit_key(elem<DT>(r[i], k), (uint32_t)id) >= cand);
+                    const int id = vi * VEC + k;
+                    n += (id < V) && (logit_key(elem<DT>(w, k), (uint32_t)id) >= cand);
                 }
             }
             n = block_sum_i32<NT>(n, s_redi);
@@ -179,13 +216,14 @@ __global__ __launch_bounds__(NT) void k_expand(TreeDev t, LevelArgs a) {
         __syncthreads();
         if (tid == 0) s_cnt = 0;
         __syncthreads();
-#pragma unroll
-        for (int i = 0; i < NV; ++i) {
+#pragma unroll 1
+        for (int vi = tid; vi < nvec; vi += NT) {
+            const uint4 w = load_row_vec<DT>(base, vi, V);
 #pragma unroll
             for (int k = 0; k < VEC; ++k) {
-                const int id = s0 + (i * NT + tid) * VEC + k;
-                if (id < s1) {
-                    const uint64_t key = logit_key(elem<DT>(r[i], k), (uint32_t)id);
+                const int id = vi * VEC + k;
+                if (id < V) {
+                    const uint64_t key = logit_key(elem<DT>(w, k), (uint32_t)id);
                     if (key >= x) {
                         const int pos = atomicAdd(&s_cnt, 1);
                         if (pos < CAP) s_keys[pos] = key;
@@ -197,117 +235,87 @@ __global__ __launch_bounds__(NT) void k_expand(TreeDev t, LevelArgs a) {
         c = min(s_cnt, CAP);
     }
 
-    // ---- exact top-S of the candidates, sorted -------------------------
-    int ns = min(S, c);
+    // ---- exact top-S of the candidates (sorted by logit desc, id asc) -------
+    rank_keys<NT>(s_keys, c, s_rank);
+    __syncthreads();
     for (int i = tid; i < c; i += NT) {
-        const uint64_t key = s_keys[i];
-        const int rk = count_greater(s_keys, c, key);
-        if (rk < ns) s_top[rk] = key;
+        const int rk = s_rank[i];
+        if (rk < S) s_top[rk] = s_keys[i];
     }
     __syncthreads();
 
-    // ---- merge the segments of the row ----------------------------------
-    if (a.G * S > CAP) {                 // excluded by the host's launch shape
-        if (tid == 0) atomicOr(t.err, 64);
-        return;
-    }
-    if (a.G > 1) {
-        uint64_t* out = t.seg_keys + ((int64_t)row * a.G + seg) * S;
-        for (int i = tid; i < S; i += NT) out[i] = (i < ns) ? s_top[i] : 0ull;
-        __threadfence();
-        __syncthreads();
-        if (tid == 0) s_last = (atomicAdd(&t.row_cnt[row], 1u) == (uint32_t)(a.G - 1));
-        __syncthreads();
-        if (!s_last) return;
-        __threadfence();
-        if (tid == 0) t.row_cnt[row] = 0u;
-        const uint64_t* in = t.seg_keys + (int64_t)row * a.G * S;
-        const int n = a.G * S;
-        for (int i = tid; i < n; i += NT) s_keys[i] = in[i];
-        __syncthreads();
-        for (int i = tid; i < n; i += NT) {
-            const uint64_t key = s_keys[i];
-            if (key == 0ull) continue;
-            const int rk = count_greater(s_keys, n, key);
-            if (rk < S) s_top[rk] = key;
-        }
-        ns = S;
-        __syncthreads();
-    }
-
-    // ---- phase 2: the node's distributions and its pool -----------------
-    const int level = a.level;
-    const int NE = t.NE, NN = t.NN;
-    const int64_t nb = (int64_t)b * NN;
-    int pu = (level == 0) ? 0 : t.frontier[b * NE + j];
+    // ---- the node's distributions and its pool ------------------------------
+    int pu = s_pu;
     if (pu < 0 || pu >= NN) {
         if (tid == 0) atomicOr(t.err, 16);
         pu = 0;
     }
     const int cb = (level == 0) ? 1 : 1 + K + (level - 1) * NE * K;
     const int e_idx = (level == 0) ? 0 : 1 + (level - 1) * NE + j;
-    double pscore = 1.0;
-    uint64_t ppath = 0;
-    if (level > 0) {
-        pscore = t.score[nb + pu];
-        ppath = t.path[nb + pu];
-    }
-
     const float M = key_value(s_top[0]);
-    uint64_t part = 0;
-    for (int i = tid; i < ns; i += NT) {
-        const uint32_t w = cweight(key_value(s_top[i]), M, a.k1);
-        s_w1[i] = w;
-        part += w;
+    uint32_t w1 = 0;
+    int myid = 0;
+    float myv = 0.0f;
+    if (tid < S) {
+        myv = key_value(s_top[tid]);
+        myid = key_id(s_top[tid]);
+        w1 = cweight(myv, M, a.k1);
+        s_w1[tid] = w1;
+        s_keys[tid] = ((uint64_t)w1 << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)myid);
     }
-    const uint64_t S1 = block_sum_u64<NT>(part, s_red);
-    // rank by construction weight (desc), then id (asc)
-    for (int i = tid; i < ns; i += NT)
-        s_keys[i] = ((uint64_t)s_w1[i] << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)key_id(s_top[i]));
+    const uint64_t S1 = block_sum_u64<NT>(w1, s_red);
+    rank_keys<NT>(s_keys, S, s_wr);
     __syncthreads();
-    for (int i = tid; i < ns; i += NT) {
-        const int rk = count_greater(s_keys, ns, s_keys[i]);
-        s_xs[rk] = (int16_t)i;
-        s_rank[i] = (int16_t)rk;
-    }
+    if (tid < S) s_xs[s_wr[tid]] = (int16_t)tid;
     __syncthreads();
     const float ref_t = key_value(s_top[s_xs[m]]);
-    part = 0;
-    for (int i = tid; i < ns; i += NT) {
-        uint32_t q = 0;
-        if (s_rank[i] >= m) q = cweight(key_value(s_top[i]), ref_t, a.kT);
-        s_q[i] = q;
-        part += q;
+    const bool in_tail = tid < S && s_wr[tid] >= m;
+    uint32_t q = 0;
+    if (in_tail) q = cweight(myv, ref_t, a.kT);
+    if (tid < S) {
+        s_q[tid] = q;
+        // order of the tail by token id (items outside the tail sort last)
+        s_keys[tid] = in_tail ? (uint64_t)(0xFFFFFFFFu - (uint32_t)myid) + 1 : 0;
     }
-    const uint64_t Zq = block_sum_u64<NT>(part, s_red);
+    const uint64_t Zq = block_sum_u64<NT>(q, s_red);
+    rank_keys<NT>(s_keys, S, s_rank);
+    __syncthreads();
+    // scatter the tail id-sorted (in s_top's tail half), then an exclusive
+    // scan of the weights in id order gives the inverse CDF
+    const int ntail = S - m;
+    uint64_t* s_sorted = s_keys;
+    if (in_tail) s_sorted[s_rank[tid]] = ((uint64_t)(uint32_t)myid << 32) | q;
     if (tid == 0) {
         const uint64_t u = philox_draw(a.rng_key, P_DRAFT, (uint64_t)b, (uint64_t)pu);
         s_t = __umul64hi(u, Zq);
         s_y = -1;
     }
     __syncthreads();
-    const uint64_t tt = s_t;
+    uint64_t qi = 0;
+    uint32_t idi = 0;
+    if (tid < ntail) {
+        const uint64_t e = s_sorted[tid];
+        qi = (uint32_t)e;
+        idi = (uint32_t)(e >> 32);
+    }
+    uint64_t total;
+    const uint64_t pre = block_excl_scan_u64<NT>(qi, s_red, &total);
     const int64_t tail_base = ((int64_t)b * t.E + e_idx) * S;
-    for (int i = tid; i < ns; i += NT) {
-        if (s_rank[i] < m) continue;
-        const int id = key_id(s_top[i]);
-        uint64_t pre = 0;
-        int idr = 0;
-        for (int q = 0; q < ns; ++q) {
-            if (s_rank[q] < m) continue;
-            if (key_id(s_top[q]) < id) { pre += s_q[q]; ++idr; }
-        }
-        if (pre <= tt && tt < pre + s_q[i]) s_y = i;
-        t.tail_id[tail_base + idr] = id;
-        t.tail_q[tail_base + idr] = s_q[i];
+    if (tid < ntail) {
+        t.tail_id[tail_base + tid] = (int32_t)idi;
+        t.tail_q[tail_base + tid] = (uint32_t)qi;
+        const uint64_t tt = s_t;
+        if (pre <= tt && tt < pre + qi) s_y = (int)idi;
     }
     __syncthreads();
-    int yi = s_y;
-    if (yi < 0) {                      // unreachable: t < Zq always has an owner
-        if (tid == 0) atomicOr(t.err, 1);
-        yi = s_xs[m];
-    }
-    const int yrank = s_rank[yi];
+    // the sampled support item
+    const int ytok = s_y;
+    if (tid == 0) s_cnt = s_xs[m];               // unreachable fallback
+    __syncthreads();
+    if (in_tail && myid == ytok) s_cnt = tid;
+    if (tid == 0 && ytok < 0) atomicOr(t.err, 1);
+    __syncthreads();
+    const int yi = s_cnt;
     if (tid == 0) {
         t.zq[(int64_t)b * t.E + e_idx] = Zq;
         t.first_child[nb + pu] = cb + j * K;
@@ -324,6 +332,7 @@ __global__ __launch_bounds__(NT) void k_expand(TreeDev t, LevelArgs a) {
     }
     if (tid < K) {
         const int s = tid;
+        const int yr = s_wr[yi];
         int item, kind;
         if (s < m) {
             item = s_xs[s];
@@ -333,16 +342,22 @@ __global__ __launch_bounds__(NT) void k_expand(TreeDev t, LevelArgs a) {
             kind = SAMPLED;
         } else {
             const int f = s - m - 1;
-            const int rk = m + f + ((m + f) >= yrank ? 1 : 0);
+            const int rk = m + f + ((m + f) >= yr ? 1 : 0);
             item = s_xs[rk];
             kind = FILL;
+        }
+        double pscore = 1.0;
+        uint64_t ppath = 0;
+        if (level > 0) {
+            pscore = t.score[nb + pu];
+            ppath = t.path[nb + pu];
         }
         double proxy;
         const double dS1 = (double)S1;
         if (kind == SAMPLED) {
             if (m >= 1) {
                 uint64_t lead = 0;
-                for (int q = 0; q < m; ++q) lead += s_w1[s_xs[q]];
+                for (int q2 = 0; q2 < m; ++q2) lead += s_w1[s_xs[q2]];
                 const uint64_t z = S1 - lead;
                 const uint64_t wm = s_w1[s_xs[m - 1]];
                 proxy = __ddiv_rn((double)(wm < z ? wm : z), dS1);
@@ -365,67 +380,65 @@ __global__ __launch_bounds__(NT) void k_expand(TreeDev t, LevelArgs a) {
         t.first_child[o] = -1;
         t.exp_of[o] = -1;
     }
+}
 
-    // ---- phase 3: next frontier (last row of the sequence) ---------------
-    __threadfence();
-    __syncthreads();
-    if (tid == 0) s_last = (atomicAdd(&t.seq_cnt[b], 1u) == (uint32_t)(a.P - 1));
-    __syncthreads();
-    if (!s_last) return;
-    __threadfence();
-    if (tid == 0) t.seq_cnt[b] = 0u;
-    if (level == t.D - 1) return;
-    const int n = a.P * K;
-    uint64_t* s_hi = s_keys;
-    uint64_t* s_lo = s_top;
-    for (int i = tid; i < n; i += NT) {
-        const int64_t o = nb + cb + i;
+// The frontier of the last expanded level in rank order, for the caller
+// (rheo_frontier): the n_expand best children by priority, per sequence.
+__global__ __launch_bounds__(256) void k_frontier(TreeDev t, int level, int P) {
+    __shared__ uint64_t s_hi[256], s_lo[256];
+    const int b = blockIdx.x, tid = threadIdx.x;
+    const int K = t.K, NE = t.NE;
+    const int cb = (level == 0) ? 1 : 1 + K + (level - 1) * NE * K;
+    const int n = P * K;
+    const int64_t nb = (int64_t)b * t.NN;
+    if (tid < n) {
         uint64_t hi, lo;
-        prio_key(t.score[o], level + 1, t.path[o], hi, lo);
-        s_hi[i] = hi;
-        s_lo[i] = lo;
+        prio_key(t.score[nb + cb + tid], level + 1, t.path[nb + cb + tid], hi, lo);
+        s_hi[tid] = hi;
+        s_lo[tid] = lo;
     }
     __syncthreads();
-    for (int i = tid; i < n; i += NT) {
-        const uint64_t hi = s_hi[i], lo = s_lo[i];
+    if (tid < n) {
+        const uint64_t hi = s_hi[tid], lo = s_lo[tid];
         int rk = 0;
-        for (int q = 0; q < n; ++q)
-            rk += (s_hi[q] > hi) || (s_hi[q] == hi && s_lo[q] > lo);
+        for (int q = 0; q < n; ++q) rk += (s_hi[q] > hi) || (s_hi[q] == hi && s_lo[q] > lo);
         if (rk < NE) {
-            t.frontier[b * NE + rk] = cb + i;
-            t.fr_parent[b * NE + rk] = i / K;
-            t.fr_token[b * NE + rk] = t.tok[nb + cb + i];
+            t.fr_parent[b * NE + rk] = tid / K;
+            t.fr_token[b * NE + rk] = t.tok[nb + cb + tid];
         }
     }
 }
 
-// (dtype, threads, elements per thread) variants; the host picks the one
-// whose segment capacity suits the vocabulary and row count.
-static const ExpandVariant kVariants[2][3] = {
-    {{512, 32}, {512, 64}, {256, 16}},     // fp32
-    {{512, 64}, {512, 128}, {256, 32}},    // bf16
-};
+// Registers per thread hold NV 16-byte vectors: a row must fit NT * NV * VEC.
+static const int kNV[] = {1, 2, 4, 8, 12, 16, 20};
 
-int expand_variant_count(int) { return 3; }
-ExpandVariant expand_variant(int dtype, int v) { return kVariants[dtype ? 1 : 0][v]; }
+int expand_variant_count(int) { return (int)(sizeof(kNV) / sizeof(kNV[0])); }
+ExpandVariant expand_variant(int dtype, int v) {
+    return ExpandVariant{NT, kNV[v] * (dtype ? 8 : 4)};
+}
 
-hipError_t launch_expand(const TreeDev& t, const LevelArgs& a, int variant,
-                         hipStream_t s) {
-    const int rows = t.B * a.P;
-    const dim3 grid(rows * a.G);
-    if (t.dtype) {
-        switch (variant) {
-        case 0: k_expand<1, 512, 64><<<grid, 512, 0, s>>>(t, a); break;
-        case 1: k_expand<1, 512, 128><<<grid, 512, 0, s>>>(t, a); break;
-        default: k_expand<1, 256, 32><<<grid, 256, 0, s>>>(t, a); break;
-        }
-    } else {
-        switch (variant) {
-        case 0: k_expand<0, 512, 32><<<grid, 512, 0, s>>>(t, a); break;
-        case 1: k_expand<0, 512, 64><<<grid, 512, 0, s>>>(t, a); break;
-        default: k_expand<0, 256, 16><<<grid, 256, 0, s>>>(t, a); break;
-        }
+template <int DT>
+static void launch_dt(const TreeDev& t, const LevelArgs& a, int v, dim3 grid, hipStream_t s) {
+    switch (v) {
+    case 0: k_expand<DT, 1><<<grid, NT, 0, s>>>(t, a); break;
+    case 1: k_expand<DT, 2><<<grid, NT, 0, s>>>(t, a); break;
+    case 2: k_expand<DT, 4><<<grid, NT, 0, s>>>(t, a); break;
+    case 3: k_expand<DT, 8><<<grid, NT, 0, s>>>(t, a); break;
+    case 4: k_expand<DT, 12><<<grid, NT, 0, s>>>(t, a); break;
+    case 5: k_expand<DT, 16><<<grid, NT, 0, s>>>(t, a); break;
+    default: k_expand<DT, 20><<<grid, NT, 0, s>>>(t, a); break;
     }
+}
+
+hipError_t launch_expand(const TreeDev& t, const LevelArgs& a, int variant, hipStream_t s) {
+    const dim3 grid(t.B * a.P);
+    if (t.dtype) launch_dt<1>(t, a, variant, grid, s);
+    else launch_dt<0>(t, a, variant, grid, s);
+    return hipGetLastError();
+}
+
+hipError_t launch_frontier(const TreeDev& t, int level, int P, hipStream_t s) {
+    k_frontier<<<t.B, 256, 0, s>>>(t, level, P);
     return hipGetLastError();
 }
 

@@ -5,7 +5,8 @@
 // ranks a parent before its children, so the kept set is ancestor-closed.
 //
 // One block per sequence ranks all nodes by counting (each node's rank is
-// the number of nodes with a larger 128-bit priority key; keys are unique).
+// the number of nodes with a larger 128-bit priority key; keys are unique),
+// several lanes sharing each node's comparisons.
 #include "rheo_device.h"
 #include "rheo_state.h"
 
@@ -31,11 +32,11 @@ __global__ __launch_bounds__(NT) void k_prune(TreeDev t, int R) {
         t.porder[nb] = 0;
     }
     __syncthreads();
+    int16_t* s_rank = (int16_t*)(s_dyn + 2 * n);
+    rank_keys128<NT>(s_hi, s_lo, n, s_rank);
+    __syncthreads();
     for (int i = threadIdx.x; i < n; i += NT) {
-        const uint64_t hi = s_hi[i], lo = s_lo[i];
-        int rk = 0;
-        for (int q = 0; q < n; ++q)
-            rk += (s_hi[q] > hi) || (s_hi[q] == hi && s_lo[q] > lo);
+        const int rk = s_rank[i];
         if (rk < R) {
             t.pidx[nb + 1 + i] = rk + 1;
             t.porder[nb + rk + 1] = 1 + i;
@@ -52,7 +53,7 @@ __global__ __launch_bounds__(NT) void k_prune(TreeDev t, int R) {
 }
 
 hipError_t launch_prune(const TreeDev& t, int R, hipStream_t s) {
-    const size_t shm = 2 * sizeof(uint64_t) * (size_t)(t.NN - 1);
+    const size_t shm = (2 * sizeof(uint64_t) + sizeof(int16_t)) * (size_t)(t.NN - 1) + 16;
     k_prune<1024><<<t.B, 1024, shm, s>>>(t, R);
     return hipGetLastError();
 }

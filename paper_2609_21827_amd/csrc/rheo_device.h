@@ -90,6 +90,13 @@ __device__ __forceinline__ void prio_key(double score, int depth, uint64_t path,
     lo = ((uint64_t)(15 - depth) << 60) | (0x0FFFFFFFFFFFFFFFull - path);
 }
 
+// 16-byte streaming load (non-temporal: the row is read once).
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 load_stream16(const void* p) {
+    const u32x4 v = __builtin_nontemporal_load((const u32x4*)p);
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 // bf16 pairs packed in a uint32: low and high element as fp32 (exact).
 __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
@@ -170,6 +177,110 @@ __device__ __forceinline__ int wave_excl_scan(int v) {
         if (l >= o) x += y;
     }
     return x - v;
+}
+
+}  // namespace rheo
+
+namespace rheo {
+
+// Wave-wide inclusive prefix sum of 64-bit values.
+__device__ __forceinline__ uint64_t wave_incl_scan_u64(uint64_t v) {
+    const int l = threadIdx.x % WAVE;
+#pragma unroll
+    for (int o = 1; o < WAVE; o <<= 1) {
+        const uint64_t y = __shfl_up(v, o);
+        if (l >= o) v += y;
+    }
+    return v;
+}
+
+// Block-wide exclusive prefix sum of 64-bit values (one value per thread);
+// sh holds NT / WAVE words.  Also returns the total through *total.
+template <int NT>
+__device__ uint64_t block_excl_scan_u64(uint64_t v, uint64_t* sh, uint64_t* total) {
+    const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE;
+    const uint64_t inc = wave_incl_scan_u64(v);
+    __syncthreads();
+    if (l == WAVE - 1) sh[w] = inc;
+    __syncthreads();
+    uint64_t base = 0, tot = 0;
+#pragma unroll
+    for (int i = 0; i < NT / WAVE; ++i) {
+        if (i < w) base += sh[i];
+        tot += sh[i];
+    }
+    *total = tot;
+    return base + inc - v;
+}
+
+// Descending bitonic sort of one float per lane across a wave.
+__device__ __forceinline__ float wave_sort_desc(float v) {
+    const int lane = threadIdx.x % WAVE;
+#pragma unroll
+    for (int k = 2; k <= WAVE; k <<= 1) {
+#pragma unroll
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            const float o = __shfl_xor(v, j);
+            const bool take_max = ((lane & j) == 0) == ((lane & k) == 0);
+            v = take_max ? fmaxf(v, o) : fminf(v, o);
+        }
+    }
+    return v;
+}
+
+// rank[i] = number of keys strictly greater than keys[i], for unique keys
+// in LDS; each key is compared by a group of F consecutive lanes.
+template <int NT>
+__device__ void rank_keys(const uint64_t* keys, int n, int16_t* rank) {
+    int npad = 1;
+    while (npad < n) npad <<= 1;
+    int F = NT / npad;
+    if (F < 1) F = 1;
+    if (F > WAVE) F = WAVE;
+    const int sub = threadIdx.x % F;
+    const int per = NT / F;
+    for (int base = 0; base < n; base += per) {
+        const int i = base + threadIdx.x / F;
+        int cnt = 0;
+        if (i < n) {
+            const uint64_t k = keys[i];
+            int j = sub;
+            for (; j + 3 * F < n; j += 4 * F) {
+                const uint64_t a = keys[j], b = keys[j + F], c = keys[j + 2 * F],
+                               d = keys[j + 3 * F];
+                cnt += (a > k) + (b > k) + (c > k) + (d > k);
+            }
+            for (; j < n; j += F) cnt += keys[j] > k;
+        }
+        for (int o = 1; o < F; o <<= 1) cnt += __shfl_xor(cnt, o);
+        if (i < n && sub == 0) rank[i] = (int16_t)cnt;
+    }
+}
+
+// rank[i] = number of (hi, lo) keys strictly greater than key i (unique
+// 128-bit keys in LDS), F consecutive lanes per key as in rank_keys.
+template <int NT>
+__device__ void rank_keys128(const uint64_t* hi, const uint64_t* lo, int n, int16_t* rank) {
+    int npad = 1;
+    while (npad < n) npad <<= 1;
+    int F = NT / npad;
+    if (F < 1) F = 1;
+    if (F > WAVE) F = WAVE;
+    const int sub = threadIdx.x % F;
+    const int per = NT / F;
+    for (int base = 0; base < n; base += per) {
+        const int i = base + threadIdx.x / F;
+        int cnt = 0;
+        if (i < n) {
+            const uint64_t kh = hi[i], kl = lo[i];
+            for (int j = sub; j < n; j += F) {
+                const uint64_t h = hi[j];
+                cnt += (h > kh) || (h == kh && lo[j] > kl);
+            }
+        }
+        for (int o = 1; o < F; o <<= 1) cnt += __shfl_xor(cnt, o);
+        if (i < n && sub == 0) rank[i] = (int16_t)cnt;
+    }
 }
 
 }  // namespace rheo

@@ -37,19 +37,18 @@ struct TreeDev {
     // pruned tree
     int32_t* pidx;                 // [B][NN]: pruned index, -1 if pruned away
     int32_t* porder;               // [B][NN]: uid of each pruned index
-    // in-kernel coordination and scratch
-    uint64_t* seg_keys;            // [rows][G][S] segment selections
-    uint32_t* row_cnt;             // [rows] arrival counters
-    uint32_t* seq_cnt;             // [B] arrival counters
     int32_t* err;                  // sticky device error flag
+    // verification team exchange (see verify.hip)
+    uint32_t* team_flag;           // [B][GMAX] arrival epochs
+    uint32_t* team_max;            // [B][GMAX] segment maxima (fp32 bits)
+    uint64_t* team_chunk;          // [B][NCMAX] chunk totals of p's weights
+    uint32_t* team_sp;             // [B][SPMAX] p's weights at the special tokens
 };
 
 struct LevelArgs {
     const void* logits;
     int level;                     // 0..D-1
     int P;                         // parents per sequence at this level
-    int G;                         // segments per row
-    int seg_len;                   // elements per segment (multiple of 8)
     float k1;                      // construction kT (untempered unless asked)
     float kT;                      // sampling kT
     uint64_t rng_key;
@@ -58,6 +57,9 @@ struct LevelArgs {
 struct VerifyArgs {
     const void* logits;
     int R;
+    int G;                         // blocks per sequence (a team)
+    int NV;                        // 16-byte vectors per thread per segment
+    uint32_t epoch;                // barrier epoch base of this call
     float kT;
     uint64_t rng_key;
     int32_t* accepted;
@@ -68,7 +70,10 @@ struct VerifyArgs {
 hipError_t launch_expand(const TreeDev& t, const LevelArgs& a, int variant,
                          hipStream_t s);
 hipError_t launch_prune(const TreeDev& t, int R, hipStream_t s);
-hipError_t launch_verify(const TreeDev& t, const VerifyArgs& a, hipStream_t s);
+hipError_t launch_frontier(const TreeDev& t, int level, int P, hipStream_t s);
+hipError_t verify_shape(const TreeDev& t, int* G, int* nv_idx, int* grid);
+hipError_t launch_verify(const TreeDev& t, const VerifyArgs& a, int nv_idx, int grid,
+                         hipStream_t s);
 
 // expand kernel variants: elements per thread x threads per block
 struct ExpandVariant { int nt, ept; };

@@ -1,36 +1,42 @@
 // RheoVerification (Algorithm 1) applied layer by layer from the root of the
-// pruned tree (Thm. 1).  One block walks one sequence.
+// pruned tree (Thm. 1).
 //
-// Per layer, at the current node u:
-//   p = softmax(target(u) / T) over the whole vocabulary, as canonical
-//   integer weights P_v (relative to the row maximum) with the exact total
-//   S_p and the totals of fixed 64*VEC-token chunks (for the inverse CDF).
-//   Candidates C = children of u in the pruned tree, in slot order; s = the
-//   sampled child's position or -1.
-//   s != -1: accept Y iff eta <= p(Y) / q~(Y), i.e.
-//            (U+1) Q_Y S_p <= 2^32 P_Y Z_q;  else drop Y and take the residual
-//            r_v ~ N_v = max(0, P_v Z_q - Q_v S_p)  (q~ is the truncated tail
-//            stored at expansion; N_v = P_v Z_q off its support).
-//   s == -1: r_v ~ N_v = P_v.
-//   Each remaining candidate in slot order is accepted iff
-//   (U+1) Z_rem <= 2^32 N_u, else N_u = 0 and Z_rem -= N_u.
-//   If none is accepted (or C is empty), u* ~ r by inverse CDF over token ids:
-//   t = floor(U64 Z_rem / 2^64), the chunk holding t from the chunk totals
-//   corrected at the overridden tokens, then a scan of that chunk.
-// All tests are exact integer comparisons (eta = (U+1) / 2^32 in (0, 1]).
+// A team of G co-resident blocks walks one sequence (cooperative launch).
+// At each layer the current node's target row is split into G segments of
+// whole 64*VEC-token chunks; every block holds its segment in registers:
+//   1. segment maximum -> team exchange -> row maximum M
+//   2. canonical weights P_v of p = softmax(target / T) (relative to M) for
+//      the segment, the totals of its chunks, and P at the special tokens
+//      (the candidates, and the stored tail of q~) that fall in it ->
+//      team exchange
+//   3. every block takes the same Algorithm 1 decision from the exchanged
+//      totals with exact integer tests:
+//        s != -1: accept Y iff (U+1) Q_Y S_p <= 2^32 P_Y Z_q; otherwise the
+//                 residual r ~ N_v = max(0, P_v Z_q - Q_v S_p) (Q_v = 0 off
+//                 the stored tail), with total
+//                 Z_r = Z_q S_p - sum_tail min(P_v Z_q, Q_v S_p);
+//        s == -1: r ~ N_v = P_v;
+//        each remaining candidate in slot order: accept iff
+//        (U+1) Z_rem <= 2^32 N_u, else N_u = 0, Z_rem -= N_u;
+//        none accepted (or no candidates): u* ~ r by inverse CDF over token
+//        ids, t = floor(U64 Z_rem / 2^64): the chunk holding t from the chunk
+//        totals corrected at the special tokens, then a scan of that chunk.
+// Team exchanges use agent-scope atomic stores and loads only (they are
+// coherent across the XCDs without cache write-back or invalidation), with
+// arrival epochs in per-block flags and bounded waits.
+#include <cstdlib>
+
 #include "rheo_device.h"
 #include "rheo_state.h"
 
 namespace rheo {
 
+constexpr int NTV = 256;
+constexpr int NWV = NTV / WAVE;
+constexpr int GMAX = 64;
 constexpr int NCMAX = 1024;      // chunks: V <= 262143, chunk >= 256 tokens
-constexpr int SPMAX = 1024 + 16; // overridden tokens: support tail + candidates
-
-template <int DT>
-__device__ __forceinline__ float load_logit(const char* row, int v) {
-    if (DT) return __uint_as_float((uint32_t)((const uint16_t*)row)[v] << 16);
-    return ((const float*)row)[v];
-}
+constexpr int SPMAX = 1024 + 16; // stored tail + candidates
+constexpr long kSpinLimit = 1L << 20;   // ~1 s: a wait that long is an error
 
 template <int DT>
 __device__ __forceinline__ float velem(const uint4& v, int k) {
@@ -40,11 +46,17 @@ __device__ __forceinline__ float velem(const uint4& v, int k) {
 }
 
 template <int DT>
+__device__ __forceinline__ float load_logit(const char* row, int v) {
+    if (DT) return __uint_as_float((uint32_t)((const uint16_t*)row)[v] << 16);
+    return ((const float*)row)[v];
+}
+
+template <int DT>
 __device__ __forceinline__ uint4 load_vec(const char* row, int vi, int V) {
     constexpr int VEC = DT ? 8 : 4;
     constexpr int ESZ = DT ? 2 : 4;
     const int e = vi * VEC;
-    if (e + VEC <= V) return *(const uint4*)(row + (int64_t)e * ESZ);
+    if (e + VEC <= V) return load_stream16(row + (int64_t)e * ESZ);
     uint32_t w[4];
     if (DT) {
         const uint16_t* p = (const uint16_t*)row;
@@ -62,60 +74,138 @@ __device__ __forceinline__ uint4 load_vec(const char* row, int vi, int V) {
     return make_uint4(w[0], w[1], w[2], w[3]);
 }
 
-// Position of token v in the id-sorted tail list, -1 if absent.
-__device__ inline int find_sorted(const int32_t* ids, int n, int v) {
+// Position of v in the id-sorted list, -1 if absent; lower bound in *lb.
+__device__ inline int find_sorted(const int32_t* ids, int n, int v, int* lb = nullptr) {
     int lo = 0, hi = n;
     while (lo < hi) {
         const int mid = (lo + hi) >> 1;
         if (ids[mid] < v) lo = mid + 1; else hi = mid;
     }
+    if (lb) *lb = lo;
     return (lo < n && ids[lo] == v) ? lo : -1;
 }
 
-template <int DT, int NT>
-__global__ __launch_bounds__(NT) void k_verify(TreeDev t, VerifyArgs a) {
+// 128-bit wave / block scans (values < 2^127).
+__device__ __forceinline__ u128 shfl_up_u128(u128 v, int o) {
+    const uint64_t lo = __shfl_up((uint64_t)v, o);
+    const uint64_t hi = __shfl_up((uint64_t)(v >> 64), o);
+    return ((u128)hi << 64) | lo;
+}
+__device__ __forceinline__ u128 shfl_xor_u128(u128 v, int o) {
+    const uint64_t lo = __shfl_xor((uint64_t)v, o);
+    const uint64_t hi = __shfl_xor((uint64_t)(v >> 64), o);
+    return ((u128)hi << 64) | lo;
+}
+// exclusive scan across the block; *total receives the sum
+__device__ u128 block_excl_scan_u128(u128 v, u128* sh, u128* total) {
+    const int l = threadIdx.x % WAVE, w = threadIdx.x / WAVE;
+    u128 inc = v;
+#pragma unroll
+    for (int o = 1; o < WAVE; o <<= 1) {
+        const u128 y = shfl_up_u128(inc, o);
+        if (l >= o) inc += y;
+    }
+    __syncthreads();
+    if (l == WAVE - 1) sh[w] = inc;
+    __syncthreads();
+    u128 base = 0, tot = 0;
+#pragma unroll
+    for (int i = 0; i < NWV; ++i) {
+        if (i < w) base += sh[i];
+        tot += sh[i];
+    }
+    *total = tot;
+    return base + inc - v;
+}
+
+// Team barrier: publish this block's arrival at `epoch`, then wait until
+// every team member has arrived.  Prior team-visible stores must be agent
+// atomic stores; each thread waits for its own before the block barrier.
+// Returns false (and raises the error flag) if the wait timed out.
+__device__ bool team_barrier(uint32_t* flags, int g, int G, uint32_t epoch, int32_t* err,
+                             int* s_ok) {
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (threadIdx.x < WAVE) {
+        if (threadIdx.x == 0) {
+            *s_ok = 1;
+            __hip_atomic_store(&flags[g], epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        long spins = 0;
+        for (;;) {
+            bool ok = true;
+            if ((int)threadIdx.x < G)
+                ok = __hip_atomic_load(&flags[threadIdx.x], __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT) >= epoch;
+            if (__all(ok)) break;
+            if (++spins > kSpinLimit) {
+                if (threadIdx.x == 0) {
+                    atomicOr(err, 128);
+                    *s_ok = 0;
+                }
+                break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+        }
+    }
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __syncthreads();
+    return *s_ok != 0;
+}
+
+template <int DT, int NV>
+__global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
     constexpr int VEC = DT ? 8 : 4;
-    constexpr int CH = WAVE * VEC;
+    constexpr int ESZ = DT ? 2 : 4;
+    constexpr int CH = WAVE * VEC;           // tokens per chunk
+    constexpr int SEGCH = NV * NWV;          // chunks per segment
 
     __shared__ uint64_t s_chunk[NCMAX];
-    __shared__ u128 s_def[NCMAX];
-    __shared__ int32_t s_sp_id[SPMAX];
-    __shared__ uint32_t s_sp_P[SPMAX];
-    __shared__ u128 s_sp_N[SPMAX];
+    __shared__ int32_t s_tid[SPMAX];         // stored tail ids (sorted)
+    __shared__ uint32_t s_tq[SPMAX];         // stored tail weights Q
+    __shared__ uint32_t s_tp[SPMAX];         // p's weights at tail tokens, then candidates
     __shared__ u128 s_cn[CH];
-    __shared__ int16_t s_mark[CH];
-    __shared__ int s_c_uid[16], s_c_tok[16], s_c_slot[16], s_c_kind[16];
-    __shared__ uint32_t s_c_P[16];
-    __shared__ float s_redf[NT / WAVE];
-    __shared__ uint64_t s_red[NT / WAVE];
-    __shared__ int s_nc, s_spos, s_e, s_nsp, s_done, s_next, s_token, s_cstar;
-    __shared__ u128 s_F, s_tt;
+    __shared__ u128 s_w128[NWV];
+    __shared__ uint64_t s_red[NWV];
+    __shared__ float s_redf[NWV];
+    __shared__ int s_c_uid[16], s_c_tok[16], s_c_slot[16], s_c_tail[16], s_c_zero[16];
+    __shared__ int s_nc, s_spos, s_e, s_nt, s_mode, s_next, s_token, s_cstar;
+    __shared__ u128 s_F, s_Zrem, s_tt;
+    __shared__ float s_M;
+    __shared__ int s_ok;
 
     const int tid = threadIdx.x;
     const int lane = tid % WAVE, wid = tid / WAVE;
-    const int b = blockIdx.x;
+    // team layout: all G blocks of a sequence on the same XCD
+    const int x = blockIdx.x;
+    const int G = a.G;
+    int b, g;
+    {
+        const int xcd = x % 8, local = x / 8;
+        const int teams_per_xcd = (t.B + 7) / 8;
+        b = xcd + 8 * (local / G);
+        g = local % G;
+        if (local / G >= teams_per_xcd || b >= t.B) return;  // padding blocks
+    }
     const int V = t.V, K = t.K, NN = t.NN;
-    const int nvec = (V + VEC - 1) / VEC;
     const int NC = (V + CH - 1) / CH;
     const int64_t nb = (int64_t)b * NN;
-    const int nt = t.S - t.m;             // entries of a stored tail list
+    uint32_t* flags = t.team_flag + (int64_t)b * GMAX;
+    uint32_t* tmax_x = t.team_max + (int64_t)b * GMAX;
+    uint64_t* chunk_x = t.team_chunk + (int64_t)b * NCMAX;
+    uint32_t* sp_x = t.team_sp + (int64_t)b * SPMAX;
+    const int c0 = g * SEGCH;                 // first chunk of this segment
+    const int c1 = min(NC, c0 + SEGCH);
 
-    int cur = 0;                          // uid of the current node
-    int level = 0;
-    int nacc = 0;
+    int cur = 0, level = 0, nacc = 0;
     for (;;) {
-        if (level > t.D) {                 // unreachable: every accept descends
+        int cur_p = t.pidx[nb + cur];
+        if (level > t.D || cur_p < 0 || cur_p > a.R) {   // unreachable
             if (tid == 0) atomicOr(t.err, 32);
             break;
         }
-        int cur_p = t.pidx[nb + cur];
-        if (cur_p < 0 || cur_p > a.R) {
-            if (tid == 0) atomicOr(t.err, 32);
-            cur_p = 0;
-        }
-        const char* row = (const char*)a.logits +
-                          ((int64_t)b * (a.R + 1) + cur_p) * t.stride * (DT ? 2 : 4);
-        // ---- candidates of this layer ----------------------------------
+        const char* row = (const char*)a.logits + ((int64_t)b * (a.R + 1) + cur_p) * t.stride * ESZ;
+        // ---- this layer's candidates and stored tail ------------------------
         if (tid == 0) {
             int nc = 0, spos = -1;
             const int fc = t.first_child[nb + cur];
@@ -128,7 +218,7 @@ __global__ __launch_bounds__(NT) void k_verify(TreeDev t, VerifyArgs a) {
                         s_c_uid[nc] = c;
                         s_c_tok[nc] = t.tok[nb + c];
                         s_c_slot[nc] = sl + 1;
-                        s_c_kind[nc] = kind;
+                        s_c_zero[nc] = 0;
                         ++nc;
                     }
                 }
@@ -136,169 +226,275 @@ __global__ __launch_bounds__(NT) void k_verify(TreeDev t, VerifyArgs a) {
             s_nc = nc;
             s_spos = spos;
             s_e = t.exp_of[nb + cur];
+            s_nt = (fc >= 0) ? t.S - t.m : 0;
         }
-        // ---- pass A: row maximum ----------------------------------------
+        // ---- 1. segment in registers, row maximum ---------------------------
+        uint4 r[NV];
+#pragma unroll
+        for (int i = 0; i < NV; ++i) {
+            const int vi = (c0 + i * NWV + wid) * WAVE + lane;   // chunk-major
+            r[i] = (c0 + i * NWV + wid < c1) ? load_vec<DT>(row, vi, V)
+                                              : make_uint4(DT ? 0xFF80FF80u : 0xFF800000u,
+                                                           DT ? 0xFF80FF80u : 0xFF800000u,
+                                                           DT ? 0xFF80FF80u : 0xFF800000u,
+                                                           DT ? 0xFF80FF80u : 0xFF800000u);
+        }
         float mx = -INFINITY;
-        for (int vi = tid; vi < nvec; vi += NT) {
-            const uint4 x = load_vec<DT>(row, vi, V);
 #pragma unroll
-            for (int k = 0; k < VEC; ++k) mx = fmaxf(mx, velem<DT>(x, k));
+        for (int i = 0; i < NV; ++i)
+#pragma unroll
+            for (int k = 0; k < VEC; ++k) mx = fmaxf(mx, velem<DT>(r[i], k));
+        mx = block_max<NTV>(mx, s_redf);
+        if (tid == 0)
+            __hip_atomic_store(&tmax_x[g], __float_as_uint(mx), __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+        // the stored tail of q~ at this node (read-only tree data)
+        const int nt = s_nt, nc = s_nc, spos = s_spos, e = s_e;
+        if (nt > 0) {
+            const int64_t tb = ((int64_t)b * t.E + e) * t.S;
+            for (int i = tid; i < nt; i += NTV) {
+                s_tid[i] = t.tail_id[tb + i];
+                s_tq[i] = t.tail_q[tb + i];
+            }
         }
-        const float M = block_max<NT>(mx, s_redf);
-        // ---- pass B: weights, chunk totals --------------------------------
-        const int iters = (nvec + NT - 1) / NT;
-        for (int it = 0; it < iters; ++it) {
-            const int vi = it * NT + tid;
-            uint64_t sum = 0;
-            if (vi < nvec) {
-                const uint4 x = load_vec<DT>(row, vi, V);
+        if (!team_barrier(flags, g, G, a.epoch + 2 * level + 1, t.err, &s_ok)) break;
+        if (tid < WAVE) {
+            float v = -INFINITY;
+            if (tid < G)
+                v = __uint_as_float(__hip_atomic_load(&tmax_x[tid], __ATOMIC_RELAXED,
+                                                      __HIP_MEMORY_SCOPE_AGENT));
+            v = wave_max(v);
+            if (tid == 0) s_M = v;
+        }
+        __syncthreads();
+        const float M = s_M;
+        // ---- 2. weights of the segment, chunk totals, special tokens --------
 #pragma unroll
-                for (int k = 0; k < VEC; ++k) {
-                    const int v = vi * VEC + k;
-                    if (v < V) sum += cweight(velem<DT>(x, k), M, a.kT);
-                }
+        for (int i = 0; i < NV; ++i) {
+            const int c = c0 + i * NWV + wid;
+            uint64_t sum = 0;
+#pragma unroll
+            for (int k = 0; k < VEC; ++k) {
+                const int v = (c * WAVE + lane) * VEC + k;
+                if (v < V) sum += cweight(velem<DT>(r[i], k), M, a.kT);
             }
             sum = wave_sum_u64(sum);
-            const int c = it * (NT / WAVE) + wid;
-            if (lane == 0 && c < NC) s_chunk[c] = sum;
+            if (lane == 0 && c < c1)
+                __hip_atomic_store(&chunk_x[c], sum, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
-        __syncthreads();
-        uint64_t part = 0;
-        for (int c = tid; c < NC; c += NT) part += s_chunk[c];
-        const uint64_t Sp = block_sum_u64<NT>(part, s_red);
-        // ---- gathers: P at the candidates and on the stored tail ---------
-        const int nc = s_nc, spos = s_spos, e = s_e;
-        if (tid < nc) s_c_P[tid] = cweight(load_logit<DT>(row, s_c_tok[tid]), M, a.kT);
-        if (spos >= 0) {
-            const int64_t tb = ((int64_t)b * t.E + e) * t.S;
-            for (int i = tid; i < nt; i += NT) {
-                const int v = t.tail_id[tb + i];
-                s_sp_id[i] = v;
-                s_sp_P[i] = cweight(load_logit<DT>(row, v), M, a.kT);
+        {
+            const int lo_tok = c0 * CH, hi_tok = min(V, c1 * CH);
+            for (int i = tid; i < nt; i += NTV) {
+                const int v = s_tid[i];
+                if (v >= lo_tok && v < hi_tok)
+                    __hip_atomic_store(&sp_x[i], cweight(load_logit<DT>(row, v), M, a.kT),
+                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+            if (tid < nc) {
+                const int v = s_c_tok[tid];
+                if (v >= lo_tok && v < hi_tok)
+                    __hip_atomic_store(&sp_x[nt + tid], cweight(load_logit<DT>(row, v), M, a.kT),
+                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
         }
-        __syncthreads();
-        // ---- Algorithm 1 at this layer (one thread, exact integers) -------
+        if (!team_barrier(flags, g, G, a.epoch + 2 * level + 2, t.err, &s_ok)) break;
+        uint64_t part = 0;
+        for (int c = tid; c < NC; c += NTV) {
+            const uint64_t v = __hip_atomic_load(&chunk_x[c], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            s_chunk[c] = v;
+            part += v;
+        }
+        for (int i = tid; i < nt + nc; i += NTV)
+            s_tp[i] = __hip_atomic_load(&sp_x[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const uint64_t Sp = block_sum_u64<NTV>(part, s_red);
+        // ---- 3. Algorithm 1 at this layer -----------------------------------
+        const uint64_t Zq = (nt > 0) ? t.zq[(int64_t)b * t.E + e] : 1;
         if (tid == 0) {
-            int done = 0, next = -1, token = -1, nsp = 0;
-            u128 F = 1, Zrem = Sp;
-            bool sampled_rejected = false;
+            int mode = 0;          // 0: residual tests follow, 1: accepted, 2: final sample
+            int next = -1, token = -1;
+            if (nc == 0) mode = 2;
+            for (int ci = 0; ci < nc; ++ci) s_c_tail[ci] = find_sorted(s_tid, nt, s_c_tok[ci]);
             if (spos >= 0) {
-                const int64_t tb = ((int64_t)b * t.E + e) * t.S;
-                const uint64_t Zq = t.zq[(int64_t)b * t.E + e];
-                const int yi = find_sorted(s_sp_id, nt, s_c_tok[spos]);
-                const uint64_t QY = (yi >= 0) ? t.tail_q[tb + yi] : 0;
-                const uint64_t PY = s_c_P[spos];
+                const int yi = s_c_tail[spos];
+                if (yi < 0) atomicOr(t.err, 4);
+                const uint64_t QY = (yi >= 0) ? s_tq[yi] : 0;
+                const uint64_t PY = s_tp[nt + spos];
                 const uint64_t U = philox_draw(a.rng_key, P_VERIFY, (uint64_t)b,
                                                (uint64_t)(32 * level)) >> 32;
-                const u128 lhs = (u128)(U + 1) * QY * Sp;
-                const u128 rhs = ((u128)PY * Zq) << 32;
-                if (yi < 0) atomicOr(t.err, 4);
-                if (lhs <= rhs) {
+                if ((u128)(U + 1) * QY * Sp <= (((u128)PY * Zq) << 32)) {
+                    mode = 1;
                     next = s_c_uid[spos];
                     token = s_c_tok[spos];
-                } else {
-                    sampled_rejected = true;
-                    F = Zq;
-                    u128 def = 0;
-                    for (int i = 0; i < nt; ++i) {
-                        const u128 pz = (u128)s_sp_P[i] * Zq;
-                        const u128 qs = (u128)t.tail_q[tb + i] * Sp;
-                        const u128 nv = pz > qs ? pz - qs : (u128)0;
-                        s_sp_N[i] = nv;
-                        def += pz - nv;
-                    }
-                    nsp = nt;
-                    Zrem = (u128)Zq * Sp - def;
                 }
             }
-            if (next < 0) {
-                for (int ci = 0; ci < nc; ++ci) {
-                    if (ci == spos) continue;
-                    const int tok = s_c_tok[ci];
-                    int sp = sampled_rejected ? find_sorted(s_sp_id, nt, tok) : -1;
-                    const u128 Nu = (sp >= 0) ? s_sp_N[sp] : F * (u128)s_c_P[ci];
-                    const uint64_t U = philox_draw(a.rng_key, P_VERIFY, (uint64_t)b,
-                                                   (uint64_t)(32 * level + s_c_slot[ci])) >> 32;
-                    if ((u128)(U + 1) * Zrem <= (Nu << 32)) {
-                        next = s_c_uid[ci];
-                        token = tok;
-                        break;
-                    }
-                    Zrem -= Nu;
-                    if (sp >= 0) {
-                        s_sp_N[sp] = 0;
-                    } else {
-                        s_sp_id[nsp] = tok;
-                        s_sp_P[nsp] = s_c_P[ci];
-                        s_sp_N[nsp] = 0;
-                        ++nsp;
-                    }
-                }
-            }
-            if (next < 0) {
-                done = 1;
-                const uint64_t U = philox_draw(a.rng_key, P_FINAL, (uint64_t)b, (uint64_t)level);
-                s_tt = mulhi_64x128(U, Zrem);
-            }
-            s_done = done;
+            s_mode = mode;
             s_next = next;
             s_token = token;
-            s_nsp = nsp;
-            s_F = F;
+            s_F = (spos >= 0 && mode == 0) ? (u128)Zq : (u128)1;
         }
         __syncthreads();
-        if (!s_done) {
-            if (tid == 0) a.accepted[(int64_t)b * t.D + nacc] = s_token;
+        const bool residual = (spos >= 0 && s_mode == 0);   // Y rejected: r from p - q~
+        if (residual) {
+            // Z_r = Zq Sp - sum over the tail of min(P_v Zq, Q_v Sp)
+            u128 d = 0;
+            for (int i = tid; i < nt; i += NTV) {
+                const u128 pz = (u128)s_tp[i] * Zq, qs = (u128)s_tq[i] * Sp;
+                d += pz < qs ? pz : qs;
+            }
+            u128 tot;
+            block_excl_scan_u128(d, s_w128, &tot);
+            if (tid == 0) s_Zrem = (u128)Zq * Sp - tot;
+        } else if (tid == 0) {
+            s_Zrem = Sp;
+        }
+        __syncthreads();
+        if (tid == 0 && s_mode == 0) {
+            const u128 F = s_F;
+            u128 Zrem = s_Zrem;
+            int mode = 2, next = -1, token = -1;
+            for (int ci = 0; ci < nc; ++ci) {
+                if (ci == spos) continue;
+                const int ti = s_c_tail[ci];
+                const uint64_t P = s_tp[nt + ci];
+                u128 Nu = F * (u128)P;
+                if (residual && ti >= 0) {
+                    const u128 pz = (u128)P * Zq, qs = (u128)s_tq[ti] * Sp;
+                    Nu = pz > qs ? pz - qs : (u128)0;
+                }
+                const uint64_t U = philox_draw(a.rng_key, P_VERIFY, (uint64_t)b,
+                                               (uint64_t)(32 * level + s_c_slot[ci])) >> 32;
+                if ((u128)(U + 1) * Zrem <= (Nu << 32)) {
+                    mode = 1;
+                    next = s_c_uid[ci];
+                    token = s_c_tok[ci];
+                    break;
+                }
+                Zrem -= Nu;
+                s_c_zero[ci] = 1;
+            }
+            s_mode = mode;
+            s_next = next;
+            s_token = token;
+            s_Zrem = Zrem;
+        }
+        if (tid == 0 && s_mode == 2) {
+            const uint64_t U = philox_draw(a.rng_key, P_FINAL, (uint64_t)b, (uint64_t)level);
+            s_tt = mulhi_64x128(U, s_Zrem);
+        }
+        __syncthreads();
+        if (s_mode == 1) {
+            if (g == 0 && tid == 0) a.accepted[(int64_t)b * t.D + nacc] = s_token;
             ++nacc;
             cur = s_next;
             ++level;
             __syncthreads();
             continue;
         }
-        // ---- final sample u* ~ r by inverse CDF over token ids -------------
-        const int nsp = s_nsp;
+        // ---- final sample u* ~ r (one block of the team) --------------------
+        if (g != 0) break;
         const u128 F = s_F;
-        for (int c = tid; c < NC; c += NT) s_def[c] = 0;
+        const u128 tt = s_tt;
+        // corrected chunk totals, contiguous chunk ranges per thread
+        const int cpt = (NC + NTV - 1) / NTV;
+        const int ca = min(NC, tid * cpt), cz = min(NC, ca + cpt);
+        auto special_def = [&](int cidx, u128* def_out) {
+            // F * P_v - N_v summed over the special tokens of chunk cidx
+            u128 d = 0;
+            if (residual) {
+                int lb;
+                find_sorted(s_tid, nt, cidx * CH, &lb);
+                for (int i = lb; i < nt && s_tid[i] < (cidx + 1) * CH; ++i) {
+                    const u128 pz = (u128)s_tp[i] * Zq, qs = (u128)s_tq[i] * Sp;
+                    d += pz < qs ? pz : qs;       // F P - N for a live tail token
+                }
+            }
+            for (int ci = 0; ci < nc; ++ci) {
+                if (!s_c_zero[ci]) continue;
+                const int v = s_c_tok[ci];
+                if (v / CH != cidx) continue;
+                const u128 fp = F * (u128)s_tp[nt + ci];
+                if (residual && s_c_tail[ci] >= 0) {
+                    // zeroed tail token: its live deficit was counted above
+                    const u128 pz = (u128)s_tp[nt + ci] * Zq, qs = (u128)s_tq[s_c_tail[ci]] * Sp;
+                    d += fp - (pz < qs ? pz : qs);
+                } else {
+                    d += fp;
+                }
+            }
+            *def_out = d;
+        };
+        u128 mysum = 0;
+        for (int c = ca; c < cz; ++c) {
+            u128 d;
+            special_def(c, &d);
+            mysum += F * (u128)s_chunk[c] - d;
+        }
+        u128 total;
+        const u128 pre = block_excl_scan_u128(mysum, s_w128, &total);
+        if (tid == 0) s_cstar = -1;
         __syncthreads();
-        if (tid == 0) {
-            for (int i = 0; i < nsp; ++i)
-                s_def[s_sp_id[i] / CH] += F * (u128)s_sp_P[i] - s_sp_N[i];
-            u128 acc = 0;
-            const u128 tt = s_tt;
-            int cs = NC - 1;
-            for (int c = 0; c < NC; ++c) {
-                const u128 w = F * (u128)s_chunk[c] - s_def[c];
-                if (acc + w > tt) { cs = c; break; }
+        if (tt >= pre && tt < pre + mysum) {
+            u128 acc = pre;
+            for (int c = ca; c < cz; ++c) {
+                u128 d;
+                special_def(c, &d);
+                const u128 w = F * (u128)s_chunk[c] - d;
+                if (tt < acc + w) {
+                    s_cstar = c;
+                    s_tt = tt - acc;
+                    break;
+                }
                 acc += w;
             }
-            s_cstar = cs;
-            s_tt = tt - acc;
         }
-        for (int i = tid; i < CH; i += NT) s_mark[i] = -1;
         __syncthreads();
         const int cs = s_cstar;
-        for (int i = tid; i < nsp; i += NT)
-            if (s_sp_id[i] / CH == cs) s_mark[s_sp_id[i] - cs * CH] = (int16_t)i;
-        __syncthreads();
-        for (int i = tid; i < CH; i += NT) {
+        if (cs < 0) {
+            if (tid == 0) atomicOr(t.err, 8);
+            break;
+        }
+        // scan of chunk cs: per-token residual weights, then a block scan
+        const u128 t2 = s_tt;
+        for (int i = tid; i < CH; i += NTV) {
             const int v = cs * CH + i;
             u128 w = 0;
             if (v < V) {
-                const int mk = s_mark[i];
-                w = (mk >= 0) ? s_sp_N[mk] : F * (u128)cweight(load_logit<DT>(row, v), M, a.kT);
+                const uint64_t P = cweight(load_logit<DT>(row, v), M, a.kT);
+                w = F * (u128)P;
+                if (residual) {
+                    const int ti = find_sorted(s_tid, nt, v);
+                    if (ti >= 0) {
+                        const u128 pz = (u128)P * Zq, qs = (u128)s_tq[ti] * Sp;
+                        w = pz > qs ? pz - qs : (u128)0;
+                    }
+                }
+                for (int ci = 0; ci < nc; ++ci)
+                    if (s_c_zero[ci] && s_c_tok[ci] == v) w = 0;
             }
             s_cn[i] = w;
         }
         __syncthreads();
-        if (tid == 0) {
-            u128 acc = 0;
-            const u128 tt = s_tt;
-            int tok = -1;
-            for (int i = 0; i < CH; ++i) {
-                acc += s_cn[i];
-                if (acc > tt) { tok = cs * CH + i; break; }
+        constexpr int TPT = CH / NTV;          // tokens per thread (1 or 2)
+        u128 mine = 0;
+#pragma unroll
+        for (int q = 0; q < TPT; ++q) mine += s_cn[tid * TPT + q];
+        const u128 pre2 = block_excl_scan_u128(mine, s_w128, &total);
+        if (tid == 0) s_token = -1;
+        __syncthreads();
+        if (t2 >= pre2 && t2 < pre2 + mine) {
+            u128 acc = pre2;
+#pragma unroll
+            for (int q = 0; q < TPT; ++q) {
+                acc += s_cn[tid * TPT + q];
+                if (t2 < acc) {
+                    s_token = cs * CH + tid * TPT + q;
+                    break;
+                }
             }
+        }
+        __syncthreads();
+        if (tid == 0) {
+            const int tok = s_token;
             if (tok < 0) atomicOr(t.err, 8);
             a.final_token[b] = tok;
             a.accept_len[b] = nacc;
@@ -308,10 +504,61 @@ __global__ __launch_bounds__(NT) void k_verify(TreeDev t, VerifyArgs a) {
     }
 }
 
-hipError_t launch_verify(const TreeDev& t, const VerifyArgs& a, hipStream_t s) {
-    if (t.dtype) k_verify<1, 1024><<<t.B, 1024, 0, s>>>(t, a);
-    else k_verify<0, 1024><<<t.B, 1024, 0, s>>>(t, a);
-    return hipGetLastError();
+// NV (vectors per thread) variants of the verification kernel
+static const int kVNV[] = {1, 2, 4, 8, 12, 16, 20};
+static const int kVN = (int)(sizeof(kVNV) / sizeof(kVNV[0]));
+
+template <int DT>
+static const void* verify_fn(int v) {
+    switch (v) {
+    case 0: return (const void*)&k_verify<DT, 1>;
+    case 1: return (const void*)&k_verify<DT, 2>;
+    case 2: return (const void*)&k_verify<DT, 4>;
+    case 3: return (const void*)&k_verify<DT, 8>;
+    case 4: return (const void*)&k_verify<DT, 12>;
+    case 5: return (const void*)&k_verify<DT, 16>;
+    default: return (const void*)&k_verify<DT, 20>;
+    }
+}
+
+// Team shape for a tree: aim for about 512 blocks in all, each holding a
+// segment of whole chunks in registers; G <= GMAX and every block of the
+// grid co-resident (cooperative launch).
+hipError_t verify_shape(const TreeDev& t, int* G_out, int* nv_idx, int* grid) {
+    const int VEC = t.dtype ? 8 : 4;
+    const int NC = (t.V + WAVE * VEC - 1) / (WAVE * VEC);
+    const char* env = getenv("RHEO_VERIFY_BLOCKS");
+    int Gd = (env ? atoi(env) : 512) / t.B;
+    if (Gd < 1) Gd = 1;
+    if (Gd > 16) Gd = 16;
+    int vi = kVN - 1;
+    for (int v = 0; v < kVN; ++v)
+        if (kVNV[v] * NWV * Gd >= NC) { vi = v; break; }
+    int G = (NC + kVNV[vi] * NWV - 1) / (kVNV[vi] * NWV);
+    if (G > GMAX) return hipErrorInvalidValue;
+    int dev = 0, cus = 0, per_cu = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    const void* fn = t.dtype ? verify_fn<1>(vi) : verify_fn<0>(vi);
+    if (e == hipSuccess) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, NTV, 0);
+    if (e != hipSuccess) return e;
+    const int teams_per_xcd = (t.B + 7) / 8;
+    const int blocks = 8 * teams_per_xcd * G;
+    if (blocks > per_cu * cus) return hipErrorCooperativeLaunchTooLarge;
+    *G_out = G;
+    *nv_idx = vi;
+    *grid = blocks;
+    return hipSuccess;
+}
+
+hipError_t launch_verify(const TreeDev& t, const VerifyArgs& a, int nv_idx, int grid,
+                         hipStream_t s) {
+    const void* fn = t.dtype ? verify_fn<1>(nv_idx) : verify_fn<0>(nv_idx);
+    TreeDev tt = t;
+    VerifyArgs aa = a;
+    aa.NV = kVNV[nv_idx];
+    void* args[] = {&tt, &aa};
+    return hipLaunchCooperativeKernel(fn, dim3(grid), dim3(NTV), args, 0, s);
 }
 
 }  // namespace rheo

@@ -129,20 +129,26 @@ def test_headline(dev):
 
 
 def test_launch_shape_independence(dev):
-    """Results do not depend on how rows are split into segments."""
+    """Results do not depend on register tiling or verification team size."""
     from paper_2609_21827_amd.driver import make_tree, run_step
     w = W["llama3"].with_(B=4)
     outs = []
-    for variant, minb in (("0", "1"), ("0", "4096"), ("2", "64")):
-        os.environ["RHEO_EXPAND_VARIANT"] = variant
-        os.environ["RHEO_EXPAND_MIN_BLOCKS"] = minb
+    for variant, vblocks in ((None, None), ("6", "4"), ("6", "64"), (None, "1024")):
+        env = {}
+        if variant:
+            env["RHEO_EXPAND_VARIANT"] = variant
+        if vblocks:
+            env["RHEO_VERIFY_BLOCKS"] = vblocks
+        os.environ.update(env)
         try:
             tree = make_tree(w, device=dev)
         finally:
-            del os.environ["RHEO_EXPAND_VARIANT"], os.environ["RHEO_EXPAND_MIN_BLOCKS"]
+            for k in env:
+                del os.environ[k]
         acc, alen, fin = run_step(tree, w, 0, device=dev)
         nodes = tree.read_nodes()
         outs.append((acc, alen, fin, {k: v.cpu() for k, v in nodes.items()}))
+        assert tree.device_error() == 0
         tree.close()
     for o in outs[1:]:
         assert torch.equal(o[0], outs[0][0]) and torch.equal(o[1], outs[0][1])
