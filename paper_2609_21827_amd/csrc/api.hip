@@ -46,7 +46,7 @@ struct rheo_tree {
     int level = 0;
     int R = 0;
     int variant = 0;
-    int vG = 1, v_nv = 0, v_grid = 1;    // verification team shape
+    int vG = 1, v_segch = 1, v_grid = 1;  // verification team shape
     uint32_t verify_calls = 0;
     float T_expand = 1.0f;
     void* blocks[32] = {};
@@ -182,7 +182,7 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
         delete t;
         return hip_fail(e, "initialising tree state");
     }
-    e = verify_shape(d, &t->vG, &t->v_nv, &t->v_grid);
+    e = verify_shape(d, &t->vG, &t->v_segch, &t->v_grid);
     if (e != hipSuccess) {
         free_all(t);
         delete t;
@@ -287,7 +287,7 @@ int rheo_verify(rheo_tree* t, const void* logits, float T, uint64_t key, int32_t
         if (e0 != hipSuccess) return hip_fail(e0, "resetting verification flags");
     }
     a.epoch = t->verify_calls * 64u;
-    const hipError_t e = launch_verify(t->dev, a, t->v_nv, t->v_grid, (hipStream_t)stream);
+    const hipError_t e = launch_verify(t->dev, a, t->v_segch, t->v_grid, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "verify launch");
     t->state = VERIFIED;
     return RHEO_OK;

@@ -37,6 +37,16 @@ __device__ __forceinline__ float elem(const uint4& v, int k) {
     return __uint_as_float(w[k]);
 }
 
+// Element k of a vector for a k known only at run time (selects, so the
+// vector stays in registers).
+template <int DT>
+__device__ __forceinline__ float elem_dyn(const uint4& v, int k) {
+    const int wi = DT ? (k >> 1) : k;
+    const uint32_t w = wi == 0 ? v.x : wi == 1 ? v.y : wi == 2 ? v.z : v.w;
+    if (DT) return (k & 1) ? bf_hi(w) : bf_lo(w);
+    return __uint_as_float(w);
+}
+
 // Vector vi (VEC consecutive elements) of a row; elements past V read as -inf.
 template <int DT>
 __device__ __forceinline__ uint4 load_row_vec(const char* base, int vi, int V) {
@@ -62,20 +72,17 @@ __device__ __forceinline__ uint4 load_row_vec(const char* base, int vi, int V) {
     return make_uint4(w[0], w[1], w[2], w[3]);
 }
 
-// Hides the register-resident row from the optimiser between passes, so
-// each pass unpacks bf16 pairs on the fly instead of keeping every element
-// unpacked (which would exceed the register budget of a 1024-thread block).
-template <int NV>
-__device__ __forceinline__ void opaque(uint4 (&r)[NV]) {
-#pragma unroll
-    for (int i = 0; i < NV; ++i)
-        asm volatile("" : "+v"(r[i].x), "+v"(r[i].y), "+v"(r[i].z), "+v"(r[i].w));
+// Orders LDS accesses of the lanes of one wave (no block barrier).
+__device__ __forceinline__ void wave_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
 }
 
 template <int DT, int NV>
 __global__ __launch_bounds__(NT) void k_expand(TreeDev t, LevelArgs a) {
     constexpr int VEC = DT ? 8 : 4;
     constexpr int ESZ = DT ? 2 : 4;
+    constexpr int NM = DT ? (NV + 1) / 2 : NV;   // registers of per-vector maxima
 
     __shared__ uint64_t s_keys[CAP];
     __shared__ uint64_t s_top[SMAX];
@@ -84,11 +91,9 @@ __global__ __launch_bounds__(NT) void k_expand(TreeDev t, LevelArgs a) {
     __shared__ int16_t s_rank[SMAX];
     __shared__ int16_t s_wr[SMAX];     // support item -> rank by construction weight
     __shared__ int16_t s_xs[SMAX];     // rank by construction weight -> support item
-    __shared__ float s_tau[NWAVE];
-    __shared__ uint64_t s_red[NWAVE];
     __shared__ int s_redi[NWAVE];
-    __shared__ int s_cnt, s_y, s_pu;
-    __shared__ uint64_t s_t;
+    __shared__ int s_cnt, s_y, s_pu, s_yi;
+    __shared__ uint64_t s_u;
 
     const int tid = threadIdx.x;
     const int lane = tid % WAVE, wid = tid / WAVE;
@@ -106,7 +111,8 @@ __global__ __launch_bounds__(NT) void k_expand(TreeDev t, LevelArgs a) {
 #pragma unroll
     for (int i = 0; i < NV; ++i) r[i] = load_row_vec<DT>(base, i * NT + tid, V);
 
-    // ---- prologue: this row's parent (ranked while the loads are in flight)
+    // ---- prologue: this row's parent (ranked while the loads are in flight),
+    //      and the Philox draw of its sampled slot
     if (tid == 0) {
         s_cnt = 0;
         s_pu = -1;
@@ -135,56 +141,88 @@ __global__ __launch_bounds__(NT) void k_expand(TreeDev t, LevelArgs a) {
             if (rk == j) s_pu = pcb + tid;
         }
     }
+    __syncthreads();
+    if (tid == 0) {
+        int pu = s_pu;
+        if (pu < 0 || pu >= NN) {
+            atomicOr(t.err, 16);
+            pu = 0;
+            s_pu = 0;
+        }
+        s_u = philox_draw(a.rng_key, P_DRAFT, (uint64_t)b, (uint64_t)pu);
+    }
 
-    // ---- threshold from the per-thread maxima -------------------------------
+    // ---- per-vector maxima (exact) and this thread's maximum ----------------
+    // bf16: a packed word read as fp32 is its high element plus a fraction of
+    // one bf16 ulp (the low element's bits), so the maximum over the raw words
+    // and the unpacked low elements, with its low 16 bits cleared, is exactly
+    // the maximum element (logits are finite; padding words are NaN and ignored)
+    uint32_t vm[NM];
+#pragma unroll
+    for (int q = 0; q < NM; ++q) vm[q] = 0;
     float tmax = -INFINITY;
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
-#pragma unroll
-        for (int k = 0; k < VEC; ++k) tmax = fmaxf(tmax, elem<DT>(r[i], k));
+        float mx;
+        if (DT) {
+            const uint32_t* w = &r[i].x;
+            mx = fmaxf(fmaxf(__uint_as_float(w[0]), bf_lo(w[0])), __uint_as_float(w[1]));
+            mx = fmaxf(fmaxf(mx, bf_lo(w[1])), __uint_as_float(w[2]));
+            mx = fmaxf(fmaxf(mx, bf_lo(w[2])), __uint_as_float(w[3]));
+            mx = fmaxf(mx, bf_lo(w[3]));
+            const uint32_t hb = __float_as_uint(mx) & 0xFFFF0000u;
+            mx = __uint_as_float(hb);
+            vm[i / 2] |= (i & 1) ? hb : (hb >> 16);
+        } else {
+            mx = fmaxf(fmaxf(elem<DT>(r[i], 0), elem<DT>(r[i], 1)),
+                       fmaxf(elem<DT>(r[i], 2), elem<DT>(r[i], 3)));
+            vm[i] = __float_as_uint(mx);
+        }
+        tmax = fmaxf(tmax, mx);
     }
-    const int cth = (S + NWAVE - 1) / NWAVE;   // <= 64 since S <= 1024
-    const float srt = wave_sort_desc(tmax);
-    const float tw = __shfl(srt, cth - 1);
-    if (lane == 0) s_tau[wid] = tw;
-    __syncthreads();
-    float tau = s_tau[0];
-#pragma unroll
-    for (int i = 1; i < NWAVE; ++i) tau = fminf(tau, s_tau[i]);
-    if (V <= CAP) tau = -INFINITY;
 
-    // ---- collect the candidates >= tau (wave-aggregated append) -------------
-    opaque(r);
-    int mine = 0;
-    if (tmax >= tau) {
+    // ---- threshold: each wave sorts its maxima and offers its top L; the
+    //      S-th largest offered value is reached by at least S elements
+    //      (usually it is the S-th largest maximum itself)
+    const int L = min(WAVE, 2 * ((S + NWAVE - 1) / NWAVE));
+    const float srt = wave_sort_desc(tmax);
+    float* s_off = (float*)s_w1;                 // NWAVE * L <= 1024 offered values
+    if (lane < L) s_off[wid * L + lane] = srt;
+    __syncthreads();
+    if (tid == 0) s_cnt = 0x7FFFFFFF;
+    __syncthreads();
+    {
+        const int n = NWAVE * L;
+        const int F = NT / n;                    // lanes per offered value (>= 1)
+        const int i = tid / F, sub = tid % F;
+        const float v = s_off[i];
+        int gt = 0;
+        for (int jj = sub; jj < n; jj += F) gt += s_off[jj] > v;
+        for (int o = 1; o < F; o <<= 1) gt += __shfl_xor(gt, o);
+        if (sub == 0 && gt < S) atomicMin(&s_cnt, (int)(ord32(v) ^ 0x80000000u));
+    }
+    __syncthreads();
+    float tau = unord32((uint32_t)s_cnt ^ 0x80000000u);
+    if (V <= CAP) tau = -INFINITY;
+    __syncthreads();
+    if (tid == 0) s_cnt = 0;
+    __syncthreads();
+
+    // ---- candidates >= tau: one compare per vector, a rare element scan ----
+    opaque_regs(r);
 #pragma unroll
-        for (int i = 0; i < NV; ++i) {
+    for (int i = 0; i < NV; ++i) {
+        const float vmax = DT ? ((i & 1) ? bf_hi(vm[i / 2]) : bf_lo(vm[i / 2]))
+                              : __uint_as_float(vm[i]);
+        if (vmax >= tau) {
+            const int e0 = (i * NT + tid) * VEC;
 #pragma unroll
             for (int k = 0; k < VEC; ++k) {
-                const int id = (i * NT + tid) * VEC + k;
-                mine += (id < V) && (elem<DT>(r[i], k) >= tau);
-            }
-        }
-    }
-    {
-        const int ex = wave_excl_scan(mine);
-        const int tot = __shfl(ex + mine, WAVE - 1);
-        int wb = 0;
-        if (lane == 0 && tot) wb = atomicAdd(&s_cnt, tot);
-        wb = __shfl(wb, 0);
-        opaque(r);
-        if (mine) {
-            int pos = wb + ex;
-#pragma unroll
-            for (int i = 0; i < NV; ++i) {
-#pragma unroll
-                for (int k = 0; k < VEC; ++k) {
-                    const int id = (i * NT + tid) * VEC + k;
-                    const float v = elem<DT>(r[i], k);
-                    if (id < V && v >= tau) {
-                        if (pos < CAP) s_keys[pos] = logit_key(v, (uint32_t)id);
-                        ++pos;
-                    }
+                const float v = elem<DT>(r[i], k);
+                const int id = e0 + k;
+                if (v >= tau && id < V) {
+                    const int pos = atomicAdd(&s_cnt, 1);
+                    if (pos < CAP) s_keys[pos] = logit_key(v, (uint32_t)id);
                 }
             }
         }
@@ -244,79 +282,114 @@ __global__ __launch_bounds__(NT) void k_expand(TreeDev t, LevelArgs a) {
     }
     __syncthreads();
 
-    // ---- the node's distributions and its pool ------------------------------
-    int pu = s_pu;
-    if (pu < 0 || pu >= NN) {
-        if (tid == 0) atomicOr(t.err, 16);
-        pu = 0;
-    }
+    // ---- the node's distributions and its pool: one wave; the other waves
+    //      leave, so the next row's block can start loading -------------------
+    if (wid != 0) return;
+    const int pu = s_pu;
     const int cb = (level == 0) ? 1 : 1 + K + (level - 1) * NE * K;
     const int e_idx = (level == 0) ? 0 : 1 + (level - 1) * NE + j;
+    const int IPL = (S + WAVE - 1) / WAVE;       // support items per lane (<= 16)
     const float M = key_value(s_top[0]);
-    uint32_t w1 = 0;
-    int myid = 0;
-    float myv = 0.0f;
-    if (tid < S) {
-        myv = key_value(s_top[tid]);
-        myid = key_id(s_top[tid]);
-        w1 = cweight(myv, M, a.k1);
-        s_w1[tid] = w1;
-        s_keys[tid] = ((uint64_t)w1 << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)myid);
+    // construction weights (untempered unless asked), S1, rank by (w1 desc, id asc)
+    uint64_t part = 0;
+    for (int q = 0; q < IPL; ++q) {
+        const int i = q * WAVE + lane;
+        if (i < S) {
+            const uint64_t tk = s_top[i];
+            const uint32_t w = cweight(key_value(tk), M, a.k1);
+            s_w1[i] = w;
+            s_keys[i] = ((uint64_t)w << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)key_id(tk));
+            part += w;
+        }
     }
-    const uint64_t S1 = block_sum_u64<NT>(w1, s_red);
-    rank_keys<NT>(s_keys, S, s_wr);
-    __syncthreads();
-    if (tid < S) s_xs[s_wr[tid]] = (int16_t)tid;
-    __syncthreads();
+    const uint64_t S1 = wave_sum_u64(part);
+    wave_sync();
+    for (int q = 0; q < IPL; ++q) {
+        const int i = q * WAVE + lane;
+        if (i < S) {
+            const uint64_t k = s_keys[i];
+            int rk = 0;
+            for (int jj = 0; jj < S; ++jj) rk += s_keys[jj] > k;
+            s_wr[i] = (int16_t)rk;
+            s_xs[rk] = (int16_t)i;
+        }
+    }
+    wave_sync();
+    // tail q~_T (relative to x_{m+1}), its total, and its order by token id
     const float ref_t = key_value(s_top[s_xs[m]]);
-    const bool in_tail = tid < S && s_wr[tid] >= m;
-    uint32_t q = 0;
-    if (in_tail) q = cweight(myv, ref_t, a.kT);
-    if (tid < S) {
-        s_q[tid] = q;
-        // order of the tail by token id (items outside the tail sort last)
-        s_keys[tid] = in_tail ? (uint64_t)(0xFFFFFFFFu - (uint32_t)myid) + 1 : 0;
+    part = 0;
+    for (int q = 0; q < IPL; ++q) {
+        const int i = q * WAVE + lane;
+        if (i < S) {
+            const bool tail = s_wr[i] >= m;
+            const uint64_t tk = s_top[i];
+            const uint32_t w = tail ? cweight(key_value(tk), ref_t, a.kT) : 0u;
+            s_q[i] = w;
+            part += w;
+            s_keys[i] = tail ? (uint64_t)(0xFFFFFFFFu - (uint32_t)key_id(tk)) + 1 : 0ull;
+        }
     }
-    const uint64_t Zq = block_sum_u64<NT>(q, s_red);
-    rank_keys<NT>(s_keys, S, s_rank);
-    __syncthreads();
-    // scatter the tail id-sorted (in s_top's tail half), then an exclusive
-    // scan of the weights in id order gives the inverse CDF
+    const uint64_t Zq = wave_sum_u64(part);
+    wave_sync();
     const int ntail = S - m;
-    uint64_t* s_sorted = s_keys;
-    if (in_tail) s_sorted[s_rank[tid]] = ((uint64_t)(uint32_t)myid << 32) | q;
-    if (tid == 0) {
-        const uint64_t u = philox_draw(a.rng_key, P_DRAFT, (uint64_t)b, (uint64_t)pu);
-        s_t = __umul64hi(u, Zq);
-        s_y = -1;
+    for (int q = 0; q < IPL; ++q) {
+        const int i = q * WAVE + lane;
+        if (i < S && s_keys[i] != 0ull) {
+            const uint64_t k = s_keys[i];
+            int rk = 0;
+            for (int jj = 0; jj < S; ++jj) rk += s_keys[jj] > k;
+            s_rank[i] = (int16_t)rk;              // position in id order
+        }
     }
-    __syncthreads();
-    uint64_t qi = 0;
-    uint32_t idi = 0;
-    if (tid < ntail) {
-        const uint64_t e = s_sorted[tid];
-        qi = (uint32_t)e;
-        idi = (uint32_t)(e >> 32);
-    }
-    uint64_t total;
-    const uint64_t pre = block_excl_scan_u64<NT>(qi, s_red, &total);
+    wave_sync();
+    // id-sorted tail written straight to the tree (q~ for verification) and
+    // kept in LDS for the inverse CDF (s_keys is free again)
     const int64_t tail_base = ((int64_t)b * t.E + e_idx) * S;
-    if (tid < ntail) {
-        t.tail_id[tail_base + tid] = (int32_t)idi;
-        t.tail_q[tail_base + tid] = (uint32_t)qi;
-        const uint64_t tt = s_t;
-        if (pre <= tt && tt < pre + qi) s_y = (int)idi;
+    for (int q = 0; q < IPL; ++q) {
+        const int i = q * WAVE + lane;
+        if (i < S && s_wr[i] >= m) {
+            const int idr = s_rank[i];
+            const int id = key_id(s_top[i]);
+            s_keys[idr] = ((uint64_t)(uint32_t)id << 32) | s_q[i];
+            t.tail_id[tail_base + idr] = id;
+            t.tail_q[tail_base + idr] = s_q[i];
+        }
     }
-    __syncthreads();
-    // the sampled support item
+    wave_sync();
+    // Y ~ q~_T: t = floor(U64 Zq / 2^64), the first id-ordered tail entry whose
+    // inclusive prefix exceeds t (each lane scans a contiguous block)
+    const uint64_t tt = __umul64hi(s_u, Zq);
+    const int lo = lane * IPL, hi = min(ntail, lo + IPL);
+    uint64_t mysum = 0;
+    for (int i = lo; i < hi; ++i) mysum += (uint32_t)s_keys[i];
+    const uint64_t incl = wave_incl_scan_u64(mysum);
+    uint64_t acc = incl - mysum;
+    if (lane == 0) s_y = -1;
+    wave_sync();
+    if (acc <= tt && tt < incl) {
+        for (int i = lo; i < hi; ++i) {
+            const uint64_t w = (uint32_t)s_keys[i];
+            if (tt < acc + w) {
+                s_y = (int)(s_keys[i] >> 32);
+                break;
+            }
+            acc += w;
+        }
+    }
+    wave_sync();
     const int ytok = s_y;
-    if (tid == 0) s_cnt = s_xs[m];               // unreachable fallback
-    __syncthreads();
-    if (in_tail && myid == ytok) s_cnt = tid;
-    if (tid == 0 && ytok < 0) atomicOr(t.err, 1);
-    __syncthreads();
-    const int yi = s_cnt;
-    if (tid == 0) {
+    if (lane == 0) {
+        s_yi = s_xs[m];                        // unreachable fallback
+        if (ytok < 0) atomicOr(t.err, 1);
+    }
+    wave_sync();
+    for (int q = 0; q < IPL; ++q) {
+        const int i = q * WAVE + lane;
+        if (i < S && s_wr[i] >= m && key_id(s_top[i]) == ytok) s_yi = i;
+    }
+    wave_sync();
+    const int yi = s_yi;
+    if (lane == 0) {
         t.zq[(int64_t)b * t.E + e_idx] = Zq;
         t.first_child[nb + pu] = cb + j * K;
         t.exp_of[nb + pu] = e_idx;
@@ -330,8 +403,9 @@ __global__ __launch_bounds__(NT) void k_expand(TreeDev t, LevelArgs a) {
             t.path[nb] = 0;
         }
     }
-    if (tid < K) {
-        const int s = tid;
+    // ---- the K children: top-m leads, Y, fills (App. C.1) ------------------
+    if (lane < K) {
+        const int s = lane;
         const int yr = s_wr[yi];
         int item, kind;
         if (s < m) {

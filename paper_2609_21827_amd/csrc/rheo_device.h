@@ -283,4 +283,14 @@ __device__ void rank_keys128(const uint64_t* hi, const uint64_t* lo, int n, int1
     }
 }
 
+// Hides register-resident 16-byte vectors from the optimiser between
+// passes, so each pass unpacks bf16 pairs on the fly instead of keeping
+// every element unpacked across the whole kernel.
+template <int NV>
+__device__ __forceinline__ void opaque_regs(uint4 (&r)[NV]) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i)
+        asm volatile("" : "+v"(r[i].x), "+v"(r[i].y), "+v"(r[i].z), "+v"(r[i].w));
+}
+
 }  // namespace rheo

@@ -58,7 +58,7 @@ struct VerifyArgs {
     const void* logits;
     int R;
     int G;                         // blocks per sequence (a team)
-    int NV;                        // 16-byte vectors per thread per segment
+    int NV;                        // chunks per segment
     uint32_t epoch;                // barrier epoch base of this call
     float kT;
     uint64_t rng_key;
@@ -71,8 +71,8 @@ hipError_t launch_expand(const TreeDev& t, const LevelArgs& a, int variant,
                          hipStream_t s);
 hipError_t launch_prune(const TreeDev& t, int R, hipStream_t s);
 hipError_t launch_frontier(const TreeDev& t, int level, int P, hipStream_t s);
-hipError_t verify_shape(const TreeDev& t, int* G, int* nv_idx, int* grid);
-hipError_t launch_verify(const TreeDev& t, const VerifyArgs& a, int nv_idx, int grid,
+hipError_t verify_shape(const TreeDev& t, int* G, int* segch, int* grid);
+hipError_t launch_verify(const TreeDev& t, const VerifyArgs& a, int segch, int grid,
                          hipStream_t s);
 
 // expand kernel variants: elements per thread x threads per block

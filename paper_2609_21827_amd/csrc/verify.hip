@@ -153,12 +153,12 @@ __device__ bool team_barrier(uint32_t* flags, int g, int G, uint32_t epoch, int3
     return *s_ok != 0;
 }
 
-template <int DT, int NV>
+template <int DT>
 __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
     constexpr int VEC = DT ? 8 : 4;
     constexpr int ESZ = DT ? 2 : 4;
     constexpr int CH = WAVE * VEC;           // tokens per chunk
-    constexpr int SEGCH = NV * NWV;          // chunks per segment
+    const int SEGCH = a.NV;                  // chunks per segment
 
     __shared__ uint64_t s_chunk[NCMAX];
     __shared__ int32_t s_tid[SPMAX];         // stored tail ids (sorted)
@@ -228,22 +228,14 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
             s_e = t.exp_of[nb + cur];
             s_nt = (fc >= 0) ? t.S - t.m : 0;
         }
-        // ---- 1. segment in registers, row maximum ---------------------------
-        uint4 r[NV];
-#pragma unroll
-        for (int i = 0; i < NV; ++i) {
-            const int vi = (c0 + i * NWV + wid) * WAVE + lane;   // chunk-major
-            r[i] = (c0 + i * NWV + wid < c1) ? load_vec<DT>(row, vi, V)
-                                              : make_uint4(DT ? 0xFF80FF80u : 0xFF800000u,
-                                                           DT ? 0xFF80FF80u : 0xFF800000u,
-                                                           DT ? 0xFF80FF80u : 0xFF800000u,
-                                                           DT ? 0xFF80FF80u : 0xFF800000u);
-        }
+        // ---- 1. row maximum (each wave streams whole chunks of the segment) ----
         float mx = -INFINITY;
+#pragma unroll 4
+        for (int c = c0 + wid; c < c1; c += NWV) {
+            const uint4 xv = load_vec<DT>(row, c * WAVE + lane, V);
 #pragma unroll
-        for (int i = 0; i < NV; ++i)
-#pragma unroll
-            for (int k = 0; k < VEC; ++k) mx = fmaxf(mx, velem<DT>(r[i], k));
+            for (int k = 0; k < VEC; ++k) mx = fmaxf(mx, velem<DT>(xv, k));
+        }
         mx = block_max<NTV>(mx, s_redf);
         if (tid == 0)
             __hip_atomic_store(&tmax_x[g], __float_as_uint(mx), __ATOMIC_RELAXED,
@@ -268,18 +260,19 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
         }
         __syncthreads();
         const float M = s_M;
-        // ---- 2. weights of the segment, chunk totals, special tokens --------
-#pragma unroll
-        for (int i = 0; i < NV; ++i) {
-            const int c = c0 + i * NWV + wid;
+        // ---- 2. weights of the segment (second pass, from L2), chunk totals,
+        //         p's weights at the special tokens ---------------------------
+#pragma unroll 2
+        for (int c = c0 + wid; c < c1; c += NWV) {
+            const uint4 xv = load_vec<DT>(row, c * WAVE + lane, V);
             uint64_t sum = 0;
 #pragma unroll
             for (int k = 0; k < VEC; ++k) {
                 const int v = (c * WAVE + lane) * VEC + k;
-                if (v < V) sum += cweight(velem<DT>(r[i], k), M, a.kT);
+                if (v < V) sum += cweight(velem<DT>(xv, k), M, a.kT);
             }
             sum = wave_sum_u64(sum);
-            if (lane == 0 && c < c1)
+            if (lane == 0)
                 __hip_atomic_store(&chunk_x[c], sum, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
         {
@@ -504,59 +497,40 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
     }
 }
 
-// NV (vectors per thread) variants of the verification kernel
-static const int kVNV[] = {1, 2, 4, 8, 12, 16, 20};
-static const int kVN = (int)(sizeof(kVNV) / sizeof(kVNV[0]));
-
-template <int DT>
-static const void* verify_fn(int v) {
-    switch (v) {
-    case 0: return (const void*)&k_verify<DT, 1>;
-    case 1: return (const void*)&k_verify<DT, 2>;
-    case 2: return (const void*)&k_verify<DT, 4>;
-    case 3: return (const void*)&k_verify<DT, 8>;
-    case 4: return (const void*)&k_verify<DT, 12>;
-    case 5: return (const void*)&k_verify<DT, 16>;
-    default: return (const void*)&k_verify<DT, 20>;
-    }
-}
-
-// Team shape for a tree: aim for about 512 blocks in all, each holding a
-// segment of whole chunks in registers; G <= GMAX and every block of the
-// grid co-resident (cooperative launch).
-hipError_t verify_shape(const TreeDev& t, int* G_out, int* nv_idx, int* grid) {
+// Team shape for a tree: about `target` blocks in all (512 by default),
+// segments of whole chunks, G <= GMAX, every block co-resident (cooperative
+// launch).
+hipError_t verify_shape(const TreeDev& t, int* G_out, int* segch, int* grid) {
     const int VEC = t.dtype ? 8 : 4;
     const int NC = (t.V + WAVE * VEC - 1) / (WAVE * VEC);
     const char* env = getenv("RHEO_VERIFY_BLOCKS");
-    int Gd = (env ? atoi(env) : 512) / t.B;
-    if (Gd < 1) Gd = 1;
-    if (Gd > 16) Gd = 16;
-    int vi = kVN - 1;
-    for (int v = 0; v < kVN; ++v)
-        if (kVNV[v] * NWV * Gd >= NC) { vi = v; break; }
-    int G = (NC + kVNV[vi] * NWV - 1) / (kVNV[vi] * NWV);
-    if (G > GMAX) return hipErrorInvalidValue;
+    const int target = env ? atoi(env) : 512;
     int dev = 0, cus = 0, per_cu = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-    const void* fn = t.dtype ? verify_fn<1>(vi) : verify_fn<0>(vi);
+    const void* fn = t.dtype ? (const void*)&k_verify<1> : (const void*)&k_verify<0>;
     if (e == hipSuccess) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, NTV, 0);
     if (e != hipSuccess) return e;
     const int teams_per_xcd = (t.B + 7) / 8;
+    int G = target / (8 * teams_per_xcd);
+    if (G > GMAX) G = GMAX;
+    if (G > NC) G = NC;
+    while (G > 1 && 8 * teams_per_xcd * G > per_cu * cus) --G;
+    if (G < 1) G = 1;
     const int blocks = 8 * teams_per_xcd * G;
     if (blocks > per_cu * cus) return hipErrorCooperativeLaunchTooLarge;
     *G_out = G;
-    *nv_idx = vi;
+    *segch = (NC + G - 1) / G;
     *grid = blocks;
     return hipSuccess;
 }
 
-hipError_t launch_verify(const TreeDev& t, const VerifyArgs& a, int nv_idx, int grid,
+hipError_t launch_verify(const TreeDev& t, const VerifyArgs& a, int segch, int grid,
                          hipStream_t s) {
-    const void* fn = t.dtype ? verify_fn<1>(nv_idx) : verify_fn<0>(nv_idx);
+    const void* fn = t.dtype ? (const void*)&k_verify<1> : (const void*)&k_verify<0>;
     TreeDev tt = t;
     VerifyArgs aa = a;
-    aa.NV = kVNV[nv_idx];
+    aa.NV = segch;
     void* args[] = {&tt, &aa};
     return hipLaunchCooperativeKernel(fn, dim3(grid), dim3(NTV), args, 0, s);
 }
