@@ -37,6 +37,60 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+KERNEL_SRCS = ["expand.hip", "rheo_device.h", "rheo_state.h"]
+
+
+def kernel_src_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SRCS:
+        with open(os.path.join(ROOT, "paper_2609_21827_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def _counter_rows(path, regex, counter):
+    """Per-dispatch values (KiB) of one counter for kernels matching regex."""
+    import csv
+    import re
+    vals = {}
+    with open(path) as f:
+        for row in csv.DictReader(f):
+            if row["Counter_Name"] == counter and re.search(regex, row["Kernel_Name"]):
+                key = row.get("Dispatch_Id") or row.get("Correlation_Id")
+                vals[key] = vals.get(key, 0.0) + float(row["Counter_Value"])
+    return list(vals.values())
+
+
+def write_traffic(paths, out, workload, copy_bytes):
+    """Scales the expand kernel's FETCH_SIZE / WRITE_SIZE by what the same
+    counters read for a plain device copy of known size."""
+    exp_f, exp_w, cp_f, cp_w = paths
+    ef = _counter_rows(exp_f, r"k_expand", "FETCH_SIZE")
+    ew = _counter_rows(exp_w, r"k_expand", "WRITE_SIZE")
+    cf = _counter_rows(cp_f, r"copy|Copy", "FETCH_SIZE")
+    cw = _counter_rows(cp_w, r"copy|Copy", "WRITE_SIZE")
+    # every copy dispatch moves copy_bytes in and copy_bytes out
+    k_f = copy_bytes / (sum(cf) / len(cf) * 1024)
+    k_w = copy_bytes / (sum(cw) / len(cw) * 1024)
+    fetch = sum(ef) / len(ef) * 1024 * k_f
+    write = sum(ew) / len(ew) * 1024 * k_w
+    res = {"workload": workload, "kernel": "k_expand",
+           "kernel_src_sha256": kernel_src_hash(),
+           "dispatches": len(ef), "copy_dispatches": len(cf),
+           "copy_bytes": copy_bytes,
+           "copy_fetch_kib": sum(cf) / len(cf), "copy_write_kib": sum(cw) / len(cw),
+           "scale_fetch": k_f, "scale_write": k_w,
+           "fetch_kib_per_launch": sum(ef) / len(ef),
+           "write_kib_per_launch": sum(ew) / len(ew),
+           "bytes_per_launch": int(fetch + write),
+           "fetch_bytes_per_launch": int(fetch), "write_bytes_per_launch": int(write)}
+    with open(out, "w") as f:
+        json.dump(res, f, indent=1)
+        f.write("\n")
+    print(json.dumps(res))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -46,8 +100,21 @@ def main():
     ap.add_argument("--distinct", type=int, default=4, help="recorded steps cycled over")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu", action="store_true")
-    ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"))
+    ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles",
+                                                      "k_expand_headline_traffic.json"))
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB five times "
+                         "(counter calibration under rocprofv3 --pmc)")
+    ap.add_argument("--traffic-from", nargs=4, default=None,
+                    metavar=("EXP_FETCH", "EXP_WRITE", "COPY_FETCH", "COPY_WRITE"),
+                    help="write the traffic file from four rocprofv3 --pmc "
+                         "counter_collection.csv files, then exit")
     args = ap.parse_args()
+
+    if args.traffic_from:
+        assert args.copy_probe, "--traffic-from needs the --copy-probe size that was profiled"
+        write_traffic(args.traffic_from, args.traffic, args.workload, args.copy_probe << 20)
+        return
 
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for {args.gpus}); "
@@ -55,10 +122,20 @@ def main():
         sys.exit(2)
 
     import torch
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.copy_probe:
+        n = args.copy_probe << 20
+        src = torch.randint(0, 255, (n,), dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": n, "copies": 5}), flush=True)
+        return
+
     import synth
     from paper_2609_21827_amd.driver import make_tree, run_step
 
-    assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = "cuda"
     w = synth.WORKLOADS[args.workload]
     esz = w.elem_bytes
@@ -100,12 +177,15 @@ def main():
         tree.verify(rec["target"], rec["T"], rec["rng_key"], out=ob, stream=stream)
 
     # ---- 2. timed replay ---------------------------------------------------
+    def check(n_replayed):
+        for i in range(min(n_replayed, len(recs))):
+            for a, b in zip(out_bufs[i], outs[i]):
+                assert torch.equal(a.cpu(), b.cpu()), "replay differs from discovery"
+
     for i in range(args.warmup):
         replay(i)
     torch.cuda.synchronize()
-    for i in range(len(recs)):
-        for a, b in zip(out_bufs[i], outs[i]):
-            assert torch.equal(a.cpu(), b), "replay differs from discovery"
+    check(args.warmup)
     ev = [[[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)]
            for _ in range(w.depth)] for _ in range(args.steps)]
     torch.cuda.synchronize()
@@ -114,6 +194,8 @@ def main():
         replay(i, ev[i])
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    check(args.steps)
+    assert tree.device_error() == 0
     ms = (t1 - t0) * 1e3 / args.steps
     steps_per_s = args.steps / (t1 - t0)
 
@@ -135,11 +217,13 @@ def main():
     lvl_us = [sum(exp_ms[i][d] for i in range(args.steps)) * 1e3 / args.steps
               for d in range(w.depth)]
 
+    # HBM bytes per launch from the committed counter runs, only while the
+    # kernel sources still hash to what was profiled
     traffic = None
     if os.path.exists(args.traffic):
         with open(args.traffic) as f:
             tr = json.load(f)
-        if tr.get("workload") == w.name:
+        if tr.get("workload") == w.name and tr.get("kernel_src_sha256") == kernel_src_hash():
             traffic = tr.get("bytes_per_launch")
 
     # ---- 4. CPU oracle baseline --------------------------------------------

@@ -159,7 +159,9 @@ int rheo_read_nodes(rheo_tree* tree, int32_t* token, int32_t* parent,
  * *host_flag (0 = no error; bit 0: no sampled token found, bit 1: pruned
  * tree not ancestor-closed, bit 2: sampled child missing from its parent's
  * tail, bit 3: residual sample out of range, bit 4: corrupt frontier,
- * bit 5: corrupt verification walk, bit 6: invalid launch shape).
+ * bit 5: corrupt verification walk, bit 6: invalid launch shape, bit 7:
+ * verification team barrier timed out, bit 8: a support slot left empty by
+ * the expand merge).
  * Diagnostic only. */
 int rheo_device_error(rheo_tree* tree, int32_t* host_flag);
 

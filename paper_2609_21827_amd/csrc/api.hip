@@ -124,23 +124,35 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
         delete t;
         return fail(RHEO_EINVAL, "tree too large (%d nodes per sequence)", d.NN);
     }
-    // expand variant: the smallest register footprint that holds a whole row
+    // expand variant: 16 vectors per thread and chunk unless the chunk lists
+    // would not fit the merge; RHEO_EXPAND_VARIANT picks another that fits
     t->variant = -1;
-    for (int v = 0; v < expand_variant_count(c.dtype); ++v) {
-        const ExpandVariant ev = expand_variant(c.dtype, v);
-        if ((int64_t)ev.nt * ev.ept >= c.vocab) {
+    for (int v = 2; v < expand_variant_count(c.dtype); ++v) {
+        if (expand_variant(c.dtype, v, c.vocab, S).ok) {
             t->variant = v;
             break;
         }
     }
     if (t->variant < 0) {
         delete t;
-        return fail(RHEO_EINVAL, "vocab %d exceeds the largest row the expand kernel holds", c.vocab);
+        return fail(RHEO_EINVAL, "vocab %d with support %d exceeds the expand merge capacity",
+                    c.vocab, S);
     }
     const char* env = getenv("RHEO_EXPAND_VARIANT");
     if (env) {
         const int v = atoi(env);
-        if (v >= t->variant && v < expand_variant_count(c.dtype)) t->variant = v;
+        if (v >= 0 && v < expand_variant_count(c.dtype) &&
+            expand_variant(c.dtype, v, c.vocab, S).ok)
+            t->variant = v;
+    }
+    {
+        const ExpandVariant ev = expand_variant(c.dtype, t->variant, c.vocab, S);
+        d.C = ev.C;
+        d.Sc = ev.Sc;
+        if (d.Sc != S) {   // chunks hold at least 4096 elements, supports at most 1024
+            delete t;
+            return fail(RHEO_EINVAL, "internal: expand chunk smaller than the support");
+        }
     }
     const size_t B = d.B, NN = d.NN, E = d.E;
     int rc = RHEO_OK;
@@ -166,6 +178,7 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
     rc = rc ? rc : dalloc(t, &d.team_max, B * 64);
     rc = rc ? rc : dalloc(t, &d.team_chunk, B * 1024);
     rc = rc ? rc : dalloc(t, &d.team_sp, B * (1024 + 16));
+    rc = rc ? rc : dalloc(t, &d.sel, B * d.NE * (size_t)d.C * d.Sc);
     if (rc) {
         free_all(t);
         delete t;

@@ -1,50 +1,44 @@
-// Level expansion of the draft tree: parent selection, top-S selection over
-// each draft-logit row, the node's distributions, the hybrid candidate pool
-// with its proxy and true probabilities.
+// Level expansion of the draft tree: top-S selection over each draft-logit
+// row, the node's distributions, the hybrid candidate pool with its proxy
+// and true probabilities, and the parent each row belongs to.
 //
-// One 1024-thread block handles one frontier row (rows = B * P), so no
-// block ever waits for another:
-//  * prologue (level >= 1): the block's parent is the j-th best child of the
-//    previous level by priority (Sec. 2.1; App. C.4 "expands exactly the K
-//    nodes with highest path scores"); it is ranked from the children records
-//    the previous launch wrote, while the row loads are in flight.
-//  * the row is streamed once from HBM into registers with 16-byte loads;
-//    each thread keeps its maximum.  Every wave sorts its 64 maxima; with
-//    c = ceil(S / waves), the smallest of the waves' c-th largest maxima is a
-//    threshold that at least S elements reach, so the row's top-S (logit
-//    desc, id asc) are among the elements at or above it (typically ~1.3 S).
-//    They are collected in LDS and ranked exactly.
-//  * the pool (Sec. 3.2; App. C.1) from the truncated distribution (Sec.
-//    3.2, sparse draft): construction weights q (untempered, Sec. 5.4),
-//    ranks by (q desc, id asc), tail q~_T = q_T / z on the support minus the
-//    top-m, Y ~ q~_T by inverse CDF over token ids, fills, proxies
-//    (min{q(x_m), z}; q(x_1) + eps for m = 0), true probability q~(Y), path
-//    scores (App. C.1).  The tail is stored id-sorted for verification.
+// Two kernels per level, neither waiting on another block:
+//  * k_select, one 256-thread block per (chunk, row): the chunk is streamed
+//    from HBM into registers with 16-byte loads.  Its exact top-Sc by
+//    (logit desc, id asc) is written, sorted, to the tree's selection
+//    scratch.  The row's top-S (Sc = min(S, chunk size)) is contained in
+//    the union of its chunks' top-Sc.  Within a chunk, a value that Sc
+//    per-vector maxima reach is a threshold at least Sc elements reach, so
+//    the chunk's top-Sc are among the few elements at or above it; they are
+//    collected in LDS and ranked exactly.  Many small blocks per CU keep
+//    loads in flight while other blocks rank.
+//  * k_pool, one 256-thread block per row: ranks the row's parent among the
+//    previous level's children (Sec. 2.1; App. C.4 "expands exactly the K
+//    nodes with highest path scores"), merges the chunk lists into the
+//    row's top-S support (Sec. 3.2, sparse draft distributions), and forms
+//    the pool (Sec. 3.2; App. C.1): construction weights q (untempered,
+//    Sec. 5.4), ranks by (q desc, id asc), the tail q~_T = q_T / z on the
+//    support minus the top-m, Y ~ q~_T by inverse CDF over token ids, fills,
+//    proxies (min{q(x_m), z}; q(x_1) + eps for m = 0), the true probability
+//    q~(Y), path scores (App. C.1).  The tail is stored id-sorted for
+//    verification.
 #include "rheo_device.h"
 #include "rheo_state.h"
 
 namespace rheo {
 
-constexpr int NT = 1024;
-constexpr int CAP = 1024;    // LDS candidate capacity
-constexpr int SMAX = 1024;   // largest support
-constexpr int NWAVE = NT / WAVE;
+constexpr int NTC = 256;      // k_select block
+constexpr int NTP = 256;      // k_pool block
+constexpr int CAPC = 1024;    // candidates a chunk collects in LDS
+constexpr int CAPV = 512;     // candidate vectors a chunk collects in LDS
+constexpr int SMAX = 1024;    // largest support
+constexpr int MERGE_MAX = 2048;  // chunk-list keys one row merges (C * Sc)
 
 template <int DT>
 __device__ __forceinline__ float elem(const uint4& v, int k) {
     const uint32_t* w = &v.x;
     if (DT) return (k & 1) ? bf_hi(w[k >> 1]) : bf_lo(w[k >> 1]);
     return __uint_as_float(w[k]);
-}
-
-// Element k of a vector for a k known only at run time (selects, so the
-// vector stays in registers).
-template <int DT>
-__device__ __forceinline__ float elem_dyn(const uint4& v, int k) {
-    const int wi = DT ? (k >> 1) : k;
-    const uint32_t w = wi == 0 ? v.x : wi == 1 ? v.y : wi == 2 ? v.z : v.w;
-    if (DT) return (k & 1) ? bf_hi(w) : bf_lo(w);
-    return __uint_as_float(w);
 }
 
 // Vector vi (VEC consecutive elements) of a row; elements past V read as -inf.
@@ -72,97 +66,54 @@ __device__ __forceinline__ uint4 load_row_vec(const char* base, int vi, int V) {
     return make_uint4(w[0], w[1], w[2], w[3]);
 }
 
-// Orders LDS accesses of the lanes of one wave (no block barrier).
-__device__ __forceinline__ void wave_sync() {
-    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-}
-
-template <int DT, int NV>
-__global__ __launch_bounds__(NT) void k_expand(TreeDev t, LevelArgs a) {
+// ---------------------------------------------------------------------------
+// k_select: the exact top-Sc of one chunk of one row
+// ---------------------------------------------------------------------------
+template <int DT, int NVC>
+__global__ __launch_bounds__(NTC) void k_select(TreeDev t, LevelArgs a) {
     constexpr int VEC = DT ? 8 : 4;
     constexpr int ESZ = DT ? 2 : 4;
-    constexpr int NM = DT ? (NV + 1) / 2 : NV;   // registers of per-vector maxima
+    constexpr int NM = DT ? (NVC + 1) / 2 : NVC;   // registers of per-vector maxima
 
-    __shared__ uint64_t s_keys[CAP];
-    __shared__ uint64_t s_top[SMAX];
-    __shared__ uint32_t s_w1[SMAX];
-    __shared__ uint32_t s_q[SMAX];
-    __shared__ int16_t s_rank[SMAX];
-    __shared__ int16_t s_wr[SMAX];     // support item -> rank by construction weight
-    __shared__ int16_t s_xs[SMAX];     // rank by construction weight -> support item
-    __shared__ int s_redi[NWAVE];
-    __shared__ int s_cnt, s_y, s_pu, s_yi;
-    __shared__ uint64_t s_u;
+    __shared__ uint64_t s_keys[CAPC];
+    __shared__ int16_t s_rank[CAPC];
+    __shared__ int s_bc[2][NTC / WAVE];
+    __shared__ uint32_t s_off[2 * NTC];
+    __shared__ uint32_t s_h;
+    __shared__ int s_redi[NTC / WAVE];
+    __shared__ uint4 s_cv[CAPV];                 // candidate vectors
+    __shared__ int s_cvi[CAPV];                  // their vector indices
+    __shared__ int s_cnt, s_nv;
 
     const int tid = threadIdx.x;
-    const int lane = tid % WAVE, wid = tid / WAVE;
-    const int row = blockIdx.x;
-    const int b = row / a.P;
-    const int j = row % a.P;
-    const int V = t.V, S = t.S, K = t.K, m = t.m;
-    const int level = a.level;
-    const int NE = t.NE, NN = t.NN;
-    const int64_t nb = (int64_t)b * NN;
+    const int c = blockIdx.x;
+    const int row = blockIdx.y;
+    const int V = t.V;
+    const int v0 = c * NTC * NVC;                           // first vector of the chunk
+    const int nvalid = min(V - v0 * VEC, NTC * NVC * VEC);  // >= 1: C = ceil(V / chunk)
+    const int nsel = min(t.Sc, nvalid);
     const char* base = (const char*)a.logits + (int64_t)row * t.stride * ESZ;
+    uint64_t* out = t.sel + ((int64_t)row * t.C + c) * t.Sc;
 
-    // ---- stream the row into registers -------------------------------------
-    uint4 r[NV];
+    uint4 r[NVC];
 #pragma unroll
-    for (int i = 0; i < NV; ++i) r[i] = load_row_vec<DT>(base, i * NT + tid, V);
-
-    // ---- prologue: this row's parent (ranked while the loads are in flight),
-    //      and the Philox draw of its sampled slot
+    for (int i = 0; i < NVC; ++i) r[i] = load_row_vec<DT>(base, v0 + i * NTC + tid, V);
     if (tid == 0) {
         s_cnt = 0;
-        s_pu = -1;
-    }
-    __syncthreads();
-    if (level == 0) {
-        if (tid == 0) s_pu = 0;
-    } else {
-        const int pcb = (level == 1) ? 1 : 1 + K + (level - 2) * NE * K;
-        const int n = ((level == 1) ? 1 : NE) * K;
-        uint64_t* s_hi = s_keys;
-        uint64_t* s_lo = s_top;
-        if (tid < n) {
-            const int64_t o = nb + pcb + tid;
-            uint64_t hi, lo;
-            prio_key(t.score[o], level, t.path[o], hi, lo);
-            s_hi[tid] = hi;
-            s_lo[tid] = lo;
-        }
-        __syncthreads();
-        if (tid < n) {
-            const uint64_t hi = s_hi[tid], lo = s_lo[tid];
-            int rk = 0;
-            for (int q = 0; q < n; ++q)
-                rk += (s_hi[q] > hi) || (s_hi[q] == hi && s_lo[q] > lo);
-            if (rk == j) s_pu = pcb + tid;
-        }
-    }
-    __syncthreads();
-    if (tid == 0) {
-        int pu = s_pu;
-        if (pu < 0 || pu >= NN) {
-            atomicOr(t.err, 16);
-            pu = 0;
-            s_pu = 0;
-        }
-        s_u = philox_draw(a.rng_key, P_DRAFT, (uint64_t)b, (uint64_t)pu);
+        s_nv = 0;
     }
 
-    // ---- per-vector maxima (exact) and this thread's maximum ----------------
-    // bf16: a packed word read as fp32 is its high element plus a fraction of
-    // one bf16 ulp (the low element's bits), so the maximum over the raw words
-    // and the unpacked low elements, with its low 16 bits cleared, is exactly
-    // the maximum element (logits are finite; padding words are NaN and ignored)
+    // per-vector maxima (exact) and this thread's maximum.  bf16: a packed
+    // word read as fp32 is its high element plus a fraction of one bf16 ulp
+    // (the low element's bits), so the maximum over the raw words and the
+    // unpacked low elements, with its low 16 bits cleared, is exactly the
+    // maximum element (logits are finite; padding words are NaN and ignored)
     uint32_t vm[NM];
 #pragma unroll
     for (int q = 0; q < NM; ++q) vm[q] = 0;
     float tmax = -INFINITY;
 #pragma unroll
-    for (int i = 0; i < NV; ++i) {
+    for (int i = 0; i < NVC; ++i) {
         float mx;
         if (DT) {
             const uint32_t* w = &r[i].x;
@@ -181,66 +132,145 @@ __global__ __launch_bounds__(NT) void k_expand(TreeDev t, LevelArgs a) {
         tmax = fmaxf(tmax, mx);
     }
 
-    // ---- threshold: each wave sorts its maxima and offers its top L; the
-    //      S-th largest offered value is reached by at least S elements
-    //      (usually it is the S-th largest maximum itself)
-    const int L = min(WAVE, 2 * ((S + NWAVE - 1) / NWAVE));
-    const float srt = wave_sort_desc(tmax);
-    float* s_off = (float*)s_w1;                 // NWAVE * L <= 1024 offered values
-    if (lane < L) s_off[wid * L + lane] = srt;
-    __syncthreads();
-    if (tid == 0) s_cnt = 0x7FFFFFFF;
-    __syncthreads();
-    {
-        const int n = NWAVE * L;
-        const int F = NT / n;                    // lanes per offered value (>= 1)
-        const int i = tid / F, sub = tid % F;
-        const float v = s_off[i];
-        int gt = 0;
-        for (int jj = sub; jj < n; jj += F) gt += s_off[jj] > v;
-        for (int o = 1; o < F; o <<= 1) gt += __shfl_xor(gt, o);
-        if (sub == 0 && gt < S) atomicMin(&s_cnt, (int)(ord32(v) ^ 0x80000000u));
-    }
-    __syncthreads();
-    float tau = unord32((uint32_t)s_cnt ^ 0x80000000u);
-    if (V <= CAP) tau = -INFINITY;
-    __syncthreads();
-    if (tid == 0) s_cnt = 0;
-    __syncthreads();
-
-    // ---- candidates >= tau: one compare per vector, a rare element scan ----
-    opaque_regs(r);
+    // threshold tau: at least nsel elements of the chunk are >= tau.  Every
+    // thread offers the 16-bit order-preserving codes of its two largest
+    // vector maxima; the largest code h that nsel offered codes reach gives
+    // tau = the smallest value with code h (each offered maximum is a
+    // distinct vector holding an element >= tau).  One wave finds h by
+    // bisection over the 2 * NTC offers.  Vectors past the row end read as
+    // -inf, so tau may fall to -inf: then every element of the chunk is a
+    // candidate.  Supports larger than the offers use all vector maxima.
+    const int lane = tid % WAVE, wid = tid / WAVE;
+    uint32_t c1 = 0, c2 = 0;
 #pragma unroll
-    for (int i = 0; i < NV; ++i) {
+    for (int i = 0; i < NVC; ++i) {
+        const float v = DT ? ((i & 1) ? bf_hi(vm[i / 2]) : bf_lo(vm[i / 2]))
+                           : __uint_as_float(vm[i]);
+        const uint32_t cv = ord32(v) >> 16;
+        c2 = max(c2, min(c1, cv));
+        c1 = max(c1, cv);
+    }
+    uint32_t h = 0;
+    if (nsel <= 2 * NTC) {
+        s_off[tid] = c1;
+        s_off[NTC + tid] = c2;
+        __syncthreads();
+        if (wid == 0) {
+            uint32_t o[2 * NTC / WAVE];
+#pragma unroll
+            for (int q = 0; q < 2 * NTC / WAVE; ++q) o[q] = s_off[q * WAVE + lane];
+#pragma unroll 1
+            for (int bit = 15; bit >= 0; --bit) {
+                const uint32_t cand = h | (1u << bit);
+                int n = 0;
+#pragma unroll
+                for (int q = 0; q < 2 * NTC / WAVE; ++q) n += __popcll(__ballot(o[q] >= cand));
+                if (n >= nsel) h = cand;
+            }
+            if (lane == 0) s_h = h;
+        }
+        __syncthreads();
+        h = s_h;
+    } else {
+#pragma unroll 1
+        for (int bit = 15; bit >= 0; --bit) {
+            const uint32_t cand = h | (1u << bit);
+            int n = 0;
+#pragma unroll
+            for (int i = 0; i < NVC; ++i) {
+                const float v = DT ? ((i & 1) ? bf_hi(vm[i / 2]) : bf_lo(vm[i / 2]))
+                                   : __uint_as_float(vm[i]);
+                n += (ord32(v) >> 16) >= cand;
+            }
+            n = wave_sum_i32(n);
+            if (lane == 0) s_bc[bit & 1][wid] = n;
+            __syncthreads();
+            int tot = 0;
+#pragma unroll
+            for (int w = 0; w < NTC / WAVE; ++w) tot += s_bc[bit & 1][w];
+            if (tot >= nsel) h = cand;
+        }
+    }
+    const float tau = (h << 16) > ord32(-INFINITY) ? unord32(h << 16) : -INFINITY;
+
+    // candidates >= tau in two compactions, so the per-element work touches
+    // only the few vectors whose maximum reaches tau: (1) every wave counts
+    // its candidate vectors with ballots, reserves LDS slots with one atomic
+    // and copies them there; (2) each thread scans whole candidate vectors
+    // and appends their elements >= tau the same way.
+    int wn = 0;
+#pragma unroll
+    for (int i = 0; i < NVC; ++i) {
         const float vmax = DT ? ((i & 1) ? bf_hi(vm[i / 2]) : bf_lo(vm[i / 2]))
                               : __uint_as_float(vm[i]);
-        if (vmax >= tau) {
-            const int e0 = (i * NT + tid) * VEC;
+        wn += __popcll(__ballot(vmax >= tau));
+    }
+    int wbase = 0;
+    if (lane == 0) wbase = atomicAdd(&s_nv, wn);
+    wbase = (int)lane_u32((uint32_t)wbase, 0);
+#pragma unroll
+    for (int i = 0; i < NVC; ++i) {
+        const float vmax = DT ? ((i & 1) ? bf_hi(vm[i / 2]) : bf_lo(vm[i / 2]))
+                              : __uint_as_float(vm[i]);
+        const bool take = vmax >= tau;
+        const uint64_t msk = __ballot(take);
+        if (take) {
+            const int pos = wbase + (int)__builtin_amdgcn_mbcnt_hi(
+                (uint32_t)(msk >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)msk, 0u));
+            if (pos < CAPV) {
+                s_cv[pos] = r[i];
+                s_cvi[pos] = v0 + i * NTC + tid;
+            }
+        }
+        wbase += __popcll(msk);
+    }
+    __syncthreads();
+    const int nv = s_nv;
+    if (nv <= CAPV) {
+        for (int j0 = 0; j0 < nv; j0 += NTC) {
+            const int j = j0 + tid;
+            uint4 x = make_uint4(0, 0, 0, 0);
+            int e0 = V;
+            if (j < nv) {
+                x = s_cv[j];
+                e0 = s_cvi[j] * VEC;
+            }
+            int n = 0;
+#pragma unroll
+            for (int k = 0; k < VEC; ++k) n += (elem<DT>(x, k) >= tau) & (e0 + k < V);
+            const int excl = wave_excl_scan(n);
+            int base = 0;
+            if (lane == WAVE - 1) base = atomicAdd(&s_cnt, excl + n);
+            int pos = (int)lane_u32((uint32_t)base, WAVE - 1) + excl;
 #pragma unroll
             for (int k = 0; k < VEC; ++k) {
-                const float v = elem<DT>(r[i], k);
-                const int id = e0 + k;
-                if (v >= tau && id < V) {
-                    const int pos = atomicAdd(&s_cnt, 1);
-                    if (pos < CAP) s_keys[pos] = logit_key(v, (uint32_t)id);
+                const float v = elem<DT>(x, k);
+                if (v >= tau && e0 + k < V) {
+                    if (pos < CAPC) s_keys[pos] = logit_key(v, (uint32_t)(e0 + k));
+                    ++pos;
                 }
             }
         }
+    } else if (tid == 0) {
+        s_cnt = CAPC + 1;                        // too many: exact fallback below
     }
     __syncthreads();
-    int c = s_cnt;
+    int cnt = s_cnt;
 
-    if (c > CAP) {
-        // Degenerate row (massive ties at the threshold): the S-th largest
-        // selection key, exactly, by bisection on the 64-bit key.  Rare, so
-        // it re-reads the row from memory rather than holding more registers.
-        const int nvec = (V + VEC - 1) / VEC;
+    if (cnt > CAPC) {
+        // Degenerate chunk (massive ties at the threshold): the nsel-th
+        // largest selection key, exactly, by bisection on the 64-bit key.
+        // Rare, so it re-reads the chunk from memory rather than holding more
+        // registers.
+        const int e_end = min(V, (v0 + NTC * NVC) * VEC);
         uint64_t x = 0;
         for (int bit = 63; bit >= 0; --bit) {
             const uint64_t cand = x | (1ull << bit);
             int n = 0;
 #pragma unroll 1
-            for (int vi = tid; vi < nvec; vi += NT) {
+            for (int i = 0; i < NVC; ++i) {
+                const int vi = v0 + i * NTC + tid;
+                if (vi * VEC >= e_end) continue;
                 const uint4 w = load_row_vec<DT>(base, vi, V);
 #pragma unroll
                 for (int k = 0; k < VEC; ++k) {
@@ -248,14 +278,16 @@ __global__ __launch_bounds__(NT) void k_expand(TreeDev t, LevelArgs a) {
                     n += (id < V) && (logit_key(elem<DT>(w, k), (uint32_t)id) >= cand);
                 }
             }
-            n = block_sum_i32<NT>(n, s_redi);
-            if (n >= S) x = cand;
+            n = block_sum_i32<NTC>(n, s_redi);
+            if (n >= nsel) x = cand;
         }
         __syncthreads();
         if (tid == 0) s_cnt = 0;
         __syncthreads();
 #pragma unroll 1
-        for (int vi = tid; vi < nvec; vi += NT) {
+        for (int i = 0; i < NVC; ++i) {
+            const int vi = v0 + i * NTC + tid;
+            if (vi * VEC >= e_end) continue;
             const uint4 w = load_row_vec<DT>(base, vi, V);
 #pragma unroll
             for (int k = 0; k < VEC; ++k) {
@@ -264,132 +296,242 @@ __global__ __launch_bounds__(NT) void k_expand(TreeDev t, LevelArgs a) {
                     const uint64_t key = logit_key(elem<DT>(w, k), (uint32_t)id);
                     if (key >= x) {
                         const int pos = atomicAdd(&s_cnt, 1);
-                        if (pos < CAP) s_keys[pos] = key;
+                        if (pos < CAPC) s_keys[pos] = key;
                     }
                 }
             }
         }
         __syncthreads();
-        c = min(s_cnt, CAP);
+        cnt = min(s_cnt, CAPC);
     }
 
-    // ---- exact top-S of the candidates (sorted by logit desc, id asc) -------
-    rank_keys<NT>(s_keys, c, s_rank);
+    // exact top-nsel of the candidates, written sorted; unused slots are 0
+    // (below every real key)
+    rank_keys<NTC>(s_keys, cnt, s_rank);
     __syncthreads();
-    for (int i = tid; i < c; i += NT) {
+    for (int i = tid; i < cnt; i += NTC) {
         const int rk = s_rank[i];
-        if (rk < S) s_top[rk] = s_keys[i];
+        if (rk < nsel) out[rk] = s_keys[i];
+    }
+    for (int i = nsel + tid; i < t.Sc; i += NTC) out[i] = 0ull;
+}
+
+// ---------------------------------------------------------------------------
+// k_pool: parent, support, distributions and pool of one row
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(NTP) void k_pool(TreeDev t, LevelArgs a) {
+    extern __shared__ uint64_t s_m[];            // the C chunk lists, C * Sc keys
+    __shared__ uint64_t s_top[SMAX];             // support by (logit desc, id asc)
+    __shared__ uint64_t s_k2[SMAX];              // ranking keys
+    __shared__ uint32_t s_w1[SMAX];              // construction weights
+    __shared__ __align__(8) uint32_t s_q[SMAX];  // tail weights (0 off the tail)
+    __shared__ int16_t s_wr[SMAX];               // item -> rank by (w1 desc, id asc)
+    __shared__ int16_t s_xs[SMAX];               // rank -> item
+    __shared__ int16_t s_ir[SMAX];               // item -> position in id order
+    __shared__ uint32_t s_tq[SMAX];              // tail weights in id order
+    __shared__ int16_t s_tx[SMAX];               // id order -> item
+    __shared__ uint64_t s_red[NTP / WAVE];
+    __shared__ int s_pu, s_yi;
+    __shared__ uint64_t s_u;
+
+    const int tid = threadIdx.x;
+    const int row = blockIdx.x;
+    const int b = row / a.P;
+    const int j = row % a.P;
+    const int S = t.S, K = t.K, m = t.m;
+    const int C = t.C, Sc = t.Sc;
+    const int level = a.level;
+    const int NE = t.NE, NN = t.NN;
+    const int64_t nb = (int64_t)b * NN;
+    uint64_t* s_ph = s_k2;                       // previous level's priority keys
+    uint64_t* s_pl = (uint64_t*)s_q;             // (free until the pool uses them)
+
+    // the chunk lists (coalesced) and, meanwhile, this row's parent: the j-th
+    // best child of the previous level by priority
+    const uint64_t* src = t.sel + (int64_t)row * C * Sc;
+    for (int i = tid; i < C * Sc; i += NTP) s_m[i] = src[i];
+    if (tid == 0) {
+        s_pu = (level == 0) ? 0 : -1;
+        s_yi = -1;
+    }
+    if (level > 0) {
+        const int pcb = (level == 1) ? 1 : 1 + K + (level - 2) * NE * K;
+        const int n = ((level == 1) ? 1 : NE) * K;      // <= 225
+        uint64_t u = 0;
+        if (tid < n) {
+            const int64_t o = nb + pcb + tid;
+            const double sc = t.score[o];
+            const uint64_t pa = t.path[o];
+            u = philox_draw(a.rng_key, P_DRAFT, (uint64_t)b, (uint64_t)(pcb + tid));
+            uint64_t hi, lo;
+            prio_key(sc, level, pa, hi, lo);
+            s_ph[tid] = hi;
+            s_pl[tid] = lo;
+        }
+        __syncthreads();
+        if (tid < n) {
+            const uint64_t hi = s_ph[tid], lo = s_pl[tid];
+            int rk = 0;
+#pragma unroll 8
+            for (int q = 0; q < n; ++q) {
+                const uint64_t h = s_ph[q], l = s_pl[q];
+                rk += (int)(h > hi) | ((int)(h == hi) & (int)(l > lo));
+            }
+            if (rk == j) {
+                s_pu = pcb + tid;
+                s_u = u;
+            }
+        }
+    } else if (tid == 0) {
+        s_u = philox_draw(a.rng_key, P_DRAFT, (uint64_t)b, 0ull);
+    }
+    __syncthreads();
+    if (tid == 0 && (s_pu < 0 || s_pu >= NN)) {
+        atomicOr(t.err, 16);
+        s_pu = 0;
+        s_u = philox_draw(a.rng_key, P_DRAFT, (uint64_t)b, 0ull);
+    }
+
+    // merge: pairs of sorted lists merge round by round until one list of
+    // the row's top S remains.  A key's position in the merged list is its
+    // position in its own list plus the count of larger keys in the partner
+    // list (one binary search); positions >= S are dropped.  Every list holds
+    // S keys (a chunk is larger than any support); keys are unique and 0
+    // marks an empty slot.  Each round computes all positions first, then
+    // rewrites the lists in place.
+    {
+        int pw2 = 1;
+        while (pw2 * 2 <= S) pw2 *= 2;
+        int nl = C;
+        while (nl > 1) {
+            const int npair = nl / 2, nout = (nl + 1) / 2;
+            uint64_t kv[MERGE_MAX / NTP];
+            int pv[MERGE_MAX / NTP];
+#pragma unroll
+            for (int q = 0; q < MERGE_MAX / NTP; ++q) {
+                const int e = tid + q * NTP;
+                pv[q] = -1;
+                kv[q] = 0ull;
+                if (e < nl * S) {
+                    const int l = e / S, i = e - l * S;
+                    const uint64_t key = s_m[e];
+                    if (l < 2 * npair) {
+                        const uint64_t* B = s_m + (l ^ 1) * S;
+                        int lo = 0;
+                        for (int half = pw2; half > 0; half >>= 1) {
+                            const uint64_t x = B[min(lo + half, S) - 1];
+                            lo += (lo + half <= S && x > key) ? half : 0;
+                        }
+                        if (i + lo < S) pv[q] = (l >> 1) * S + i + lo;
+                    } else {
+                        pv[q] = npair * S + i;          // the odd list passes through
+                    }
+                    kv[q] = key;
+                }
+            }
+            __syncthreads();
+            for (int i = tid; i < nout * S; i += NTP) s_m[i] = 0ull;
+            __syncthreads();
+#pragma unroll
+            for (int q = 0; q < MERGE_MAX / NTP; ++q)
+                if (pv[q] >= 0 && kv[q] != 0ull) s_m[pv[q]] = kv[q];
+            __syncthreads();
+            nl = nout;
+        }
+        for (int i = tid; i < S; i += NTP) s_top[i] = s_m[i];
+        __syncthreads();
+    }
+    for (int i = tid; i < S; i += NTP) {
+        if ((uint32_t)key_id(s_top[i]) >= (uint32_t)t.V) {   // a support slot left empty
+            atomicOr(t.err, 256);
+            s_top[i] = logit_key(-INFINITY, 0u);
+        }
     }
     __syncthreads();
 
-    // ---- the node's distributions and its pool: one wave; the other waves
-    //      leave, so the next row's block can start loading -------------------
-    if (wid != 0) return;
+    // construction weights (untempered unless asked), S1, rank by (w1 desc, id asc)
     const int pu = s_pu;
     const int cb = (level == 0) ? 1 : 1 + K + (level - 1) * NE * K;
     const int e_idx = (level == 0) ? 0 : 1 + (level - 1) * NE + j;
-    const int IPL = (S + WAVE - 1) / WAVE;       // support items per lane (<= 16)
     const float M = key_value(s_top[0]);
-    // construction weights (untempered unless asked), S1, rank by (w1 desc, id asc)
     uint64_t part = 0;
-    for (int q = 0; q < IPL; ++q) {
-        const int i = q * WAVE + lane;
-        if (i < S) {
-            const uint64_t tk = s_top[i];
-            const uint32_t w = cweight(key_value(tk), M, a.k1);
-            s_w1[i] = w;
-            s_keys[i] = ((uint64_t)w << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)key_id(tk));
-            part += w;
-        }
+    for (int i = tid; i < S; i += NTP) {
+        const uint64_t tk = s_top[i];
+        const uint32_t w = cweight(key_value(tk), M, a.k1);
+        s_w1[i] = w;
+        s_k2[i] = ((uint64_t)w << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)key_id(tk));
+        part += w;
     }
-    const uint64_t S1 = wave_sum_u64(part);
-    wave_sync();
-    for (int q = 0; q < IPL; ++q) {
-        const int i = q * WAVE + lane;
-        if (i < S) {
-            const uint64_t k = s_keys[i];
-            int rk = 0;
-            for (int jj = 0; jj < S; ++jj) rk += s_keys[jj] > k;
-            s_wr[i] = (int16_t)rk;
-            s_xs[rk] = (int16_t)i;
-        }
+    int tie = 0;
+    const uint64_t S1 = block_sum_u64<NTP>(part, s_red);
+    // The support is in (logit desc, id asc) order and the weight never
+    // grows along it, so ranks by (w1 desc, id asc) differ from positions
+    // only inside runs of equal weights.
+    for (int i = tid + 1; i < S; i += NTP) tie |= s_w1[i] == s_w1[i - 1];
+    if (__syncthreads_or(tie)) {
+        rank_keys<NTP>(s_k2, S, s_wr);
+    } else {
+        for (int i = tid; i < S; i += NTP) s_wr[i] = (int16_t)i;
     }
-    wave_sync();
+    __syncthreads();
+    for (int i = tid; i < S; i += NTP) s_xs[s_wr[i]] = (int16_t)i;
+    __syncthreads();
+
     // tail q~_T (relative to x_{m+1}), its total, and its order by token id
     const float ref_t = key_value(s_top[s_xs[m]]);
     part = 0;
-    for (int q = 0; q < IPL; ++q) {
-        const int i = q * WAVE + lane;
-        if (i < S) {
-            const bool tail = s_wr[i] >= m;
-            const uint64_t tk = s_top[i];
-            const uint32_t w = tail ? cweight(key_value(tk), ref_t, a.kT) : 0u;
-            s_q[i] = w;
-            part += w;
-            s_keys[i] = tail ? (uint64_t)(0xFFFFFFFFu - (uint32_t)key_id(tk)) + 1 : 0ull;
-        }
+    for (int i = tid; i < S; i += NTP) {
+        const bool tail = s_wr[i] >= m;
+        const uint64_t tk = s_top[i];
+        const uint32_t w = tail ? cweight(key_value(tk), ref_t, a.kT) : 0u;
+        s_q[i] = w;
+        part += w;
+        s_k2[i] = tail ? (uint64_t)(0xFFFFFFFFu - (uint32_t)key_id(tk)) + 1 : 0ull;
     }
-    const uint64_t Zq = wave_sum_u64(part);
-    wave_sync();
+    const uint64_t Zq = block_sum_u64<NTP>(part, s_red);
+    rank_keys<NTP>(s_k2, S, s_ir);
+    __syncthreads();
+    // id-sorted tail, written straight to the tree (q~ for verification)
     const int ntail = S - m;
-    for (int q = 0; q < IPL; ++q) {
-        const int i = q * WAVE + lane;
-        if (i < S && s_keys[i] != 0ull) {
-            const uint64_t k = s_keys[i];
-            int rk = 0;
-            for (int jj = 0; jj < S; ++jj) rk += s_keys[jj] > k;
-            s_rank[i] = (int16_t)rk;              // position in id order
-        }
-    }
-    wave_sync();
-    // id-sorted tail written straight to the tree (q~ for verification) and
-    // kept in LDS for the inverse CDF (s_keys is free again)
     const int64_t tail_base = ((int64_t)b * t.E + e_idx) * S;
-    for (int q = 0; q < IPL; ++q) {
-        const int i = q * WAVE + lane;
-        if (i < S && s_wr[i] >= m) {
-            const int idr = s_rank[i];
-            const int id = key_id(s_top[i]);
-            s_keys[idr] = ((uint64_t)(uint32_t)id << 32) | s_q[i];
-            t.tail_id[tail_base + idr] = id;
+    for (int i = tid; i < S; i += NTP) {
+        if (s_wr[i] >= m) {
+            const int idr = s_ir[i];
+            s_tq[idr] = s_q[i];
+            s_tx[idr] = (int16_t)i;
+            t.tail_id[tail_base + idr] = key_id(s_top[i]);
             t.tail_q[tail_base + idr] = s_q[i];
         }
     }
-    wave_sync();
-    // Y ~ q~_T: t = floor(U64 Zq / 2^64), the first id-ordered tail entry whose
-    // inclusive prefix exceeds t (each lane scans a contiguous block)
+    __syncthreads();
+
+    // Y ~ q~_T: t = floor(U64 Zq / 2^64), the first id-ordered tail entry
+    // whose inclusive prefix exceeds t (each thread scans a contiguous block)
     const uint64_t tt = __umul64hi(s_u, Zq);
-    const int lo = lane * IPL, hi = min(ntail, lo + IPL);
+    const int IPT = (ntail + NTP - 1) / NTP;
+    const int lo = min(ntail, tid * IPT), hi = min(ntail, lo + IPT);
     uint64_t mysum = 0;
-    for (int i = lo; i < hi; ++i) mysum += (uint32_t)s_keys[i];
-    const uint64_t incl = wave_incl_scan_u64(mysum);
-    uint64_t acc = incl - mysum;
-    if (lane == 0) s_y = -1;
-    wave_sync();
-    if (acc <= tt && tt < incl) {
+    for (int i = lo; i < hi; ++i) mysum += s_tq[i];
+    uint64_t total;
+    uint64_t acc = block_excl_scan_u64<NTP>(mysum, s_red, &total);
+    if (acc <= tt && tt < acc + mysum) {
         for (int i = lo; i < hi; ++i) {
-            const uint64_t w = (uint32_t)s_keys[i];
+            const uint64_t w = s_tq[i];
             if (tt < acc + w) {
-                s_y = (int)(s_keys[i] >> 32);
+                s_yi = s_tx[i];
                 break;
             }
             acc += w;
         }
     }
-    wave_sync();
-    const int ytok = s_y;
-    if (lane == 0) {
-        s_yi = s_xs[m];                        // unreachable fallback
-        if (ytok < 0) atomicOr(t.err, 1);
+    __syncthreads();
+    int yi = s_yi;
+    if (yi < 0) {
+        if (tid == 0) atomicOr(t.err, 1);
+        yi = s_xs[m];                            // unreachable fallback
     }
-    wave_sync();
-    for (int q = 0; q < IPL; ++q) {
-        const int i = q * WAVE + lane;
-        if (i < S && s_wr[i] >= m && key_id(s_top[i]) == ytok) s_yi = i;
-    }
-    wave_sync();
-    const int yi = s_yi;
-    if (lane == 0) {
+
+    if (tid == 0) {
         t.zq[(int64_t)b * t.E + e_idx] = Zq;
         t.first_child[nb + pu] = cb + j * K;
         t.exp_of[nb + pu] = e_idx;
@@ -403,9 +545,9 @@ __global__ __launch_bounds__(NT) void k_expand(TreeDev t, LevelArgs a) {
             t.path[nb] = 0;
         }
     }
-    // ---- the K children: top-m leads, Y, fills (App. C.1) ------------------
-    if (lane < K) {
-        const int s = lane;
+    // the K children: top-m leads, Y, fills (App. C.1)
+    if (tid < K) {
+        const int s = tid;
         const int yr = s_wr[yi];
         int item, kind;
         if (s < m) {
@@ -475,7 +617,11 @@ __global__ __launch_bounds__(256) void k_frontier(TreeDev t, int level, int P) {
     if (tid < n) {
         const uint64_t hi = s_hi[tid], lo = s_lo[tid];
         int rk = 0;
-        for (int q = 0; q < n; ++q) rk += (s_hi[q] > hi) || (s_hi[q] == hi && s_lo[q] > lo);
+#pragma unroll 8
+        for (int q = 0; q < n; ++q) {
+            const uint64_t h = s_hi[q], l = s_lo[q];
+            rk += (int)(h > hi) | ((int)(h == hi) & (int)(l > lo));
+        }
         if (rk < NE) {
             t.fr_parent[b * NE + rk] = tid / K;
             t.fr_token[b * NE + rk] = t.tok[nb + cb + tid];
@@ -483,31 +629,39 @@ __global__ __launch_bounds__(256) void k_frontier(TreeDev t, int level, int P) {
     }
 }
 
-// Registers per thread hold NV 16-byte vectors: a row must fit NT * NV * VEC.
-static const int kNV[] = {1, 2, 4, 8, 12, 16, 20};
+// 16-byte vectors per thread of k_select; a chunk is NTC * NVC vectors.
+static const int kNVC[] = {4, 8, 16, 32};
 
-int expand_variant_count(int) { return (int)(sizeof(kNV) / sizeof(kNV[0])); }
-ExpandVariant expand_variant(int dtype, int v) {
-    return ExpandVariant{NT, kNV[v] * (dtype ? 8 : 4)};
+int expand_variant_count(int) { return (int)(sizeof(kNVC) / sizeof(kNVC[0])); }
+
+ExpandVariant expand_variant(int dtype, int v, int V, int S) {
+    const int chunk = NTC * kNVC[v] * (dtype ? 8 : 4);
+    ExpandVariant ev;
+    ev.chunk = chunk;
+    ev.C = (V + chunk - 1) / chunk;
+    ev.Sc = S < chunk ? S : chunk;
+    ev.ok = (int64_t)ev.C * ev.Sc <= MERGE_MAX;
+    return ev;
 }
 
 template <int DT>
-static void launch_dt(const TreeDev& t, const LevelArgs& a, int v, dim3 grid, hipStream_t s) {
+static void launch_select(const TreeDev& t, const LevelArgs& a, int v, dim3 grid, hipStream_t s) {
     switch (v) {
-    case 0: k_expand<DT, 1><<<grid, NT, 0, s>>>(t, a); break;
-    case 1: k_expand<DT, 2><<<grid, NT, 0, s>>>(t, a); break;
-    case 2: k_expand<DT, 4><<<grid, NT, 0, s>>>(t, a); break;
-    case 3: k_expand<DT, 8><<<grid, NT, 0, s>>>(t, a); break;
-    case 4: k_expand<DT, 12><<<grid, NT, 0, s>>>(t, a); break;
-    case 5: k_expand<DT, 16><<<grid, NT, 0, s>>>(t, a); break;
-    default: k_expand<DT, 20><<<grid, NT, 0, s>>>(t, a); break;
+    case 0: k_select<DT, 4><<<grid, NTC, 0, s>>>(t, a); break;
+    case 1: k_select<DT, 8><<<grid, NTC, 0, s>>>(t, a); break;
+    case 2: k_select<DT, 16><<<grid, NTC, 0, s>>>(t, a); break;
+    default: k_select<DT, 32><<<grid, NTC, 0, s>>>(t, a); break;
     }
 }
 
 hipError_t launch_expand(const TreeDev& t, const LevelArgs& a, int variant, hipStream_t s) {
-    const dim3 grid(t.B * a.P);
-    if (t.dtype) launch_dt<1>(t, a, variant, grid, s);
-    else launch_dt<0>(t, a, variant, grid, s);
+    const int rows = t.B * a.P;
+    const dim3 grid(t.C, rows);
+    if (t.dtype) launch_select<1>(t, a, variant, grid, s);
+    else launch_select<0>(t, a, variant, grid, s);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    k_pool<<<rows, NTP, (size_t)t.C * t.Sc * sizeof(uint64_t), s>>>(t, a);
     return hipGetLastError();
 }
 

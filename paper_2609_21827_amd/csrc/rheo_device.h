@@ -112,20 +112,55 @@ __device__ __forceinline__ u128 mulhi_64x128(uint64_t a, u128 b) {
 // ---------------------------------------------------------------------------
 // wave / block reductions (wave64)
 // ---------------------------------------------------------------------------
+// Lane movement inside rows of 16 lanes (DPP): rotate right by N, and shift
+// right by N with zeros shifted in.  Reductions and scans built on them stay
+// in the vector ALU (no LDS round trip); all 64 lanes must be active.
+template <int N>
+__device__ __forceinline__ uint32_t row_ror(uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x120 + N, 0xF, 0xF, false);
+}
+template <int N>
+__device__ __forceinline__ uint32_t row_shr(uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x110 + N, 0xF, 0xF, true);
+}
+template <int N>
+__device__ __forceinline__ uint64_t row_ror64(uint64_t v) {
+    return ((uint64_t)row_ror<N>((uint32_t)(v >> 32)) << 32) | row_ror<N>((uint32_t)v);
+}
+template <int N>
+__device__ __forceinline__ uint64_t row_shr64(uint64_t v) {
+    return ((uint64_t)row_shr<N>((uint32_t)(v >> 32)) << 32) | row_shr<N>((uint32_t)v);
+}
+__device__ __forceinline__ uint32_t lane_u32(uint32_t v, int l) {
+    return (uint32_t)__builtin_amdgcn_readlane((int)v, l);
+}
+__device__ __forceinline__ uint64_t lane_u64(uint64_t v, int l) {
+    return ((uint64_t)lane_u32((uint32_t)(v >> 32), l) << 32) | lane_u32((uint32_t)v, l);
+}
+
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
-    return v;
+    uint32_t x = __float_as_uint(v);
+    x = __float_as_uint(fmaxf(__uint_as_float(x), __uint_as_float(row_ror<8>(x))));
+    x = __float_as_uint(fmaxf(__uint_as_float(x), __uint_as_float(row_ror<4>(x))));
+    x = __float_as_uint(fmaxf(__uint_as_float(x), __uint_as_float(row_ror<2>(x))));
+    x = __float_as_uint(fmaxf(__uint_as_float(x), __uint_as_float(row_ror<1>(x))));
+    return fmaxf(fmaxf(__uint_as_float(lane_u32(x, 0)), __uint_as_float(lane_u32(x, 16))),
+                 fmaxf(__uint_as_float(lane_u32(x, 32)), __uint_as_float(lane_u32(x, 48))));
 }
 __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-    return v;
+    v += row_ror64<8>(v);
+    v += row_ror64<4>(v);
+    v += row_ror64<2>(v);
+    v += row_ror64<1>(v);
+    return lane_u64(v, 0) + lane_u64(v, 16) + lane_u64(v, 32) + lane_u64(v, 48);
 }
 __device__ __forceinline__ int wave_sum_i32(int v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-    return v;
+    uint32_t x = (uint32_t)v;
+    x += row_ror<8>(x);
+    x += row_ror<4>(x);
+    x += row_ror<2>(x);
+    x += row_ror<1>(x);
+    return (int)(lane_u32(x, 0) + lane_u32(x, 16) + lane_u32(x, 32) + lane_u32(x, 48));
 }
 
 template <int NT>
@@ -169,14 +204,15 @@ __device__ int block_sum_i32(int v, int* sh) {
 
 // Exclusive prefix of v over the wave (lane order).
 __device__ __forceinline__ int wave_excl_scan(int v) {
-    const int l = threadIdx.x % WAVE;
-    int x = v;
-#pragma unroll
-    for (int o = 1; o < WAVE; o <<= 1) {
-        const int y = __shfl_up(x, o);
-        if (l >= o) x += y;
-    }
-    return x - v;
+    const int row = (threadIdx.x % WAVE) >> 4;
+    uint32_t x = (uint32_t)v;
+    x += row_shr<1>(x);
+    x += row_shr<2>(x);
+    x += row_shr<4>(x);
+    x += row_shr<8>(x);
+    const uint32_t r0 = lane_u32(x, 15), r1 = lane_u32(x, 31), r2 = lane_u32(x, 47);
+    x += (row >= 1 ? r0 : 0u) + (row >= 2 ? r1 : 0u) + (row >= 3 ? r2 : 0u);
+    return (int)x - v;
 }
 
 }  // namespace rheo
@@ -185,12 +221,13 @@ namespace rheo {
 
 // Wave-wide inclusive prefix sum of 64-bit values.
 __device__ __forceinline__ uint64_t wave_incl_scan_u64(uint64_t v) {
-    const int l = threadIdx.x % WAVE;
-#pragma unroll
-    for (int o = 1; o < WAVE; o <<= 1) {
-        const uint64_t y = __shfl_up(v, o);
-        if (l >= o) v += y;
-    }
+    const int row = (threadIdx.x % WAVE) >> 4;
+    v += row_shr64<1>(v);
+    v += row_shr64<2>(v);
+    v += row_shr64<4>(v);
+    v += row_shr64<8>(v);
+    const uint64_t r0 = lane_u64(v, 15), r1 = lane_u64(v, 31), r2 = lane_u64(v, 47);
+    v += (row >= 1 ? r0 : 0ull) + (row >= 2 ? r1 : 0ull) + (row >= 3 ? r2 : 0ull);
     return v;
 }
 
@@ -273,9 +310,10 @@ __device__ void rank_keys128(const uint64_t* hi, const uint64_t* lo, int n, int1
         int cnt = 0;
         if (i < n) {
             const uint64_t kh = hi[i], kl = lo[i];
+#pragma unroll 4
             for (int j = sub; j < n; j += F) {
-                const uint64_t h = hi[j];
-                cnt += (h > kh) || (h == kh && lo[j] > kl);
+                const uint64_t h = hi[j], l = lo[j];
+                cnt += (int)(h > kh) | ((int)(h == kh) & (int)(l > kl));
             }
         }
         for (int o = 1; o < F; o <<= 1) cnt += __shfl_xor(cnt, o);

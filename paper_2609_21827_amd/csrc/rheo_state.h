@@ -43,6 +43,9 @@ struct TreeDev {
     uint32_t* team_max;            // [B][GMAX] segment maxima (fp32 bits)
     uint64_t* team_chunk;          // [B][NCMAX] chunk totals of p's weights
     uint32_t* team_sp;             // [B][SPMAX] p's weights at the special tokens
+    // expansion: each row's C chunk lists of Sc selection keys, sorted
+    uint64_t* sel;                 // [B * NE][C][Sc]
+    int C, Sc;
 };
 
 struct LevelArgs {
@@ -75,10 +78,15 @@ hipError_t verify_shape(const TreeDev& t, int* G, int* segch, int* grid);
 hipError_t launch_verify(const TreeDev& t, const VerifyArgs& a, int segch, int grid,
                          hipStream_t s);
 
-// expand kernel variants: elements per thread x threads per block
-struct ExpandVariant { int nt, ept; };
+// expand kernel variants: the chunk each selection block holds in registers
+struct ExpandVariant {
+    int chunk;                     // elements per chunk
+    int C;                         // chunks per row
+    int Sc;                        // selection keys kept per chunk
+    bool ok;                       // the row's C * Sc keys fit the merge
+};
 int expand_variant_count(int dtype);
-ExpandVariant expand_variant(int dtype, int v);
+ExpandVariant expand_variant(int dtype, int v, int V, int S);
 
 }  // namespace rheo
 

@@ -98,6 +98,8 @@ def test_tiny_variants(dev, over):
     dict(V=5000, dtype="bf16", recipe="zipf", quantum=0.5, support=128, K=4, depth=3, R=12),
     dict(V=32000, dtype="f32", recipe="zipf", support=1024, K=8, depth=3, R=30),
     dict(V=4099, dtype="f32", recipe="zipf_t3", support=64, K=6, depth=5, R=40, B=2),
+    dict(V=128256, dtype="bf16", recipe="zipf", support=512, K=8, depth=2, R=10),
+    dict(V=70001, dtype="bf16", recipe="zipf", quantum=2.0, support=128, K=4, depth=2, R=6),
 ])
 def test_edge_shapes(dev, over):
     w = W["tiny"].with_(name="edge", sigma=1.5, sigma_t=0.8, **over)
@@ -129,11 +131,11 @@ def test_headline(dev):
 
 
 def test_launch_shape_independence(dev):
-    """Results do not depend on register tiling or verification team size."""
+    """Results do not depend on the expand chunk size or verification team size."""
     from paper_2609_21827_amd.driver import make_tree, run_step
     w = W["llama3"].with_(B=4)
     outs = []
-    for variant, vblocks in ((None, None), ("6", "4"), ("6", "64"), (None, "1024")):
+    for variant, vblocks in ((None, None), ("0", "4"), ("3", "64"), ("1", "1024")):
         env = {}
         if variant:
             env["RHEO_EXPAND_VARIANT"] = variant
