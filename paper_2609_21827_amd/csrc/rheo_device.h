@@ -294,30 +294,21 @@ __device__ void rank_keys(const uint64_t* keys, int n, int16_t* rank) {
     }
 }
 
-// rank[i] = number of (hi, lo) keys strictly greater than key i (unique
-// 128-bit keys in LDS), F consecutive lanes per key as in rank_keys.
+// rank[i] = number of 128-bit keys strictly greater than key i (unique keys
+// in LDS as {hi, lo} pairs).  One key per lane; every lane of a wave reads
+// the same key at the same time (LDS broadcast).
 template <int NT>
-__device__ void rank_keys128(const uint64_t* hi, const uint64_t* lo, int n, int16_t* rank) {
-    int npad = 1;
-    while (npad < n) npad <<= 1;
-    int F = NT / npad;
-    if (F < 1) F = 1;
-    if (F > WAVE) F = WAVE;
-    const int sub = threadIdx.x % F;
-    const int per = NT / F;
-    for (int base = 0; base < n; base += per) {
-        const int i = base + threadIdx.x / F;
+__device__ void rank_keys128(const ulonglong2* keys, int n, int16_t* rank) {
+    for (int base = 0; base < n; base += NT) {
+        const int i = base + threadIdx.x;
+        const ulonglong2 k = keys[i < n ? i : 0];
         int cnt = 0;
-        if (i < n) {
-            const uint64_t kh = hi[i], kl = lo[i];
-#pragma unroll 4
-            for (int j = sub; j < n; j += F) {
-                const uint64_t h = hi[j], l = lo[j];
-                cnt += (int)(h > kh) | ((int)(h == kh) & (int)(l > kl));
-            }
+#pragma unroll 8
+        for (int j = 0; j < n; ++j) {
+            const ulonglong2 x = keys[j];
+            cnt += (int)(x.x > k.x) | ((int)(x.x == k.x) & (int)(x.y > k.y));
         }
-        for (int o = 1; o < F; o <<= 1) cnt += __shfl_xor(cnt, o);
-        if (i < n && sub == 0) rank[i] = (int16_t)cnt;
+        if (i < n) rank[i] = (int16_t)cnt;
     }
 }
 

@@ -85,26 +85,44 @@ __device__ inline int find_sorted(const int32_t* ids, int n, int v, int* lb = nu
     return (lo < n && ids[lo] == v) ? lo : -1;
 }
 
-// 128-bit wave / block scans (values < 2^127).
-__device__ __forceinline__ u128 shfl_up_u128(u128 v, int o) {
-    const uint64_t lo = __shfl_up((uint64_t)v, o);
-    const uint64_t hi = __shfl_up((uint64_t)(v >> 64), o);
-    return ((u128)hi << 64) | lo;
+// 128-bit wave / block sums and scans (values < 2^127), on DPP row moves
+// with explicit carries between the 64-bit halves.
+__device__ __forceinline__ void add_u128(uint64_t& lo, uint64_t& hi, uint64_t blo, uint64_t bhi) {
+    const uint64_t n = lo + blo;
+    hi += bhi + (n < lo ? 1ull : 0ull);
+    lo = n;
 }
-__device__ __forceinline__ u128 shfl_xor_u128(u128 v, int o) {
-    const uint64_t lo = __shfl_xor((uint64_t)v, o);
-    const uint64_t hi = __shfl_xor((uint64_t)(v >> 64), o);
+__device__ __forceinline__ u128 wave_sum_u128(u128 v) {
+    uint64_t lo = (uint64_t)v, hi = (uint64_t)(v >> 64);
+    add_u128(lo, hi, row_ror64<8>(lo), row_ror64<8>(hi));
+    add_u128(lo, hi, row_ror64<4>(lo), row_ror64<4>(hi));
+    add_u128(lo, hi, row_ror64<2>(lo), row_ror64<2>(hi));
+    add_u128(lo, hi, row_ror64<1>(lo), row_ror64<1>(hi));
+    uint64_t rlo = lane_u64(lo, 0), rhi = lane_u64(hi, 0);
+    add_u128(rlo, rhi, lane_u64(lo, 16), lane_u64(hi, 16));
+    add_u128(rlo, rhi, lane_u64(lo, 32), lane_u64(hi, 32));
+    add_u128(rlo, rhi, lane_u64(lo, 48), lane_u64(hi, 48));
+    return ((u128)rhi << 64) | rlo;
+}
+__device__ __forceinline__ u128 wave_incl_scan_u128(u128 v) {
+    const int row = (threadIdx.x % WAVE) >> 4;
+    uint64_t lo = (uint64_t)v, hi = (uint64_t)(v >> 64);
+    add_u128(lo, hi, row_shr64<1>(lo), row_shr64<1>(hi));
+    add_u128(lo, hi, row_shr64<2>(lo), row_shr64<2>(hi));
+    add_u128(lo, hi, row_shr64<4>(lo), row_shr64<4>(hi));
+    add_u128(lo, hi, row_shr64<8>(lo), row_shr64<8>(hi));
+    const uint64_t l0 = lane_u64(lo, 15), h0 = lane_u64(hi, 15);
+    const uint64_t l1 = lane_u64(lo, 31), h1 = lane_u64(hi, 31);
+    const uint64_t l2 = lane_u64(lo, 47), h2 = lane_u64(hi, 47);
+    if (row >= 1) add_u128(lo, hi, l0, h0);
+    if (row >= 2) add_u128(lo, hi, l1, h1);
+    if (row >= 3) add_u128(lo, hi, l2, h2);
     return ((u128)hi << 64) | lo;
 }
 // exclusive scan across the block; *total receives the sum
 __device__ u128 block_excl_scan_u128(u128 v, u128* sh, u128* total) {
     const int l = threadIdx.x % WAVE, w = threadIdx.x / WAVE;
-    u128 inc = v;
-#pragma unroll
-    for (int o = 1; o < WAVE; o <<= 1) {
-        const u128 y = shfl_up_u128(inc, o);
-        if (l >= o) inc += y;
-    }
+    const u128 inc = wave_incl_scan_u128(v);
     __syncthreads();
     if (l == WAVE - 1) sh[w] = inc;
     __syncthreads();
@@ -116,6 +134,17 @@ __device__ u128 block_excl_scan_u128(u128 v, u128* sh, u128* total) {
     }
     *total = tot;
     return base + inc - v;
+}
+__device__ u128 block_sum_u128(u128 v, u128* sh) {
+    const int l = threadIdx.x % WAVE, w = threadIdx.x / WAVE;
+    v = wave_sum_u128(v);
+    __syncthreads();
+    if (l == 0) sh[w] = v;
+    __syncthreads();
+    u128 tot = 0;
+#pragma unroll
+    for (int i = 0; i < NWV; ++i) tot += sh[i];
+    return tot;
 }
 
 // Team barrier: publish this block's arrival at `epoch`, then wait until
@@ -169,7 +198,8 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
     __shared__ uint64_t s_red[NWV];
     __shared__ float s_redf[NWV];
     __shared__ int s_c_uid[16], s_c_tok[16], s_c_slot[16], s_c_tail[16], s_c_zero[16];
-    __shared__ int s_nc, s_spos, s_e, s_nt, s_mode, s_next, s_token, s_cstar;
+    __shared__ int s_nc, s_spos, s_mode, s_next, s_token, s_cstar;
+    __shared__ uint64_t s_U[16], s_Ufin;         // the layer's uniforms
     __shared__ u128 s_F, s_Zrem, s_tt;
     __shared__ float s_M;
     __shared__ int s_ok;
@@ -205,28 +235,39 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
             break;
         }
         const char* row = (const char*)a.logits + ((int64_t)b * (a.R + 1) + cur_p) * t.stride * ESZ;
-        // ---- this layer's candidates and stored tail ------------------------
-        if (tid == 0) {
-            int nc = 0, spos = -1;
-            const int fc = t.first_child[nb + cur];
-            if (fc >= 0) {
-                for (int sl = 0; sl < K; ++sl) {
-                    const int c = fc + sl;
-                    if (t.pidx[nb + c] > 0) {
-                        const int kind = (t.meta[nb + c] >> 16) & 0xFF;
-                        if (kind == SAMPLED) spos = nc;
-                        s_c_uid[nc] = c;
-                        s_c_tok[nc] = t.tok[nb + c];
-                        s_c_slot[nc] = sl + 1;
-                        s_c_zero[nc] = 0;
-                        ++nc;
-                    }
-                }
+        // ---- this layer's candidates (one lane per slot, compacted in slot
+        //      order) and all of the layer's uniforms ------------------------
+        const int fc = t.first_child[nb + cur];
+        const int e = t.exp_of[nb + cur];
+        const int nt = (fc >= 0) ? t.S - t.m : 0;
+        if (tid < WAVE) {
+            bool keep = false;
+            int kind = -1, tok = -1;
+            if (fc >= 0 && lane < K) {
+                keep = t.pidx[nb + fc + lane] > 0;
+                kind = (t.meta[nb + fc + lane] >> 16) & 0xFF;
+                tok = t.tok[nb + fc + lane];
             }
-            s_nc = nc;
-            s_spos = spos;
-            s_e = t.exp_of[nb + cur];
-            s_nt = (fc >= 0) ? t.S - t.m : 0;
+            const uint64_t msk = __ballot(keep);
+            const uint64_t smk = __ballot(keep && kind == SAMPLED);
+            if (keep) {
+                const int pos = (int)__builtin_amdgcn_mbcnt_hi(
+                    (uint32_t)(msk >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)msk, 0u));
+                s_c_uid[pos] = fc + lane;
+                s_c_tok[pos] = tok;
+                s_c_slot[pos] = lane + 1;
+                s_c_zero[pos] = 0;
+            }
+            if (lane == 0) {
+                s_nc = __popcll(msk);
+                s_spos = smk ? __popcll(msk & ((smk & (~smk + 1)) - 1)) : -1;
+            }
+            // draw j of this layer: j = 0 the sampled-token test, j = slot
+            // for the candidate tests; then the final sample
+            if (lane <= K)
+                s_U[lane] = philox_draw(a.rng_key, P_VERIFY, (uint64_t)b,
+                                        (uint64_t)(32 * level + lane)) >> 32;
+            if (lane == K + 1) s_Ufin = philox_draw(a.rng_key, P_FINAL, (uint64_t)b, (uint64_t)level);
         }
         // ---- 1. row maximum (each wave streams whole chunks of the segment) ----
         float mx = -INFINITY;
@@ -241,7 +282,6 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
             __hip_atomic_store(&tmax_x[g], __float_as_uint(mx), __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
         // the stored tail of q~ at this node (read-only tree data)
-        const int nt = s_nt, nc = s_nc, spos = s_spos, e = s_e;
         if (nt > 0) {
             const int64_t tb = ((int64_t)b * t.E + e) * t.S;
             for (int i = tid; i < nt; i += NTV) {
@@ -250,6 +290,7 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
             }
         }
         if (!team_barrier(flags, g, G, a.epoch + 2 * level + 1, t.err, &s_ok)) break;
+        const int nc = s_nc, spos = s_spos;
         if (tid < WAVE) {
             float v = -INFINITY;
             if (tid < G)
@@ -299,6 +340,7 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
         }
         for (int i = tid; i < nt + nc; i += NTV)
             s_tp[i] = __hip_atomic_load(&sp_x[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (tid < nc) s_c_tail[tid] = find_sorted(s_tid, nt, s_c_tok[tid]);
         const uint64_t Sp = block_sum_u64<NTV>(part, s_red);
         // ---- 3. Algorithm 1 at this layer -----------------------------------
         const uint64_t Zq = (nt > 0) ? t.zq[(int64_t)b * t.E + e] : 1;
@@ -306,14 +348,12 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
             int mode = 0;          // 0: residual tests follow, 1: accepted, 2: final sample
             int next = -1, token = -1;
             if (nc == 0) mode = 2;
-            for (int ci = 0; ci < nc; ++ci) s_c_tail[ci] = find_sorted(s_tid, nt, s_c_tok[ci]);
             if (spos >= 0) {
                 const int yi = s_c_tail[spos];
                 if (yi < 0) atomicOr(t.err, 4);
                 const uint64_t QY = (yi >= 0) ? s_tq[yi] : 0;
                 const uint64_t PY = s_tp[nt + spos];
-                const uint64_t U = philox_draw(a.rng_key, P_VERIFY, (uint64_t)b,
-                                               (uint64_t)(32 * level)) >> 32;
+                const uint64_t U = s_U[0];
                 if ((u128)(U + 1) * QY * Sp <= (((u128)PY * Zq) << 32)) {
                     mode = 1;
                     next = s_c_uid[spos];
@@ -334,8 +374,7 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
                 const u128 pz = (u128)s_tp[i] * Zq, qs = (u128)s_tq[i] * Sp;
                 d += pz < qs ? pz : qs;
             }
-            u128 tot;
-            block_excl_scan_u128(d, s_w128, &tot);
+            const u128 tot = block_sum_u128(d, s_w128);
             if (tid == 0) s_Zrem = (u128)Zq * Sp - tot;
         } else if (tid == 0) {
             s_Zrem = Sp;
@@ -354,8 +393,7 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
                     const u128 pz = (u128)P * Zq, qs = (u128)s_tq[ti] * Sp;
                     Nu = pz > qs ? pz - qs : (u128)0;
                 }
-                const uint64_t U = philox_draw(a.rng_key, P_VERIFY, (uint64_t)b,
-                                               (uint64_t)(32 * level + s_c_slot[ci])) >> 32;
+                const uint64_t U = s_U[s_c_slot[ci]];
                 if ((u128)(U + 1) * Zrem <= (Nu << 32)) {
                     mode = 1;
                     next = s_c_uid[ci];
@@ -371,8 +409,7 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
             s_Zrem = Zrem;
         }
         if (tid == 0 && s_mode == 2) {
-            const uint64_t U = philox_draw(a.rng_key, P_FINAL, (uint64_t)b, (uint64_t)level);
-            s_tt = mulhi_64x128(U, s_Zrem);
+            s_tt = mulhi_64x128(s_Ufin, s_Zrem);
         }
         __syncthreads();
         if (s_mode == 1) {
@@ -446,26 +483,26 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
             if (tid == 0) atomicOr(t.err, 8);
             break;
         }
-        // scan of chunk cs: per-token residual weights, then a block scan
+        // scan of chunk cs: F * P for every token, then the special tokens
+        // (live tail tokens get their residual weight, zeroed candidates 0),
+        // then a block scan
         const u128 t2 = s_tt;
         for (int i = tid; i < CH; i += NTV) {
             const int v = cs * CH + i;
-            u128 w = 0;
-            if (v < V) {
-                const uint64_t P = cweight(load_logit<DT>(row, v), M, a.kT);
-                w = F * (u128)P;
-                if (residual) {
-                    const int ti = find_sorted(s_tid, nt, v);
-                    if (ti >= 0) {
-                        const u128 pz = (u128)P * Zq, qs = (u128)s_tq[ti] * Sp;
-                        w = pz > qs ? pz - qs : (u128)0;
-                    }
-                }
-                for (int ci = 0; ci < nc; ++ci)
-                    if (s_c_zero[ci] && s_c_tok[ci] == v) w = 0;
-            }
-            s_cn[i] = w;
+            s_cn[i] = (v < V) ? F * (u128)cweight(load_logit<DT>(row, v), M, a.kT) : (u128)0;
         }
+        __syncthreads();
+        if (residual) {
+            for (int i = tid; i < nt; i += NTV) {
+                const int v = s_tid[i];
+                if (v / CH == cs) {
+                    const u128 pz = (u128)s_tp[i] * Zq, qs = (u128)s_tq[i] * Sp;
+                    s_cn[v - cs * CH] = pz > qs ? pz - qs : (u128)0;
+                }
+            }
+        }
+        __syncthreads();
+        if (tid < nc && s_c_zero[tid] && s_c_tok[tid] / CH == cs) s_cn[s_c_tok[tid] - cs * CH] = 0;
         __syncthreads();
         constexpr int TPT = CH / NTV;          // tokens per thread (1 or 2)
         u128 mine = 0;
