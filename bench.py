@@ -154,13 +154,15 @@ def main():
 
     stream = torch.cuda.current_stream()
     out_bufs = [tuple(torch.empty_like(x, device=dev) for x in o) for o in outs]
-    fr_buf = tuple(torch.empty((w.B, w.n_expand), dtype=torch.int32, device=dev) for _ in range(2))
     pv_buf = tuple(torch.empty((w.B, w.R + 1), dtype=torch.int32, device=dev) for _ in range(2))
 
+    # the frontier each level chooses (which rows the draft model computes
+    # next) is read in place through these views: no call, no copy
+    fr_view = tree.frontier_view()
+
     def replay(i, events=None):
-        # the calls a serving loop makes: expand, frontier (which rows the
-        # draft model computes next), ..., prune, pruned view (which rows the
-        # target model computes), verify
+        # the calls a serving loop makes: expand (x depth), prune, pruned
+        # view (which rows the target model computes), verify
         rec = recs[i % len(recs)]
         ob = out_bufs[i % len(recs)]
         tree.begin_step()
@@ -170,8 +172,6 @@ def main():
             tree.expand_level(rows, rec["T"], rec["rng_key"], stream=stream)
             if events is not None:
                 events[d][1].record(stream)
-            if d + 1 < w.depth:
-                tree.frontier(out=fr_buf, stream=stream)
         tree.prune(w.R, stream=stream)
         tree.pruned_view(out=pv_buf, stream=stream)
         tree.verify(rec["target"], rec["T"], rec["rng_key"], out=ob, stream=stream)

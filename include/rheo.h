@@ -113,13 +113,24 @@ int rheo_begin_step(rheo_tree* tree);
 int rheo_expand_level(rheo_tree* tree, const void* draft_logits, float T,
                       uint64_t rng_key, void* stream);
 
-/* The frontier chosen by the last rheo_expand_level, in rank order:
+/* The frontier chosen by the last rheo_expand_level, in rank order, copied
+ * into caller buffers on `stream`:
  *   parent_index  [B][n_expand] int32: index of the node's parent in the
  *                 previous frontier (0 at level 1)
  *   token         [B][n_expand] int32: the node's token
- * (device pointers; either may be NULL). */
+ * (device pointers; either may be NULL).  Valid below the last level.
+ * RHEO_ESTATE if no level below the last has been expanded in this step. */
 int rheo_frontier(rheo_tree* tree, int32_t* parent_index, int32_t* token,
                   void* stream);
+
+/* The same frontier without a copy: *parent_index and *token receive the
+ * tree-owned device arrays ([B][n_expand] int32 each, layout as above).  The
+ * pointers stay fixed for the life of the handle; their contents are those
+ * of the last rheo_expand_level below the last level, once that call's
+ * work has run on its stream, until the next such call.  Host-only: no
+ * device work, no synchronisation. */
+int rheo_frontier_view(const rheo_tree* tree, const int32_t** parent_index,
+                       const int32_t** token);
 
 /* Keeps the budget R best non-root nodes (1 <= R <= K + (D-1) n_expand K) by
  * path score, ties by depth (shallower first) then left-to-right sibling

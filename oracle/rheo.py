@@ -12,7 +12,7 @@ One *step* for one sequence is
      "Dual treatment"; App. C.1 proxy list).  Path score = product of the
      proxies along the root-to-node path (App. C.1).  The next level expands
      the n_expand new nodes with the highest path scores (Sec. 2.1; App.
-     C.4 Step 1: "expands exactly the K nodes with highest path scores").
+     C.4, step 1, where the K best-scoring nodes are the ones expanded).
   2. global top-R pruning by path score, ties broken by depth (shallower
      first) and then left-to-right sibling order (App. C.1, "Tie-breaking
      rule"), which keeps the pruned tree ancestor-closed.

@@ -21,7 +21,7 @@ ERROR_NAMES = {RHEO_EINVAL: "EINVAL", RHEO_ENOMEM: "ENOMEM", RHEO_EHIP: "EHIP",
 
 # every symbol the header declares
 EXPORTS = ["rheo_create", "rheo_destroy", "rheo_begin_step", "rheo_expand_level",
-           "rheo_frontier", "rheo_prune", "rheo_pruned_view", "rheo_verify",
+           "rheo_frontier", "rheo_frontier_view", "rheo_prune", "rheo_pruned_view", "rheo_verify",
            "rheo_read_nodes", "rheo_device_error", "rheo_node_count",
            "rheo_last_error"]
 
@@ -60,6 +60,7 @@ def load_library(path=LIB_PATH):
         "rheo_begin_step": ([vp], ctypes.c_int),
         "rheo_expand_level": ([vp, vp, f32, u64, vp], ctypes.c_int),
         "rheo_frontier": ([vp, vp, vp, vp], ctypes.c_int),
+        "rheo_frontier_view": ([vp, ctypes.POINTER(vp), ctypes.POINTER(vp)], ctypes.c_int),
         "rheo_prune": ([vp, i32, vp], ctypes.c_int),
         "rheo_pruned_view": ([vp, vp, vp, vp], ctypes.c_int),
         "rheo_verify": ([vp, vp, f32, u64, vp, vp, vp, vp], ctypes.c_int),
@@ -89,6 +90,19 @@ def _stream(stream):
     if stream is None:
         stream = torch.cuda.current_stream()
     return ctypes.c_void_p(stream.cuda_stream)
+
+
+class _CudaArray:
+    """A device int32 array exposed through __cuda_array_interface__."""
+
+    def __init__(self, ptr, shape):
+        self.__cuda_array_interface__ = {"shape": tuple(shape), "typestr": "<i4",
+                                         "data": (int(ptr), False), "version": 3,
+                                         "strides": None}
+
+
+def _device_view(ptr, shape, device):
+    return torch.as_tensor(_CudaArray(ptr, shape), device=device)
 
 
 class Tree:
@@ -138,6 +152,15 @@ class Tree:
         par, tok = out
         _check(_LIB.rheo_frontier(self._h, _ptr(par), _ptr(tok), _stream(stream)))
         return par, tok
+
+    def frontier_view(self):
+        """The tree-owned frontier arrays as int32 [B, n_expand] tensors
+        (zero-copy views; contents change with every expand below the last
+        level)."""
+        par, tok = ctypes.c_void_p(), ctypes.c_void_p()
+        _check(_LIB.rheo_frontier_view(self._h, ctypes.byref(par), ctypes.byref(tok)))
+        return (_device_view(par.value, (self.B, self.NE), self.device),
+                _device_view(tok.value, (self.B, self.NE), self.device))
 
     def prune(self, budget, stream=None):
         _check(_LIB.rheo_prune(self._h, int(budget), _stream(stream)))

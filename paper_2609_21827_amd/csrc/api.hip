@@ -47,7 +47,6 @@ struct rheo_tree {
     int R = 0;
     int variant = 0;
     int vG = 1, v_segch = 1, v_grid = 1;  // verification team shape
-    uint32_t verify_calls = 0;
     float T_expand = 1.0f;
     void* blocks[32] = {};
     int nblocks = 0;
@@ -169,23 +168,30 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
     rc = rc ? rc : dalloc(t, &d.tail_q, B * E * S);
     rc = rc ? rc : dalloc(t, &d.zq, B * E);
     rc = rc ? rc : dalloc(t, &d.frontier, B * d.NE);
+    rc = rc ? rc : dalloc(t, &d.fr_u, B * d.NE);
     rc = rc ? rc : dalloc(t, &d.fr_parent, B * d.NE);
     rc = rc ? rc : dalloc(t, &d.fr_token, B * d.NE);
     rc = rc ? rc : dalloc(t, &d.pidx, B * NN);
     rc = rc ? rc : dalloc(t, &d.porder, B * NN);
     rc = rc ? rc : dalloc(t, &d.err, 1);
     rc = rc ? rc : dalloc(t, &d.team_flag, B * 64);
+    rc = rc ? rc : dalloc(t, &d.team_epoch, B);
     rc = rc ? rc : dalloc(t, &d.team_max, B * 64);
     rc = rc ? rc : dalloc(t, &d.team_chunk, B * 1024);
     rc = rc ? rc : dalloc(t, &d.team_sp, B * (1024 + 16));
     rc = rc ? rc : dalloc(t, &d.sel, B * d.NE * (size_t)d.C * d.Sc);
+    rc = rc ? rc : dalloc(t, &d.row_cnt, B * d.NE);
+    rc = rc ? rc : dalloc(t, &d.seq_cnt, B);
     if (rc) {
         free_all(t);
         delete t;
         return rc;
     }
     hipError_t e = hipMemset(d.err, 0, sizeof(int32_t));
-    if (e == hipSuccess) e = hipMemset(d.team_flag, 0, B * 64 * sizeof(uint32_t));
+    if (e == hipSuccess) e = hipMemset(d.team_flag, 0, B * 64 * sizeof(uint64_t));
+    if (e == hipSuccess) e = hipMemset(d.team_epoch, 0, B * sizeof(uint64_t));
+    if (e == hipSuccess) e = hipMemset(d.row_cnt, 0, B * d.NE * sizeof(uint32_t));
+    if (e == hipSuccess) e = hipMemset(d.seq_cnt, 0, B * sizeof(uint32_t));
     if (e == hipSuccess) e = hipMemset(d.pidx, 0xFF, B * NN * sizeof(int32_t));
     if (e == hipSuccess) e = hipMemset(d.frontier, 0, B * d.NE * sizeof(int32_t));
     if (e == hipSuccess) e = hipMemset(d.first_child, 0xFF, B * NN * sizeof(int32_t));
@@ -247,13 +253,22 @@ int rheo_frontier(rheo_tree* t, int32_t* parent_index, int32_t* token, void* str
     if (!t) return fail(RHEO_EINVAL, "NULL tree");
     if (t->state != EXPANDING || t->level < 1)
         return fail(RHEO_ESTATE, "no frontier: expand a level below the last first");
-    TreeDev d = t->dev;
-    // write straight into the caller's buffers (NULL: tree-owned scratch)
-    if (parent_index) d.fr_parent = parent_index;
-    if (token) d.fr_token = token;
-    const int level = t->level - 1;
-    const hipError_t e = launch_frontier(d, level, level == 0 ? 1 : d.NE, (hipStream_t)stream);
-    return e == hipSuccess ? RHEO_OK : hip_fail(e, "frontier launch");
+    const size_t bytes = (size_t)t->dev.B * t->dev.NE * sizeof(int32_t);
+    hipError_t e = hipSuccess;
+    if (parent_index)
+        e = hipMemcpyAsync(parent_index, t->dev.fr_parent, bytes, hipMemcpyDeviceToDevice,
+                           (hipStream_t)stream);
+    if (e == hipSuccess && token)
+        e = hipMemcpyAsync(token, t->dev.fr_token, bytes, hipMemcpyDeviceToDevice,
+                           (hipStream_t)stream);
+    return e == hipSuccess ? RHEO_OK : hip_fail(e, "frontier copy");
+}
+
+int rheo_frontier_view(const rheo_tree* t, const int32_t** parent_index, const int32_t** token) {
+    if (!t || !parent_index || !token) return fail(RHEO_EINVAL, "NULL argument");
+    *parent_index = t->dev.fr_parent;
+    *token = t->dev.fr_token;
+    return RHEO_OK;
 }
 
 int rheo_prune(rheo_tree* t, int32_t R, void* stream) {
@@ -291,15 +306,6 @@ int rheo_verify(rheo_tree* t, const void* logits, float T, uint64_t key, int32_t
     a.accept_len = accept_len;
     a.final_token = final_token;
     a.G = t->vG;
-    // team barrier epochs grow across calls; the flags restart on wrap-around
-    if (++t->verify_calls >= (1u << 26)) {
-        t->verify_calls = 1;
-        const hipError_t e0 = hipMemsetAsync(t->dev.team_flag, 0,
-                                             (size_t)t->dev.B * 64 * sizeof(uint32_t),
-                                             (hipStream_t)stream);
-        if (e0 != hipSuccess) return hip_fail(e0, "resetting verification flags");
-    }
-    a.epoch = t->verify_calls * 64u;
     const hipError_t e = launch_verify(t->dev, a, t->v_segch, t->v_grid, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "verify launch");
     t->state = VERIFIED;

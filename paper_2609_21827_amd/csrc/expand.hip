@@ -2,33 +2,36 @@
 // row, the node's distributions, the hybrid candidate pool with its proxy
 // and true probabilities, and the parent each row belongs to.
 //
-// Two kernels per level, neither waiting on another block:
+// Two kernels per level:
 //  * k_select, one 256-thread block per (chunk, row): the chunk is streamed
-//    from HBM into registers with 16-byte loads.  Its exact top-Sc by
+//    from HBM into registers with 16-byte loads and its exact top-Sc by
 //    (logit desc, id asc) is written, sorted, to the tree's selection
-//    scratch.  The row's top-S (Sc = min(S, chunk size)) is contained in
-//    the union of its chunks' top-Sc.  Within a chunk, a value that Sc
-//    per-vector maxima reach is a threshold at least Sc elements reach, so
-//    the chunk's top-Sc are among the few elements at or above it; they are
-//    collected in LDS and ranked exactly.  Many small blocks per CU keep
+//    scratch (Sc = S: a chunk is larger than any support).  The row's top-S
+//    lies in the union of its chunks' top-S.  Within a chunk, a value that
+//    Sc per-vector maxima reach is a threshold at least Sc elements reach,
+//    so the chunk's top-Sc are among the few elements at or above it; they
+//    are collected in LDS and ranked exactly.  Many small blocks per CU keep
 //    loads in flight while other blocks rank.
-//  * k_pool, one 256-thread block per row: ranks the row's parent among the
-//    previous level's children (Sec. 2.1; App. C.4 "expands exactly the K
-//    nodes with highest path scores"), merges the chunk lists into the
-//    row's top-S support (Sec. 3.2, sparse draft distributions), and forms
-//    the pool (Sec. 3.2; App. C.1): construction weights q (untempered,
-//    Sec. 5.4), ranks by (q desc, id asc), the tail q~_T = q_T / z on the
-//    support minus the top-m, Y ~ q~_T by inverse CDF over token ids, fills,
-//    proxies (min{q(x_m), z}; q(x_1) + eps for m = 0), the true probability
-//    q~(Y), path scores (App. C.1).  The tail is stored id-sorted for
-//    verification.
+//  * k_pool, one 256-thread block per row: takes the row's parent from the
+//    stored frontier, merges the chunk lists into the row's top-S support
+//    (Sec. 3.2, sparse draft distributions), and forms the pool (Sec. 3.2;
+//    App. C.1): construction weights q (untempered, Sec. 5.4), ranks by
+//    (q desc, id asc), the tail q~_T = q_T / z on the support minus the
+//    top-m, Y ~ q~_T by inverse CDF over token ids, fills, proxies
+//    (min{q(x_m), z}; q(x_1) + eps for m = 0), the true probability q~(Y),
+//    path scores (App. C.1).  The tail is stored id-sorted for verification.
+//    The last row of a sequence to finish (an arrival counter) ranks the
+//    level's new children by priority and stores the n_expand best, which
+//    the next level's rows expand (Sec. 2.1; App. C.4, step 1).
+// No block waits for another; children fields pass between blocks only
+// through agent-coherent atomic stores and loads.
 #include "rheo_device.h"
 #include "rheo_state.h"
 
 namespace rheo {
 
-constexpr int NTC = 256;      // k_select block
-constexpr int NTP = 256;      // k_pool block
+constexpr int NTC = 256;      // threads per k_select block
+constexpr int NTP = 256;      // threads per k_pool block
 constexpr int CAPC = 1024;    // candidates a chunk collects in LDS
 constexpr int CAPV = 512;     // candidate vectors a chunk collects in LDS
 constexpr int SMAX = 1024;    // largest support
@@ -67,23 +70,441 @@ __device__ __forceinline__ uint4 load_row_vec(const char* base, int vi, int V) {
 }
 
 // ---------------------------------------------------------------------------
+// the pool of one row, formed by the last of its chunk blocks: parent,
+// support, distributions and children
+// ---------------------------------------------------------------------------
+// LDS layout of the pool phase inside the block's dynamic buffer; the
+// previous level's priority keys (<= 225 of them) share the regions of the
+// support and the ranking keys.
+struct PoolLds {
+    int m, top, k2, w1, q, tq, wr, xs, ir, tx, bytes;
+};
+__host__ __device__ inline int pad16(int x) { return (x + 15) & ~15; }
+__host__ __device__ inline PoolLds pool_lds(int S, int C) {
+    PoolLds L;
+    const int S2 = S > 256 ? S : 256;
+    L.m = 0;
+    L.top = L.m + pad16(8 * C * S);
+    L.k2 = L.top + pad16(8 * S2);
+    L.w1 = L.k2 + pad16(8 * S2);
+    L.q = L.w1 + pad16(4 * S);
+    L.tq = L.q + pad16(4 * S);
+    L.wr = L.tq + pad16(4 * S);
+    L.xs = L.wr + pad16(2 * S);
+    L.ir = L.xs + pad16(2 * S);
+    L.tx = L.ir + pad16(2 * S);
+    L.bytes = L.tx + pad16(2 * S);
+    return L;
+}
+
+// Orders LDS accesses of the lanes of one wave (no block barrier).
+__device__ __forceinline__ void wave_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+}
+
+// Ranks of two keys at once (counts of larger keys among n unique keys in
+// LDS, 16-byte aligned); 16 keys per step keep eight loads in flight.
+__device__ __forceinline__ void count_greater2(const uint64_t* keys, int n, uint64_t k0,
+                                               uint64_t k1, int& c0, int& c1) {
+    const ulonglong2* kp = (const ulonglong2*)keys;
+    int a0 = 0, a1 = 0;
+    const int np = n >> 1;
+#pragma unroll 8
+    for (int j = 0; j < np; ++j) {
+        const ulonglong2 x = kp[j];
+        a0 += (int)(x.x > k0) + (int)(x.y > k0);
+        a1 += (int)(x.x > k1) + (int)(x.y > k1);
+    }
+    if (n & 1) {
+        const uint64_t x = keys[n - 1];
+        a0 += (int)(x > k0);
+        a1 += (int)(x > k1);
+    }
+    c0 = a0;
+    c1 = a1;
+}
+// Ranks (counts of larger keys) of keys[i] for i = tid, tid + NT, ...
+template <int NT>
+__device__ __forceinline__ void rank_all(const uint64_t* keys, int n, int16_t* rank) {
+    for (int i = threadIdx.x % NT; i < n; i += 2 * NT) {
+        const int i2 = i + NT;
+        int c0, c1;
+        count_greater2(keys, n, keys[i], i2 < n ? keys[i2] : ~0ull, c0, c1);
+        rank[i] = (int16_t)c0;
+        if (i2 < n) rank[i2] = (int16_t)c1;
+    }
+}
+
+// Synchronisation and sums over the NT threads that form a pool: one wave
+// (small supports) or the whole block.
+template <int NT>
+__device__ __forceinline__ void psync() {
+    if (NT == WAVE) wave_sync();
+    else __syncthreads();
+}
+template <int NT>
+__device__ __forceinline__ uint64_t psum(uint64_t v, uint64_t* sh) {
+    if (NT == WAVE) return wave_sum_u64(v);
+    return block_sum_u64<NT>(v, sh);
+}
+template <int NT>
+__device__ __forceinline__ bool pany(bool p) {
+    if (NT == WAVE) return __ballot(p) != 0ull;
+    return __syncthreads_or(p) != 0;
+}
+
+// The pool of one row from its merged support s_top (App. C.1), formed by
+// NT threads (tid < NT).  Children fields the frontier selection reads in
+// other blocks (token, score, path) are published with agent-scope atomics.
+template <int NT>
+__device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, int row,
+                                          uint8_t* lds, int pu, uint64_t u, uint64_t* s_red,
+                                          int* s_yi) {
+    const PoolLds L = pool_lds(t.S, t.C);
+    uint64_t* s_top = (uint64_t*)(lds + L.top);
+    uint64_t* s_k2 = (uint64_t*)(lds + L.k2);
+    uint32_t* s_w1 = (uint32_t*)(lds + L.w1);
+    uint32_t* s_q = (uint32_t*)(lds + L.q);
+    uint32_t* s_tq = (uint32_t*)(lds + L.tq);
+    int16_t* s_wr = (int16_t*)(lds + L.wr);
+    int16_t* s_xs = (int16_t*)(lds + L.xs);
+    int16_t* s_ir = (int16_t*)(lds + L.ir);
+    int16_t* s_tx = (int16_t*)(lds + L.tx);
+    const int tid = threadIdx.x;
+    const int b = row / a.P;
+    const int j = row % a.P;
+    const int S = t.S, K = t.K, m = t.m;
+    const int level = a.level;
+    const int NE = t.NE;
+    const int64_t nb = (int64_t)b * t.NN;
+
+    // construction weights (untempered unless asked), S1, rank by (w1 desc, id asc)
+    const int cb = (level == 0) ? 1 : 1 + K + (level - 1) * NE * K;
+    const int e_idx = (level == 0) ? 0 : 1 + (level - 1) * NE + j;
+    const float M = key_value(s_top[0]);
+    uint64_t part = 0;
+    for (int i = tid; i < S; i += NT) {
+        const uint64_t tk = s_top[i];
+        const uint32_t w = cweight(key_value(tk), M, a.k1);
+        s_w1[i] = w;
+        s_k2[i] = ((uint64_t)w << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)key_id(tk));
+        part += w;
+    }
+    const uint64_t S1 = psum<NT>(part, s_red);
+    psync<NT>();
+    // The support is in (logit desc, id asc) order and the weight never
+    // grows along it, so ranks by (w1 desc, id asc) differ from positions
+    // only where two different logits share a weight.
+    bool tie = false;
+    for (int i = tid + 1; i < S; i += NT)
+        tie |= s_w1[i] == s_w1[i - 1] && (s_top[i] >> 32) != (s_top[i - 1] >> 32);
+    if (pany<NT>(tie)) {
+        rank_all<NT>(s_k2, S, s_wr);
+    } else {
+        for (int i = tid; i < S; i += NT) s_wr[i] = (int16_t)i;
+    }
+    psync<NT>();
+    for (int i = tid; i < S; i += NT) s_xs[s_wr[i]] = (int16_t)i;
+    psync<NT>();
+
+    // tail q~_T (relative to x_{m+1}), its total, and its order by token id
+    const float ref_t = key_value(s_top[s_xs[m]]);
+    part = 0;
+    for (int i = tid; i < S; i += NT) {
+        const bool tail = s_wr[i] >= m;
+        const uint64_t tk = s_top[i];
+        const uint32_t w = tail ? cweight(key_value(tk), ref_t, a.kT) : 0u;
+        s_q[i] = w;
+        part += w;
+        s_k2[i] = tail ? (uint64_t)(0xFFFFFFFFu - (uint32_t)key_id(tk)) + 1 : 0ull;
+    }
+    const uint64_t Zq = psum<NT>(part, s_red);
+    psync<NT>();
+    rank_all<NT>(s_k2, S, s_ir);
+    psync<NT>();
+    // id-sorted tail, written straight to the tree (q~ for verification)
+    const int ntail = S - m;
+    const int64_t tail_base = ((int64_t)b * t.E + e_idx) * S;
+    for (int i = tid; i < S; i += NT) {
+        if (s_wr[i] >= m) {
+            const int idr = s_ir[i];
+            s_tq[idr] = s_q[i];
+            s_tx[idr] = (int16_t)i;
+            t.tail_id[tail_base + idr] = key_id(s_top[i]);
+            t.tail_q[tail_base + idr] = s_q[i];
+        }
+    }
+    if (tid == 0) *s_yi = -1;
+    psync<NT>();
+
+    // Y ~ q~_T: t = floor(U64 Zq / 2^64), the first id-ordered tail entry
+    // whose inclusive prefix exceeds t (each thread scans a contiguous block)
+    const uint64_t tt = __umul64hi(u, Zq);
+    const int IPT = (ntail + NT - 1) / NT;
+    const int lo = min(ntail, tid * IPT), hi = min(ntail, lo + IPT);
+    uint64_t mysum = 0;
+    for (int i = lo; i < hi; ++i) mysum += s_tq[i];
+    uint64_t acc;
+    if (NT == WAVE) {
+        acc = wave_incl_scan_u64(mysum) - mysum;
+    } else {
+        uint64_t total;
+        acc = block_excl_scan_u64<NT>(mysum, s_red, &total);
+    }
+    if (acc <= tt && tt < acc + mysum) {
+        for (int i = lo; i < hi; ++i) {
+            const uint64_t w = s_tq[i];
+            if (tt < acc + w) {
+                *s_yi = s_tx[i];
+                break;
+            }
+            acc += w;
+        }
+    }
+    psync<NT>();
+    int yi = *s_yi;
+    if (yi < 0) {
+        if (tid == 0) atomicOr(t.err, 1);
+        yi = s_xs[m];                            // unreachable fallback
+    }
+
+    if (tid == 0) {
+        t.zq[(int64_t)b * t.E + e_idx] = Zq;
+        t.first_child[nb + pu] = cb + j * K;
+        t.exp_of[nb + pu] = e_idx;
+        if (level == 0) {
+            t.tok[nb] = -1;
+            t.par[nb] = -1;
+            t.meta[nb] = 0;
+            t.proxy[nb] = 1.0;
+            t.qtrue[nb] = 1.0;
+            t.score[nb] = 1.0;
+            t.path[nb] = 0;
+        }
+    }
+    // the K children: top-m leads, Y, fills (App. C.1)
+    if (tid < K) {
+        const int s = tid;
+        const int yr = s_wr[yi];
+        int item, kind;
+        if (s < m) {
+            item = s_xs[s];
+            kind = LEAD;
+        } else if (s == m) {
+            item = yi;
+            kind = SAMPLED;
+        } else {
+            const int f = s - m - 1;
+            const int rk = m + f + ((m + f) >= yr ? 1 : 0);
+            item = s_xs[rk];
+            kind = FILL;
+        }
+        double pscore = 1.0;
+        uint64_t ppath = 0;
+        if (level > 0) {
+            pscore = t.score[nb + pu];
+            ppath = t.path[nb + pu];
+        }
+        double proxy;
+        const double dS1 = (double)S1;
+        if (kind == SAMPLED) {
+            if (m >= 1) {
+                uint64_t lead = 0;
+                for (int q2 = 0; q2 < m; ++q2) lead += s_w1[s_xs[q2]];
+                const uint64_t z = S1 - lead;
+                const uint64_t wm = s_w1[s_xs[m - 1]];
+                proxy = __ddiv_rn((double)(wm < z ? wm : z), dS1);
+            } else {
+                proxy = fmin(1.0, __dadd_rn(__ddiv_rn((double)s_w1[s_xs[0]], dS1), t.eps));
+            }
+        } else {
+            proxy = __ddiv_rn((double)s_w1[item], dS1);
+        }
+        const double qtrue = (kind == SAMPLED) ? __ddiv_rn((double)s_q[item], (double)Zq) : proxy;
+        const int uid = cb + j * K + s;
+        const int64_t o = nb + uid;
+        t.par[o] = pu;
+        t.meta[o] = (level + 1) | ((s + 1) << 8) | (kind << 16);
+        t.proxy[o] = proxy;
+        t.qtrue[o] = qtrue;
+        t.first_child[o] = -1;
+        t.exp_of[o] = -1;
+        __hip_atomic_store(&t.tok[o], key_id(s_top[item]), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store((uint64_t*)&t.score[o], (uint64_t)__double_as_longlong(__dmul_rn(pscore, proxy)),
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&t.path[o], ppath | ((uint64_t)(s + 1) << (56 - 4 * level)),
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// k_pool: one block per row: parent, support (merge of the chunk lists),
+// pool, and, by the last row of each sequence, the next frontier
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(NTP) void k_pool(TreeDev t, LevelArgs a) {
+    extern __shared__ __align__(16) uint8_t s_pdyn[];
+    __shared__ uint64_t s_red[NTP / WAVE];
+    __shared__ int s_pu, s_yi, s_lastseq;
+    __shared__ uint64_t s_u;
+    const PoolLds L = pool_lds(t.S, t.C);
+    uint64_t* s_m = (uint64_t*)(s_pdyn + L.m);    // the C chunk lists, C * S keys
+    uint64_t* s_top = (uint64_t*)(s_pdyn + L.top);
+    uint64_t* s_k2 = (uint64_t*)(s_pdyn + L.k2);
+
+    const int tid = threadIdx.x;
+    const int row = blockIdx.x;
+    const int b = row / a.P;
+    const int j = row % a.P;
+    const int S = t.S, K = t.K;
+    const int C = t.C;
+    const int level = a.level;
+    const int NE = t.NE;
+    const int64_t nb = (int64_t)b * t.NN;
+
+    // the chunk lists, and the parent: frontier node j of the previous level
+    // (the n_expand children with the highest priority, chosen by the
+    // previous launch) with the Philox draw of its sampled slot
+    const uint64_t* src = t.sel + (int64_t)row * C * S;
+    for (int i = tid; i < C * S; i += NTP) s_m[i] = src[i];
+    for (int i = tid; i < S; i += NTP) s_top[i] = 0ull;   // id -1 until merged
+    if (tid == 0) {
+        int pu = (level == 0) ? 0 : t.frontier[(int64_t)b * NE + j];
+        const int lo_uid = (level == 0) ? 0 : ((level == 1) ? 1 : 1 + K + (level - 2) * NE * K);
+        const int hi_uid = (level == 0) ? 1 : lo_uid + ((level == 1) ? 1 : NE) * K;
+        if (pu < lo_uid || pu >= hi_uid) {
+            atomicOr(t.err, 16);
+            pu = 0;
+        }
+        s_pu = pu;
+        s_u = (level == 0) ? philox_draw(a.rng_key, P_DRAFT, (uint64_t)b, 0ull)
+                           : t.fr_u[(int64_t)b * NE + j];
+        if (pu == 0 && level > 0) s_u = philox_draw(a.rng_key, P_DRAFT, (uint64_t)b, 0ull);
+    }
+    __syncthreads();
+
+    // merge: a key's rank in the row is its position in its own (sorted)
+    // list plus the count of larger keys in every other list (a binary
+    // search per list).  Every list holds S keys (a chunk is larger than any
+    // support); keys are unique and 0 marks an empty slot.  Two keys per
+    // thread and four lists at a time keep eight searches in flight.
+    {
+        int pw2 = 1;
+        while (pw2 * 2 <= S) pw2 *= 2;
+        const int nk = C * S;
+        for (int eA = tid; eA < nk; eA += 2 * NTP) {
+            const int eB = eA + NTP;
+            const uint64_t kA = s_m[eA], kB = eB < nk ? s_m[eB] : 0ull;
+            const int lA = eA / S, lB = eB / S;
+            int rA = eA - lA * S, rB = eB - lB * S;
+            for (int c2 = 0; c2 < C; c2 += 4) {
+                int oA[4] = {0, 0, 0, 0}, oB[4] = {0, 0, 0, 0};
+                for (int half = pw2; half > 0; half >>= 1) {
+#pragma unroll
+                    for (int cc = 0; cc < 4; ++cc) {
+                        if (c2 + cc < C) {
+                            const uint64_t* L2 = s_m + (c2 + cc) * S;
+                            const uint64_t xA = L2[min(oA[cc] + half, S) - 1];
+                            const uint64_t xB = L2[min(oB[cc] + half, S) - 1];
+                            oA[cc] += (oA[cc] + half <= S && xA > kA) ? half : 0;
+                            oB[cc] += (oB[cc] + half <= S && xB > kB) ? half : 0;
+                        }
+                    }
+                }
+#pragma unroll
+                for (int cc = 0; cc < 4; ++cc) {
+                    if (c2 + cc < C && c2 + cc != lA) rA += oA[cc];
+                    if (c2 + cc < C && c2 + cc != lB) rB += oB[cc];
+                }
+            }
+            if (kA != 0ull && rA < S) s_top[rA] = kA;
+            if (kB != 0ull && rB < S) s_top[rB] = kB;
+        }
+    }
+    __syncthreads();
+    for (int i = tid; i < S; i += NTP) {
+        if ((uint32_t)key_id(s_top[i]) >= (uint32_t)t.V) {   // a support slot left empty
+            atomicOr(t.err, 256);
+            s_top[i] = logit_key(-INFINITY, 0u);
+        }
+    }
+    __syncthreads();
+
+    // the pool: one wave for small supports (no block barriers), else all
+    if (S <= 256) {
+        if (tid < WAVE) pool_form<WAVE>(t, a, row, s_pdyn, s_pu, s_u, s_red, &s_yi);
+    } else {
+        pool_form<NTP>(t, a, row, s_pdyn, s_pu, s_u, s_red, &s_yi);
+    }
+    if (level + 1 >= t.D) return;
+
+    // the next frontier (Sec. 2.1; App. C.4, step 1: the next level expands
+    // the best-scoring new nodes): the last row of the sequence to finish
+    // ranks the level's P * K new children by priority and keeps the best
+    // n_expand
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (tid == 0) {
+        const uint32_t old = __hip_atomic_fetch_add(&t.seq_cnt[b], 1u, __ATOMIC_RELAXED,
+                                                    __HIP_MEMORY_SCOPE_AGENT);
+        s_lastseq = old == (uint32_t)(a.P - 1);
+        if (s_lastseq) __hip_atomic_store(&t.seq_cnt[b], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __syncthreads();
+    if (!s_lastseq) return;
+    const int n = a.P * K;                       // <= 225
+    const int cb = (level == 0) ? 1 : 1 + K + (level - 1) * NE * K;
+    uint64_t* s_hi = s_top;                      // free again: the pool is written
+    uint64_t* s_lo = s_k2;
+    if (tid < n) {
+        const int64_t o = nb + cb + tid;
+        const double sc = __longlong_as_double((long long)__hip_atomic_load(
+            (uint64_t*)&t.score[o], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+        const uint64_t pa = __hip_atomic_load(&t.path[o], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        uint64_t hi, lo;
+        prio_key(sc, level + 1, pa, hi, lo);
+        s_hi[tid] = hi;
+        s_lo[tid] = lo;
+    }
+    __syncthreads();
+    if (tid < n) {
+        const uint64_t hi = s_hi[tid], lo = s_lo[tid];
+        int rk = 0;
+#pragma unroll 8
+        for (int q = 0; q < n; ++q) {
+            const uint64_t h = s_hi[q], l = s_lo[q];
+            rk += (int)(h > hi) | ((int)(h == hi) & (int)(l > lo));
+        }
+        if (rk < NE) {
+            t.frontier[(int64_t)b * NE + rk] = cb + tid;
+            t.fr_u[(int64_t)b * NE + rk] =     // the draw of its sampled slot
+                philox_draw(a.rng_key, P_DRAFT, (uint64_t)b, (uint64_t)(cb + tid));
+            t.fr_parent[(int64_t)b * NE + rk] = tid / K;
+            t.fr_token[(int64_t)b * NE + rk] =
+                __hip_atomic_load(&t.tok[nb + cb + tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // k_select: the exact top-Sc of one chunk of one row
 // ---------------------------------------------------------------------------
 template <int DT, int NVC>
-__global__ __launch_bounds__(NTC) void k_select(TreeDev t, LevelArgs a) {
+__device__ __forceinline__ void select_block(const TreeDev& t, const LevelArgs& a) {
     constexpr int VEC = DT ? 8 : 4;
     constexpr int ESZ = DT ? 2 : 4;
     constexpr int NM = DT ? (NVC + 1) / 2 : NVC;   // registers of per-vector maxima
 
-    __shared__ uint64_t s_keys[CAPC];
-    __shared__ int16_t s_rank[CAPC];
-    __shared__ int s_bc[2][NTC / WAVE];
-    __shared__ uint32_t s_off[2 * NTC];
-    __shared__ uint32_t s_h;
-    __shared__ int s_redi[NTC / WAVE];
+    __shared__ uint64_t s_keys[CAPC];           // candidates
     __shared__ uint4 s_cv[CAPV];                 // candidate vectors
+    __shared__ int16_t s_rank[CAPC];
     __shared__ int s_cvi[CAPV];                  // their vector indices
+    __shared__ uint32_t s_off[2 * NTC];          // threshold offers
+    __shared__ int s_bc[2][NTC / WAVE];
+    __shared__ uint32_t s_h;
     __shared__ int s_cnt, s_nv;
+    __shared__ int s_redi[NTC / WAVE];
 
     const int tid = threadIdx.x;
     const int c = blockIdx.x;
@@ -314,322 +735,22 @@ __global__ __launch_bounds__(NTC) void k_select(TreeDev t, LevelArgs a) {
         if (rk < nsel) out[rk] = s_keys[i];
     }
     for (int i = nsel + tid; i < t.Sc; i += NTC) out[i] = 0ull;
+
 }
 
-// ---------------------------------------------------------------------------
-// k_pool: parent, support, distributions and pool of one row
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(NTP) void k_pool(TreeDev t, LevelArgs a) {
-    extern __shared__ uint64_t s_m[];            // the C chunk lists, C * Sc keys
-    __shared__ uint64_t s_top[SMAX];             // support by (logit desc, id asc)
-    __shared__ uint64_t s_k2[SMAX];              // ranking keys
-    __shared__ uint32_t s_w1[SMAX];              // construction weights
-    __shared__ __align__(8) uint32_t s_q[SMAX];  // tail weights (0 off the tail)
-    __shared__ int16_t s_wr[SMAX];               // item -> rank by (w1 desc, id asc)
-    __shared__ int16_t s_xs[SMAX];               // rank -> item
-    __shared__ int16_t s_ir[SMAX];               // item -> position in id order
-    __shared__ uint32_t s_tq[SMAX];              // tail weights in id order
-    __shared__ int16_t s_tx[SMAX];               // id order -> item
-    __shared__ uint64_t s_red[NTP / WAVE];
-    __shared__ int s_pu, s_yi;
-    __shared__ uint64_t s_u;
-
-    const int tid = threadIdx.x;
-    const int row = blockIdx.x;
-    const int b = row / a.P;
-    const int j = row % a.P;
-    const int S = t.S, K = t.K, m = t.m;
-    const int C = t.C, Sc = t.Sc;
-    const int level = a.level;
-    const int NE = t.NE, NN = t.NN;
-    const int64_t nb = (int64_t)b * NN;
-    uint64_t* s_ph = s_k2;                       // previous level's priority keys
-    uint64_t* s_pl = (uint64_t*)s_q;             // (free until the pool uses them)
-
-    // the chunk lists (coalesced) and, meanwhile, this row's parent: the j-th
-    // best child of the previous level by priority
-    const uint64_t* src = t.sel + (int64_t)row * C * Sc;
-    for (int i = tid; i < C * Sc; i += NTP) s_m[i] = src[i];
-    if (tid == 0) {
-        s_pu = (level == 0) ? 0 : -1;
-        s_yi = -1;
-    }
-    if (level > 0) {
-        const int pcb = (level == 1) ? 1 : 1 + K + (level - 2) * NE * K;
-        const int n = ((level == 1) ? 1 : NE) * K;      // <= 225
-        uint64_t u = 0;
-        if (tid < n) {
-            const int64_t o = nb + pcb + tid;
-            const double sc = t.score[o];
-            const uint64_t pa = t.path[o];
-            u = philox_draw(a.rng_key, P_DRAFT, (uint64_t)b, (uint64_t)(pcb + tid));
-            uint64_t hi, lo;
-            prio_key(sc, level, pa, hi, lo);
-            s_ph[tid] = hi;
-            s_pl[tid] = lo;
-        }
-        __syncthreads();
-        if (tid < n) {
-            const uint64_t hi = s_ph[tid], lo = s_pl[tid];
-            int rk = 0;
-#pragma unroll 8
-            for (int q = 0; q < n; ++q) {
-                const uint64_t h = s_ph[q], l = s_pl[q];
-                rk += (int)(h > hi) | ((int)(h == hi) & (int)(l > lo));
-            }
-            if (rk == j) {
-                s_pu = pcb + tid;
-                s_u = u;
-            }
-        }
-    } else if (tid == 0) {
-        s_u = philox_draw(a.rng_key, P_DRAFT, (uint64_t)b, 0ull);
-    }
-    __syncthreads();
-    if (tid == 0 && (s_pu < 0 || s_pu >= NN)) {
-        atomicOr(t.err, 16);
-        s_pu = 0;
-        s_u = philox_draw(a.rng_key, P_DRAFT, (uint64_t)b, 0ull);
-    }
-
-    // merge: pairs of sorted lists merge round by round until one list of
-    // the row's top S remains.  A key's position in the merged list is its
-    // position in its own list plus the count of larger keys in the partner
-    // list (one binary search); positions >= S are dropped.  Every list holds
-    // S keys (a chunk is larger than any support); keys are unique and 0
-    // marks an empty slot.  Each round computes all positions first, then
-    // rewrites the lists in place.
-    {
-        int pw2 = 1;
-        while (pw2 * 2 <= S) pw2 *= 2;
-        int nl = C;
-        while (nl > 1) {
-            const int npair = nl / 2, nout = (nl + 1) / 2;
-            uint64_t kv[MERGE_MAX / NTP];
-            int pv[MERGE_MAX / NTP];
-#pragma unroll
-            for (int q = 0; q < MERGE_MAX / NTP; ++q) {
-                const int e = tid + q * NTP;
-                pv[q] = -1;
-                kv[q] = 0ull;
-                if (e < nl * S) {
-                    const int l = e / S, i = e - l * S;
-                    const uint64_t key = s_m[e];
-                    if (l < 2 * npair) {
-                        const uint64_t* B = s_m + (l ^ 1) * S;
-                        int lo = 0;
-                        for (int half = pw2; half > 0; half >>= 1) {
-                            const uint64_t x = B[min(lo + half, S) - 1];
-                            lo += (lo + half <= S && x > key) ? half : 0;
-                        }
-                        if (i + lo < S) pv[q] = (l >> 1) * S + i + lo;
-                    } else {
-                        pv[q] = npair * S + i;          // the odd list passes through
-                    }
-                    kv[q] = key;
-                }
-            }
-            __syncthreads();
-            for (int i = tid; i < nout * S; i += NTP) s_m[i] = 0ull;
-            __syncthreads();
-#pragma unroll
-            for (int q = 0; q < MERGE_MAX / NTP; ++q)
-                if (pv[q] >= 0 && kv[q] != 0ull) s_m[pv[q]] = kv[q];
-            __syncthreads();
-            nl = nout;
-        }
-        for (int i = tid; i < S; i += NTP) s_top[i] = s_m[i];
-        __syncthreads();
-    }
-    for (int i = tid; i < S; i += NTP) {
-        if ((uint32_t)key_id(s_top[i]) >= (uint32_t)t.V) {   // a support slot left empty
-            atomicOr(t.err, 256);
-            s_top[i] = logit_key(-INFINITY, 0u);
-        }
-    }
-    __syncthreads();
-
-    // construction weights (untempered unless asked), S1, rank by (w1 desc, id asc)
-    const int pu = s_pu;
-    const int cb = (level == 0) ? 1 : 1 + K + (level - 1) * NE * K;
-    const int e_idx = (level == 0) ? 0 : 1 + (level - 1) * NE + j;
-    const float M = key_value(s_top[0]);
-    uint64_t part = 0;
-    for (int i = tid; i < S; i += NTP) {
-        const uint64_t tk = s_top[i];
-        const uint32_t w = cweight(key_value(tk), M, a.k1);
-        s_w1[i] = w;
-        s_k2[i] = ((uint64_t)w << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)key_id(tk));
-        part += w;
-    }
-    int tie = 0;
-    const uint64_t S1 = block_sum_u64<NTP>(part, s_red);
-    // The support is in (logit desc, id asc) order and the weight never
-    // grows along it, so ranks by (w1 desc, id asc) differ from positions
-    // only inside runs of equal weights.
-    for (int i = tid + 1; i < S; i += NTP) tie |= s_w1[i] == s_w1[i - 1];
-    if (__syncthreads_or(tie)) {
-        rank_keys<NTP>(s_k2, S, s_wr);
-    } else {
-        for (int i = tid; i < S; i += NTP) s_wr[i] = (int16_t)i;
-    }
-    __syncthreads();
-    for (int i = tid; i < S; i += NTP) s_xs[s_wr[i]] = (int16_t)i;
-    __syncthreads();
-
-    // tail q~_T (relative to x_{m+1}), its total, and its order by token id
-    const float ref_t = key_value(s_top[s_xs[m]]);
-    part = 0;
-    for (int i = tid; i < S; i += NTP) {
-        const bool tail = s_wr[i] >= m;
-        const uint64_t tk = s_top[i];
-        const uint32_t w = tail ? cweight(key_value(tk), ref_t, a.kT) : 0u;
-        s_q[i] = w;
-        part += w;
-        s_k2[i] = tail ? (uint64_t)(0xFFFFFFFFu - (uint32_t)key_id(tk)) + 1 : 0ull;
-    }
-    const uint64_t Zq = block_sum_u64<NTP>(part, s_red);
-    rank_keys<NTP>(s_k2, S, s_ir);
-    __syncthreads();
-    // id-sorted tail, written straight to the tree (q~ for verification)
-    const int ntail = S - m;
-    const int64_t tail_base = ((int64_t)b * t.E + e_idx) * S;
-    for (int i = tid; i < S; i += NTP) {
-        if (s_wr[i] >= m) {
-            const int idr = s_ir[i];
-            s_tq[idr] = s_q[i];
-            s_tx[idr] = (int16_t)i;
-            t.tail_id[tail_base + idr] = key_id(s_top[i]);
-            t.tail_q[tail_base + idr] = s_q[i];
-        }
-    }
-    __syncthreads();
-
-    // Y ~ q~_T: t = floor(U64 Zq / 2^64), the first id-ordered tail entry
-    // whose inclusive prefix exceeds t (each thread scans a contiguous block)
-    const uint64_t tt = __umul64hi(s_u, Zq);
-    const int IPT = (ntail + NTP - 1) / NTP;
-    const int lo = min(ntail, tid * IPT), hi = min(ntail, lo + IPT);
-    uint64_t mysum = 0;
-    for (int i = lo; i < hi; ++i) mysum += s_tq[i];
-    uint64_t total;
-    uint64_t acc = block_excl_scan_u64<NTP>(mysum, s_red, &total);
-    if (acc <= tt && tt < acc + mysum) {
-        for (int i = lo; i < hi; ++i) {
-            const uint64_t w = s_tq[i];
-            if (tt < acc + w) {
-                s_yi = s_tx[i];
-                break;
-            }
-            acc += w;
-        }
-    }
-    __syncthreads();
-    int yi = s_yi;
-    if (yi < 0) {
-        if (tid == 0) atomicOr(t.err, 1);
-        yi = s_xs[m];                            // unreachable fallback
-    }
-
-    if (tid == 0) {
-        t.zq[(int64_t)b * t.E + e_idx] = Zq;
-        t.first_child[nb + pu] = cb + j * K;
-        t.exp_of[nb + pu] = e_idx;
-        if (level == 0) {
-            t.tok[nb] = -1;
-            t.par[nb] = -1;
-            t.meta[nb] = 0;
-            t.proxy[nb] = 1.0;
-            t.qtrue[nb] = 1.0;
-            t.score[nb] = 1.0;
-            t.path[nb] = 0;
-        }
-    }
-    // the K children: top-m leads, Y, fills (App. C.1)
-    if (tid < K) {
-        const int s = tid;
-        const int yr = s_wr[yi];
-        int item, kind;
-        if (s < m) {
-            item = s_xs[s];
-            kind = LEAD;
-        } else if (s == m) {
-            item = yi;
-            kind = SAMPLED;
-        } else {
-            const int f = s - m - 1;
-            const int rk = m + f + ((m + f) >= yr ? 1 : 0);
-            item = s_xs[rk];
-            kind = FILL;
-        }
-        double pscore = 1.0;
-        uint64_t ppath = 0;
-        if (level > 0) {
-            pscore = t.score[nb + pu];
-            ppath = t.path[nb + pu];
-        }
-        double proxy;
-        const double dS1 = (double)S1;
-        if (kind == SAMPLED) {
-            if (m >= 1) {
-                uint64_t lead = 0;
-                for (int q2 = 0; q2 < m; ++q2) lead += s_w1[s_xs[q2]];
-                const uint64_t z = S1 - lead;
-                const uint64_t wm = s_w1[s_xs[m - 1]];
-                proxy = __ddiv_rn((double)(wm < z ? wm : z), dS1);
-            } else {
-                proxy = fmin(1.0, __dadd_rn(__ddiv_rn((double)s_w1[s_xs[0]], dS1), t.eps));
-            }
-        } else {
-            proxy = __ddiv_rn((double)s_w1[item], dS1);
-        }
-        const double qtrue = (kind == SAMPLED) ? __ddiv_rn((double)s_q[item], (double)Zq) : proxy;
-        const int uid = cb + j * K + s;
-        const int64_t o = nb + uid;
-        t.tok[o] = key_id(s_top[item]);
-        t.par[o] = pu;
-        t.meta[o] = (level + 1) | ((s + 1) << 8) | (kind << 16);
-        t.proxy[o] = proxy;
-        t.qtrue[o] = qtrue;
-        t.score[o] = __dmul_rn(pscore, proxy);
-        t.path[o] = ppath | ((uint64_t)(s + 1) << (56 - 4 * level));
-        t.first_child[o] = -1;
-        t.exp_of[o] = -1;
-    }
+// Four blocks per CU keep enough loads in flight; the largest chunk variant
+// holds twice the registers and runs at two.
+template <int DT, int NVC>
+__global__ __launch_bounds__(NTC) void k_select(TreeDev t,
+                                                                                         LevelArgs a) {
+    select_block<DT, NVC>(t, a);
+}
+template <int DT>
+__global__ __launch_bounds__(NTC) void k_select_wide(TreeDev t, LevelArgs a) {
+    select_block<DT, 32>(t, a);
 }
 
-// The frontier of the last expanded level in rank order, for the caller
-// (rheo_frontier): the n_expand best children by priority, per sequence.
-__global__ __launch_bounds__(256) void k_frontier(TreeDev t, int level, int P) {
-    __shared__ uint64_t s_hi[256], s_lo[256];
-    const int b = blockIdx.x, tid = threadIdx.x;
-    const int K = t.K, NE = t.NE;
-    const int cb = (level == 0) ? 1 : 1 + K + (level - 1) * NE * K;
-    const int n = P * K;
-    const int64_t nb = (int64_t)b * t.NN;
-    if (tid < n) {
-        uint64_t hi, lo;
-        prio_key(t.score[nb + cb + tid], level + 1, t.path[nb + cb + tid], hi, lo);
-        s_hi[tid] = hi;
-        s_lo[tid] = lo;
-    }
-    __syncthreads();
-    if (tid < n) {
-        const uint64_t hi = s_hi[tid], lo = s_lo[tid];
-        int rk = 0;
-#pragma unroll 8
-        for (int q = 0; q < n; ++q) {
-            const uint64_t h = s_hi[q], l = s_lo[q];
-            rk += (int)(h > hi) | ((int)(h == hi) & (int)(l > lo));
-        }
-        if (rk < NE) {
-            t.fr_parent[b * NE + rk] = tid / K;
-            t.fr_token[b * NE + rk] = t.tok[nb + cb + tid];
-        }
-    }
-}
-
-// 16-byte vectors per thread of k_select; a chunk is NTC * NVC vectors.
+// 16-byte vectors per thread of k_expand; a chunk is NTC * NVC vectors.
 static const int kNVC[] = {4, 8, 16, 32};
 
 int expand_variant_count(int) { return (int)(sizeof(kNVC) / sizeof(kNVC[0])); }
@@ -645,28 +766,24 @@ ExpandVariant expand_variant(int dtype, int v, int V, int S) {
 }
 
 template <int DT>
-static void launch_select(const TreeDev& t, const LevelArgs& a, int v, dim3 grid, hipStream_t s) {
+static void launch_dt(const TreeDev& t, const LevelArgs& a, int v, dim3 grid, size_t shm,
+                      hipStream_t s) {
     switch (v) {
-    case 0: k_select<DT, 4><<<grid, NTC, 0, s>>>(t, a); break;
-    case 1: k_select<DT, 8><<<grid, NTC, 0, s>>>(t, a); break;
-    case 2: k_select<DT, 16><<<grid, NTC, 0, s>>>(t, a); break;
-    default: k_select<DT, 32><<<grid, NTC, 0, s>>>(t, a); break;
+    case 0: k_select<DT, 4><<<grid, NTC, shm, s>>>(t, a); break;
+    case 1: k_select<DT, 8><<<grid, NTC, shm, s>>>(t, a); break;
+    case 2: k_select<DT, 16><<<grid, NTC, shm, s>>>(t, a); break;
+    default: k_select_wide<DT><<<grid, NTC, shm, s>>>(t, a); break;
     }
 }
 
 hipError_t launch_expand(const TreeDev& t, const LevelArgs& a, int variant, hipStream_t s) {
     const int rows = t.B * a.P;
     const dim3 grid(t.C, rows);
-    if (t.dtype) launch_select<1>(t, a, variant, grid, s);
-    else launch_select<0>(t, a, variant, grid, s);
+    if (t.dtype) launch_dt<1>(t, a, variant, grid, 0, s);
+    else launch_dt<0>(t, a, variant, grid, 0, s);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    k_pool<<<rows, NTP, (size_t)t.C * t.Sc * sizeof(uint64_t), s>>>(t, a);
-    return hipGetLastError();
-}
-
-hipError_t launch_frontier(const TreeDev& t, int level, int P, hipStream_t s) {
-    k_frontier<<<t.B, 256, 0, s>>>(t, level, P);
+    k_pool<<<rows, NTP, (size_t)pool_lds(t.S, t.C).bytes, s>>>(t, a);
     return hipGetLastError();
 }
 

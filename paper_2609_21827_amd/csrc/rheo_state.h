@@ -30,8 +30,10 @@ struct TreeDev {
     int32_t* tail_id;              // [B][E][S]
     uint32_t* tail_q;              // [B][E][S]
     uint64_t* zq;                  // [B][E]
-    // frontier of the last expanded level, [B][NE]
+    // frontier of the last expanded level, [B][NE]: node uid, index of its
+    // parent in the previous frontier, token
     int32_t* frontier;
+    uint64_t* fr_u;                // Philox draw of each frontier node's sampled slot
     int32_t* fr_parent;
     int32_t* fr_token;
     // pruned tree
@@ -39,12 +41,15 @@ struct TreeDev {
     int32_t* porder;               // [B][NN]: uid of each pruned index
     int32_t* err;                  // sticky device error flag
     // verification team exchange (see verify.hip)
-    uint32_t* team_flag;           // [B][GMAX] arrival epochs
+    uint64_t* team_flag;           // [B][GMAX] arrival epochs
+    uint64_t* team_epoch;          // [B] first barrier epoch of the next call
     uint32_t* team_max;            // [B][GMAX] segment maxima (fp32 bits)
     uint64_t* team_chunk;          // [B][NCMAX] chunk totals of p's weights
     uint32_t* team_sp;             // [B][SPMAX] p's weights at the special tokens
     // expansion: each row's C chunk lists of Sc selection keys, sorted
     uint64_t* sel;                 // [B * NE][C][Sc]
+    uint32_t* row_cnt;             // [B * NE] chunk blocks arrived (0 between launches)
+    uint32_t* seq_cnt;             // [B] rows whose pool is written (0 between launches)
     int C, Sc;
 };
 
@@ -62,7 +67,6 @@ struct VerifyArgs {
     int R;
     int G;                         // blocks per sequence (a team)
     int NV;                        // chunks per segment
-    uint32_t epoch;                // barrier epoch base of this call
     float kT;
     uint64_t rng_key;
     int32_t* accepted;
@@ -73,7 +77,6 @@ struct VerifyArgs {
 hipError_t launch_expand(const TreeDev& t, const LevelArgs& a, int variant,
                          hipStream_t s);
 hipError_t launch_prune(const TreeDev& t, int R, hipStream_t s);
-hipError_t launch_frontier(const TreeDev& t, int level, int P, hipStream_t s);
 hipError_t verify_shape(const TreeDev& t, int* G, int* segch, int* grid);
 hipError_t launch_verify(const TreeDev& t, const VerifyArgs& a, int segch, int grid,
                          hipStream_t s);

@@ -151,7 +151,7 @@ __device__ u128 block_sum_u128(u128 v, u128* sh) {
 // every team member has arrived.  Prior team-visible stores must be agent
 // atomic stores; each thread waits for its own before the block barrier.
 // Returns false (and raises the error flag) if the wait timed out.
-__device__ bool team_barrier(uint32_t* flags, int g, int G, uint32_t epoch, int32_t* err,
+__device__ bool team_barrier(uint64_t* flags, int g, int G, uint64_t epoch, int32_t* err,
                              int* s_ok) {
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
@@ -220,7 +220,10 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
     const int V = t.V, K = t.K, NN = t.NN;
     const int NC = (V + CH - 1) / CH;
     const int64_t nb = (int64_t)b * NN;
-    uint32_t* flags = t.team_flag + (int64_t)b * GMAX;
+    uint64_t* flags = t.team_flag + (int64_t)b * GMAX;
+    // barrier epochs of this call: the team's base, read before any block
+    // of the team can pass its first barrier; the leader advances it on exit
+    const uint64_t epoch = t.team_epoch[b];
     uint32_t* tmax_x = t.team_max + (int64_t)b * GMAX;
     uint64_t* chunk_x = t.team_chunk + (int64_t)b * NCMAX;
     uint32_t* sp_x = t.team_sp + (int64_t)b * SPMAX;
@@ -289,7 +292,7 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
                 s_tq[i] = t.tail_q[tb + i];
             }
         }
-        if (!team_barrier(flags, g, G, a.epoch + 2 * level + 1, t.err, &s_ok)) break;
+        if (!team_barrier(flags, g, G, epoch + 2 * level + 1, t.err, &s_ok)) break;
         const int nc = s_nc, spos = s_spos;
         if (tid < WAVE) {
             float v = -INFINITY;
@@ -331,7 +334,7 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
                                        __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
         }
-        if (!team_barrier(flags, g, G, a.epoch + 2 * level + 2, t.err, &s_ok)) break;
+        if (!team_barrier(flags, g, G, epoch + 2 * level + 2, t.err, &s_ok)) break;
         uint64_t part = 0;
         for (int c = tid; c < NC; c += NTV) {
             const uint64_t v = __hip_atomic_load(&chunk_x[c], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -532,16 +535,17 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
         }
         break;
     }
+    if (g == 0 && tid == 0) t.team_epoch[b] = epoch + 64;   // > every epoch this call used
 }
 
-// Team shape for a tree: about `target` blocks in all (512 by default),
+// Team shape for a tree: about `target` blocks in all (1024 by default),
 // segments of whole chunks, G <= GMAX, every block co-resident (cooperative
 // launch).
 hipError_t verify_shape(const TreeDev& t, int* G_out, int* segch, int* grid) {
     const int VEC = t.dtype ? 8 : 4;
     const int NC = (t.V + WAVE * VEC - 1) / (WAVE * VEC);
     const char* env = getenv("RHEO_VERIFY_BLOCKS");
-    const int target = env ? atoi(env) : 512;
+    const int target = env ? atoi(env) : 1024;
     int dev = 0, cus = 0, per_cu = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);

@@ -187,3 +187,29 @@ def test_generator_cpu_gpu_identical(dev):
         ta = synth.target_rows(w, keys, [0.9] * 3, device="cpu")
         tg = synth.target_rows(w, keys, [0.9] * 3, device=dev).cpu()
         assert torch.equal(ta.float(), tg.float())
+
+
+def test_frontier_view_matches_copy(dev):
+    """The zero-copy frontier view and rheo_frontier's copy agree at every
+    level, and match the oracle's frontier (via the step's parity above)."""
+    from paper_2609_21827_amd.driver import make_tree
+    import synth
+    w = W["llama2"].with_(B=3, depth=4, R=30)
+    tree = make_tree(w, device=dev)
+    view = tree.frontier_view()
+    keys = [[synth.root_key(w, b, 0)] for b in range(w.B)]
+    tree.begin_step()
+    for d in range(w.depth):
+        P = len(keys[0])
+        flat = [k for ks in keys for k in ks]
+        rows = synth.draft_rows(w, flat, device=dev).view(w.B, P, w.V)
+        tree.expand_level(rows, w.T, synth.step_rng_key(w, 0))
+        if d + 1 < w.depth:
+            par, tok = tree.frontier()
+            torch.cuda.synchronize()
+            assert torch.equal(par, view[0]) and torch.equal(tok, view[1])
+            p, t = par.cpu().tolist(), tok.cpu().tolist()
+            keys = [[synth.child_key(keys[b][p[b][j]], t[b][j]) for j in range(w.n_expand)]
+                    for b in range(w.B)]
+    assert tree.device_error() == 0
+    tree.close()
