@@ -13,8 +13,11 @@ Protocol
      cycling over the recorded steps, bracketed by torch.cuda.synchronize();
      every replay must reproduce the discovery outputs bit for bit.
   3. HIP events around each rheo_expand_level call (on the stream it launches
-     on) give the dominant kernel's average duration; its algorithmic bytes
-     are the draft rows it must read (rows x V x 2 bytes).
+     on) give the duration of an expand level (k_select + k_pool, the
+     dominant work); its algorithmic bytes are the draft rows it must read
+     (rows x V x 2 bytes).  Then the same steps are captured as HIP graphs
+     (one per recorded step) and replayed; `value` is the graph-replay
+     throughput unless --graph 0 (eager launch loop, also reported).
   4. cpu_baseline: the CPU oracle timed on a bounded sample of the same
      workload (one step of a few sequences, rows pre-generated).
 Prints one JSON line on stdout.
@@ -66,8 +69,11 @@ def write_traffic(paths, out, workload, copy_bytes):
     """Scales the expand kernel's FETCH_SIZE / WRITE_SIZE by what the same
     counters read for a plain device copy of known size."""
     exp_f, exp_w, cp_f, cp_w = paths
-    ef = _counter_rows(exp_f, r"k_expand", "FETCH_SIZE")
-    ew = _counter_rows(exp_w, r"k_expand", "WRITE_SIZE")
+    # one expand level = one k_select and one k_pool dispatch
+    nf = len(_counter_rows(exp_f, r"k_select", "FETCH_SIZE"))
+    nw = len(_counter_rows(exp_w, r"k_select", "WRITE_SIZE"))
+    ef = [sum(_counter_rows(exp_f, r"k_select|k_pool", "FETCH_SIZE")) / nf]
+    ew = [sum(_counter_rows(exp_w, r"k_select|k_pool", "WRITE_SIZE")) / nw]
     cf = _counter_rows(cp_f, r"copy|Copy", "FETCH_SIZE")
     cw = _counter_rows(cp_w, r"copy|Copy", "WRITE_SIZE")
     # every copy dispatch moves copy_bytes in and copy_bytes out
@@ -75,9 +81,9 @@ def write_traffic(paths, out, workload, copy_bytes):
     k_w = copy_bytes / (sum(cw) / len(cw) * 1024)
     fetch = sum(ef) / len(ef) * 1024 * k_f
     write = sum(ew) / len(ew) * 1024 * k_w
-    res = {"workload": workload, "kernel": "k_expand",
+    res = {"workload": workload, "kernel": "expand level (k_select + k_pool)",
            "kernel_src_sha256": kernel_src_hash(),
-           "dispatches": len(ef), "copy_dispatches": len(cf),
+           "levels": nf, "copy_dispatches": len(cf),
            "copy_bytes": copy_bytes,
            "copy_fetch_kib": sum(cf) / len(cf), "copy_write_kib": sum(cw) / len(cw),
            "scale_fetch": k_f, "scale_write": k_w,
@@ -100,8 +106,10 @@ def main():
     ap.add_argument("--distinct", type=int, default=4, help="recorded steps cycled over")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--graph", type=int, default=1,
+                    help="1: the timed loop replays each step as a captured HIP graph")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles",
-                                                      "k_expand_headline_traffic.json"))
+                                                      "expand_level_headline_traffic.json"))
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB five times "
                          "(counter calibration under rocprofv3 --pmc)")
@@ -160,9 +168,10 @@ def main():
     # next) is read in place through these views: no call, no copy
     fr_view = tree.frontier_view()
 
-    def replay(i, events=None):
+    def replay(i, events=None, stream_override=None):
         # the calls a serving loop makes: expand (x depth), prune, pruned
         # view (which rows the target model computes), verify
+        stream = stream_override or torch.cuda.current_stream()
         rec = recs[i % len(recs)]
         ob = out_bufs[i % len(recs)]
         tree.begin_step()
@@ -177,10 +186,13 @@ def main():
         tree.verify(rec["target"], rec["T"], rec["rng_key"], out=ob, stream=stream)
 
     # ---- 2. timed replay ---------------------------------------------------
+    def check_one(i):
+        for a, b in zip(out_bufs[i], outs[i]):
+            assert torch.equal(a.cpu(), b.cpu()), "replay differs from discovery"
+
     def check(n_replayed):
         for i in range(min(n_replayed, len(recs))):
-            for a, b in zip(out_bufs[i], outs[i]):
-                assert torch.equal(a.cpu(), b.cpu()), "replay differs from discovery"
+            check_one(i)
 
     for i in range(args.warmup):
         replay(i)
@@ -196,8 +208,41 @@ def main():
     t1 = time.perf_counter()
     check(args.steps)
     assert tree.device_error() == 0
-    ms = (t1 - t0) * 1e3 / args.steps
-    steps_per_s = args.steps / (t1 - t0)
+    eager_ms = (t1 - t0) * 1e3 / args.steps
+    ms, steps_per_s, mode = eager_ms, args.steps / (t1 - t0), "eager"
+
+    # ---- 3. the same steps replayed as HIP graphs (one per recorded step):
+    #      the launch sequence of a step is captured once and replayed; every
+    #      replay must still reproduce the discovery outputs -------------------
+    graph_ms = None
+    if args.graph:
+        try:
+            cap = torch.cuda.Stream()
+            graphs = []
+            for i in range(len(recs)):
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g, stream=cap):
+                    replay(i, stream_override=cap)
+                graphs.append(g)
+            torch.cuda.synchronize()
+            for i in range(max(args.warmup, len(recs))):
+                for o in out_bufs[i % len(recs)]:
+                    o.fill_(-7)
+                graphs[i % len(recs)].replay()
+                torch.cuda.synchronize()
+                check_one(i % len(recs))
+            torch.cuda.synchronize()
+            g0 = time.perf_counter()
+            for i in range(args.steps):
+                graphs[i % len(recs)].replay()
+            torch.cuda.synchronize()
+            g1 = time.perf_counter()
+            check(args.steps)
+            assert tree.device_error() == 0
+            graph_ms = (g1 - g0) * 1e3 / args.steps
+            ms, steps_per_s, mode = graph_ms, args.steps / (g1 - g0), "hip-graph"
+        except (RuntimeError, AssertionError) as e:
+            log(f"graph replay unavailable ({e}); reporting the eager launch loop")
 
     # algorithmic bytes: every draft row once, the target rows on each walk
     rows_per_level = [w.B] + [w.B * w.n_expand] * (w.depth - 1)
@@ -263,7 +308,9 @@ def main():
                                f"budget={w.R} T={w.T} sparse top-{w.support} {w.dtype}",
                    "batch": w.B, "vocab": w.V, "K": w.K, "m": w.m, "depth": w.depth,
                    "budget": w.R, "T": w.T, "support": w.support},
-        "roofline": {"bound": "hbm", "kernel": "k_expand",
+        "mode": mode,
+        "eager_ms_per_step": round(eager_ms, 4),
+        "roofline": {"bound": "hbm", "kernel": "expand level (k_select + k_pool)",
                      "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS,
                      "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4),
                      "traffic": traffic,

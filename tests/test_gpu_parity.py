@@ -213,3 +213,42 @@ def test_frontier_view_matches_copy(dev):
                     for b in range(w.B)]
     assert tree.device_error() == 0
     tree.close()
+
+
+def test_graph_replay_matches_eager(dev):
+    """A captured step replays bit-exactly, several times, with eager steps
+    and synchronisations between the replays."""
+    from paper_2609_21827_amd.driver import make_tree, run_step
+    w = W["llama3"].with_(B=3, depth=4, R=20)
+    tree = make_tree(w, device=dev)
+    rec = {}
+    acc, alen, fin = run_step(tree, w, 0, device=dev, record=rec)
+    ref = (acc.cpu(), alen.cpu(), fin.cpu())
+    out = tuple(torch.empty_like(x, device=dev) for x in (acc, alen, fin))
+    pv = tuple(torch.empty((w.B, w.R + 1), dtype=torch.int32, device=dev) for _ in range(2))
+    cap = torch.cuda.Stream()
+
+    def step(stream):
+        tree.begin_step()
+        for rows in rec["draft"]:
+            tree.expand_level(rows, rec["T"], rec["rng_key"], stream=stream)
+        tree.prune(w.R, stream=stream)
+        tree.pruned_view(out=pv, stream=stream)
+        tree.verify(rec["target"], rec["T"], rec["rng_key"], out=out, stream=stream)
+
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=cap):
+        step(cap)
+    torch.cuda.synchronize()
+    for r in range(4):
+        for o in out:
+            o.fill_(-5)
+        g.replay()
+        torch.cuda.synchronize()
+        for a, b in zip(out, ref):
+            assert torch.equal(a.cpu(), b), f"replay {r}"
+        run_step(tree, w, 1 + r, device=dev)          # eager work in between
+        torch.cuda.synchronize()
+    assert tree.device_error() == 0
+    tree.close()
