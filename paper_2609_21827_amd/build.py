@@ -13,7 +13,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "librheo.so")
-SOURCES = ["api.hip", "expand.hip", "prune.hip", "verify.hip", "views.hip"]
+SOURCES = ["api.hip", "expand.hip", "dense.hip", "prune.hip", "verify.hip", "views.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 

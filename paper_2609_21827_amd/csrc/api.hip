@@ -37,6 +37,16 @@ constexpr int kMaxV = 262143;
 
 float k_of_T(float T) { return (float)(1.4426950408889634 / (double)T); }
 
+// tokens of one 64-vector sub-chunk (16-byte vectors of bf16 or fp32)
+int WAVE_TOKENS(int dtype) { return 64 * (dtype == RHEO_BF16 ? 8 : 4); }
+
+// A chunk size fits when the row's chunk lists fit the merge (and, in dense
+// mode, the weights pass's copy of them).
+bool variant_fits(int dtype, int v, int V, int SL, bool dense) {
+    const ExpandVariant ev = expand_variant(dtype, v, V, SL);
+    return ev.ok && (!dense || ev.C * ev.Sc <= 512);
+}
+
 }  // namespace
 
 struct rheo_tree {
@@ -48,7 +58,8 @@ struct rheo_tree {
     int variant = 0;
     int vG = 1, v_segch = 1, v_grid = 1;  // verification team shape
     float T_expand = 1.0f;
-    void* blocks[32] = {};
+    void* blocks[48] = {};
+    const void* draft[16] = {};           // dense: each level's draft rows (borrowed)
     int nblocks = 0;
 };
 
@@ -101,11 +112,16 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
     if (c.n_expand < 1 || c.n_expand > c.pool) return fail(RHEO_EINVAL, "n_expand must be in [1, K]");
     if (c.dtype != RHEO_F32 && c.dtype != RHEO_BF16) return fail(RHEO_EINVAL, "unknown dtype");
     if (c.reserved != 0) return fail(RHEO_EINVAL, "reserved field must be 0");
-    if (c.support <= 0) return fail(RHEO_EINVAL, "support S must be >= K (dense mode is not available)");
-    const int S = c.support < c.vocab ? c.support : c.vocab;
+    // support <= 0: dense mode, the support is the whole vocabulary
+    const bool dense = c.support <= 0;
+    const int S = dense ? c.vocab : (c.support < c.vocab ? c.support : c.vocab);
+    if (c.pool > c.vocab) return fail(RHEO_EINVAL, "pool K must be <= vocab");
     if (S < c.pool) return fail(RHEO_EINVAL, "support must be >= pool K");
-    if (S > 1024) return fail(RHEO_EINVAL, "support must be <= 1024");
+    if (!dense && S > 1024) return fail(RHEO_EINVAL, "support must be <= 1024");
     if (S <= c.leads) return fail(RHEO_EINVAL, "support must exceed leads m");
+    // list length of the selection pass: the support, or in dense mode the
+    // m + K tokens the pool can use
+    const int SL = dense ? (c.vocab < c.leads + c.pool ? c.vocab : c.leads + c.pool) : S;
     if (c.row_stride < c.vocab) return fail(RHEO_EINVAL, "row_stride must be >= vocab");
     const int esz = c.dtype == RHEO_BF16 ? 2 : 4;
     if ((c.row_stride * esz) % 16) return fail(RHEO_EINVAL, "row_stride must be a multiple of 16 bytes");
@@ -116,6 +132,8 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
     TreeDev& d = t->dev;
     d.B = c.batch; d.V = c.vocab; d.K = c.pool; d.m = c.leads; d.D = c.depth;
     d.NE = c.n_expand; d.S = S; d.dtype = c.dtype; d.stride = c.row_stride;
+    d.dense = dense ? 1 : 0;
+    d.NCH = (c.vocab + WAVE_TOKENS(c.dtype) - 1) / WAVE_TOKENS(c.dtype);
     d.eps = c.eps_m0;
     d.NN = 1 + c.pool + (c.depth - 1) * c.n_expand * c.pool;
     d.E = 1 + (c.depth - 1) * c.n_expand;
@@ -127,7 +145,7 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
     // would not fit the merge; RHEO_EXPAND_VARIANT picks another that fits
     t->variant = -1;
     for (int v = 2; v < expand_variant_count(c.dtype); ++v) {
-        if (expand_variant(c.dtype, v, c.vocab, S).ok) {
+        if (variant_fits(c.dtype, v, c.vocab, SL, dense)) {
             t->variant = v;
             break;
         }
@@ -135,20 +153,20 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
     if (t->variant < 0) {
         delete t;
         return fail(RHEO_EINVAL, "vocab %d with support %d exceeds the expand merge capacity",
-                    c.vocab, S);
+                    c.vocab, SL);
     }
     const char* env = getenv("RHEO_EXPAND_VARIANT");
     if (env) {
         const int v = atoi(env);
         if (v >= 0 && v < expand_variant_count(c.dtype) &&
-            expand_variant(c.dtype, v, c.vocab, S).ok)
+            variant_fits(c.dtype, v, c.vocab, SL, dense))
             t->variant = v;
     }
     {
-        const ExpandVariant ev = expand_variant(c.dtype, t->variant, c.vocab, S);
+        const ExpandVariant ev = expand_variant(c.dtype, t->variant, c.vocab, SL);
         d.C = ev.C;
         d.Sc = ev.Sc;
-        if (d.Sc != S) {   // chunks hold at least 4096 elements, supports at most 1024
+        if (d.Sc != SL) {   // chunks hold at least 4096 elements, lists at most 1024
             delete t;
             return fail(RHEO_EINVAL, "internal: expand chunk smaller than the support");
         }
@@ -164,8 +182,15 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
     rc = rc ? rc : dalloc(t, &d.path, B * NN);
     rc = rc ? rc : dalloc(t, &d.first_child, B * NN);
     rc = rc ? rc : dalloc(t, &d.exp_of, B * NN);
-    rc = rc ? rc : dalloc(t, &d.tail_id, B * E * S);
-    rc = rc ? rc : dalloc(t, &d.tail_q, B * E * S);
+    const size_t TS = dense ? 1 : S;              // dense mode keeps no tail copy
+    rc = rc ? rc : dalloc(t, &d.tail_id, B * E * TS);
+    rc = rc ? rc : dalloc(t, &d.tail_q, B * E * TS);
+    const size_t DN = dense ? 1 : 0;
+    rc = rc ? rc : dalloc(t, &d.dq, DN ? B * d.NE * (size_t)d.NCH : 1);
+    rc = rc ? rc : dalloc(t, &d.dpart, DN ? B * d.NE * (size_t)d.C * 2 : 1);
+    rc = rc ? rc : dalloc(t, &d.dflag, DN ? B * d.NE : 1);
+    rc = rc ? rc : dalloc(t, &d.dref, DN ? B * E : 1);
+    rc = rc ? rc : dalloc(t, &d.dleads, DN ? B * E * 16 : 1);
     rc = rc ? rc : dalloc(t, &d.zq, B * E);
     rc = rc ? rc : dalloc(t, &d.frontier, B * d.NE);
     rc = rc ? rc : dalloc(t, &d.fr_u, B * d.NE);
@@ -179,6 +204,7 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
     rc = rc ? rc : dalloc(t, &d.team_max, B * 64);
     rc = rc ? rc : dalloc(t, &d.team_chunk, B * 1024);
     rc = rc ? rc : dalloc(t, &d.team_sp, B * (1024 + 16));
+    rc = rc ? rc : dalloc(t, &d.team_nchunk, dense ? B * 1024 * 2 : 1);
     rc = rc ? rc : dalloc(t, &d.sel, B * d.NE * (size_t)d.C * d.Sc);
     rc = rc ? rc : dalloc(t, &d.row_cnt, B * d.NE);
     rc = rc ? rc : dalloc(t, &d.seq_cnt, B);
@@ -192,6 +218,7 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
     if (e == hipSuccess) e = hipMemset(d.team_epoch, 0, B * sizeof(uint64_t));
     if (e == hipSuccess) e = hipMemset(d.row_cnt, 0, B * d.NE * sizeof(uint32_t));
     if (e == hipSuccess) e = hipMemset(d.seq_cnt, 0, B * sizeof(uint32_t));
+    if (e == hipSuccess && dense) e = hipMemset(d.dflag, 0, B * d.NE * sizeof(int32_t));
     if (e == hipSuccess) e = hipMemset(d.pidx, 0xFF, B * NN * sizeof(int32_t));
     if (e == hipSuccess) e = hipMemset(d.frontier, 0, B * d.NE * sizeof(int32_t));
     if (e == hipSuccess) e = hipMemset(d.first_child, 0xFF, B * NN * sizeof(int32_t));
@@ -242,8 +269,16 @@ int rheo_expand_level(rheo_tree* t, const void* logits, float T, uint64_t key, v
     a.k1 = k_of_T(t->cfg.construct_tempered ? T : 1.0f);
     a.kT = k_of_T(T);
     a.rng_key = key;
-    const hipError_t e = launch_expand(t->dev, a, t->variant, (hipStream_t)stream);
+    hipError_t e;
+    if (t->dev.dense) {
+        e = launch_select(t->dev, a, t->variant, (hipStream_t)stream);
+        if (e == hipSuccess)
+            e = launch_dense(t->dev, a, expand_variant_nvc(t->variant), (hipStream_t)stream);
+    } else {
+        e = launch_expand(t->dev, a, t->variant, (hipStream_t)stream);
+    }
     if (e != hipSuccess) return hip_fail(e, "expand launch");
+    t->draft[t->level] = logits;
     t->T_expand = T;
     if (++t->level == t->dev.D) t->state = EXPANDED;
     return RHEO_OK;
@@ -306,6 +341,7 @@ int rheo_verify(rheo_tree* t, const void* logits, float T, uint64_t key, int32_t
     a.accept_len = accept_len;
     a.final_token = final_token;
     a.G = t->vG;
+    for (int i = 0; i < 16; ++i) a.draft[i] = t->draft[i];
     const hipError_t e = launch_verify(t->dev, a, t->v_segch, t->v_grid, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "verify launch");
     t->state = VERIFIED;

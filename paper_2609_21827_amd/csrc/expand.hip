@@ -27,6 +27,7 @@
 // through agent-coherent atomic stores and loads.
 #include "rheo_device.h"
 #include "rheo_state.h"
+#include "pool_common.h"
 
 namespace rheo {
 
@@ -44,7 +45,10 @@ __device__ __forceinline__ float elem(const uint4& v, int k) {
     return __uint_as_float(w[k]);
 }
 
-// Vector vi (VEC consecutive elements) of a row; elements past V read as -inf.
+// Vector vi (VEC consecutive elements) of a row; elements past V read as the
+// most negative finite value (bf16 0xFF7F, fp32 -inf).  A bf16 pair read as
+// one fp32 word must never be a NaN (the maxima below compare raw words), and
+// 0xFF80 (-inf) in the high half would make it one.
 template <int DT>
 __device__ __forceinline__ uint4 load_row_vec(const char* base, int vi, int V) {
     constexpr int VEC = DT ? 8 : 4;
@@ -57,8 +61,8 @@ __device__ __forceinline__ uint4 load_row_vec(const char* base, int vi, int V) {
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const int e0 = e + 2 * q;
-            const uint32_t lo = (e0 < V) ? p16[e0] : 0xFF80u;
-            const uint32_t hi = (e0 + 1 < V) ? p16[e0 + 1] : 0xFF80u;
+            const uint32_t lo = (e0 < V) ? p16[e0] : 0xFF7Fu;
+            const uint32_t hi = (e0 + 1 < V) ? p16[e0 + 1] : 0xFF7Fu;
             w[q] = lo | (hi << 16);
         }
     } else {
@@ -95,63 +99,6 @@ __host__ __device__ inline PoolLds pool_lds(int S, int C) {
     L.tx = L.ir + pad16(2 * S);
     L.bytes = L.tx + pad16(2 * S);
     return L;
-}
-
-// Orders LDS accesses of the lanes of one wave (no block barrier).
-__device__ __forceinline__ void wave_sync() {
-    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-}
-
-// Ranks of two keys at once (counts of larger keys among n unique keys in
-// LDS, 16-byte aligned); 16 keys per step keep eight loads in flight.
-__device__ __forceinline__ void count_greater2(const uint64_t* keys, int n, uint64_t k0,
-                                               uint64_t k1, int& c0, int& c1) {
-    const ulonglong2* kp = (const ulonglong2*)keys;
-    int a0 = 0, a1 = 0;
-    const int np = n >> 1;
-#pragma unroll 8
-    for (int j = 0; j < np; ++j) {
-        const ulonglong2 x = kp[j];
-        a0 += (int)(x.x > k0) + (int)(x.y > k0);
-        a1 += (int)(x.x > k1) + (int)(x.y > k1);
-    }
-    if (n & 1) {
-        const uint64_t x = keys[n - 1];
-        a0 += (int)(x > k0);
-        a1 += (int)(x > k1);
-    }
-    c0 = a0;
-    c1 = a1;
-}
-// Ranks (counts of larger keys) of keys[i] for i = tid, tid + NT, ...
-template <int NT>
-__device__ __forceinline__ void rank_all(const uint64_t* keys, int n, int16_t* rank) {
-    for (int i = threadIdx.x % NT; i < n; i += 2 * NT) {
-        const int i2 = i + NT;
-        int c0, c1;
-        count_greater2(keys, n, keys[i], i2 < n ? keys[i2] : ~0ull, c0, c1);
-        rank[i] = (int16_t)c0;
-        if (i2 < n) rank[i2] = (int16_t)c1;
-    }
-}
-
-// Synchronisation and sums over the NT threads that form a pool: one wave
-// (small supports) or the whole block.
-template <int NT>
-__device__ __forceinline__ void psync() {
-    if (NT == WAVE) wave_sync();
-    else __syncthreads();
-}
-template <int NT>
-__device__ __forceinline__ uint64_t psum(uint64_t v, uint64_t* sh) {
-    if (NT == WAVE) return wave_sum_u64(v);
-    return block_sum_u64<NT>(v, sh);
-}
-template <int NT>
-__device__ __forceinline__ bool pany(bool p) {
-    if (NT == WAVE) return __ballot(p) != 0ull;
-    return __syncthreads_or(p) != 0;
 }
 
 // The pool of one row from its merged support s_top (App. C.1), formed by
@@ -273,15 +220,7 @@ __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, 
         t.zq[(int64_t)b * t.E + e_idx] = Zq;
         t.first_child[nb + pu] = cb + j * K;
         t.exp_of[nb + pu] = e_idx;
-        if (level == 0) {
-            t.tok[nb] = -1;
-            t.par[nb] = -1;
-            t.meta[nb] = 0;
-            t.proxy[nb] = 1.0;
-            t.qtrue[nb] = 1.0;
-            t.score[nb] = 1.0;
-            t.path[nb] = 0;
-        }
+        if (level == 0) emit_root(t, nb);
     }
     // the K children: top-m leads, Y, fills (App. C.1)
     if (tid < K) {
@@ -300,12 +239,6 @@ __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, 
             item = s_xs[rk];
             kind = FILL;
         }
-        double pscore = 1.0;
-        uint64_t ppath = 0;
-        if (level > 0) {
-            pscore = t.score[nb + pu];
-            ppath = t.path[nb + pu];
-        }
         double proxy;
         const double dS1 = (double)S1;
         if (kind == SAMPLED) {
@@ -322,19 +255,7 @@ __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, 
             proxy = __ddiv_rn((double)s_w1[item], dS1);
         }
         const double qtrue = (kind == SAMPLED) ? __ddiv_rn((double)s_q[item], (double)Zq) : proxy;
-        const int uid = cb + j * K + s;
-        const int64_t o = nb + uid;
-        t.par[o] = pu;
-        t.meta[o] = (level + 1) | ((s + 1) << 8) | (kind << 16);
-        t.proxy[o] = proxy;
-        t.qtrue[o] = qtrue;
-        t.first_child[o] = -1;
-        t.exp_of[o] = -1;
-        __hip_atomic_store(&t.tok[o], key_id(s_top[item]), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store((uint64_t*)&t.score[o], (uint64_t)__double_as_longlong(__dmul_rn(pscore, proxy)),
-                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(&t.path[o], ppath | ((uint64_t)(s + 1) << (56 - 4 * level)),
-                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        emit_child(t, level, nb, pu, cb + j * K + s, s, kind, key_id(s_top[item]), proxy, qtrue);
     }
 }
 
@@ -345,7 +266,7 @@ __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, 
 __global__ __launch_bounds__(NTP) void k_pool(TreeDev t, LevelArgs a) {
     extern __shared__ __align__(16) uint8_t s_pdyn[];
     __shared__ uint64_t s_red[NTP / WAVE];
-    __shared__ int s_pu, s_yi, s_lastseq;
+    __shared__ int s_pu, s_yi;
     __shared__ uint64_t s_u;
     const PoolLds L = pool_lds(t.S, t.C);
     uint64_t* s_m = (uint64_t*)(s_pdyn + L.m);    // the C chunk lists, C * S keys
@@ -438,53 +359,8 @@ __global__ __launch_bounds__(NTP) void k_pool(TreeDev t, LevelArgs a) {
     }
     if (level + 1 >= t.D) return;
 
-    // the next frontier (Sec. 2.1; App. C.4, step 1: the next level expands
-    // the best-scoring new nodes): the last row of the sequence to finish
-    // ranks the level's P * K new children by priority and keeps the best
-    // n_expand
-    __atomic_signal_fence(__ATOMIC_SEQ_CST);
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    if (tid == 0) {
-        const uint32_t old = __hip_atomic_fetch_add(&t.seq_cnt[b], 1u, __ATOMIC_RELAXED,
-                                                    __HIP_MEMORY_SCOPE_AGENT);
-        s_lastseq = old == (uint32_t)(a.P - 1);
-        if (s_lastseq) __hip_atomic_store(&t.seq_cnt[b], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-    __syncthreads();
-    if (!s_lastseq) return;
-    const int n = a.P * K;                       // <= 225
-    const int cb = (level == 0) ? 1 : 1 + K + (level - 1) * NE * K;
-    uint64_t* s_hi = s_top;                      // free again: the pool is written
-    uint64_t* s_lo = s_k2;
-    if (tid < n) {
-        const int64_t o = nb + cb + tid;
-        const double sc = __longlong_as_double((long long)__hip_atomic_load(
-            (uint64_t*)&t.score[o], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-        const uint64_t pa = __hip_atomic_load(&t.path[o], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        uint64_t hi, lo;
-        prio_key(sc, level + 1, pa, hi, lo);
-        s_hi[tid] = hi;
-        s_lo[tid] = lo;
-    }
-    __syncthreads();
-    if (tid < n) {
-        const uint64_t hi = s_hi[tid], lo = s_lo[tid];
-        int rk = 0;
-#pragma unroll 8
-        for (int q = 0; q < n; ++q) {
-            const uint64_t h = s_hi[q], l = s_lo[q];
-            rk += (int)(h > hi) | ((int)(h == hi) & (int)(l > lo));
-        }
-        if (rk < NE) {
-            t.frontier[(int64_t)b * NE + rk] = cb + tid;
-            t.fr_u[(int64_t)b * NE + rk] =     // the draw of its sampled slot
-                philox_draw(a.rng_key, P_DRAFT, (uint64_t)b, (uint64_t)(cb + tid));
-            t.fr_parent[(int64_t)b * NE + rk] = tid / K;
-            t.fr_token[(int64_t)b * NE + rk] =
-                __hip_atomic_load(&t.tok[nb + cb + tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-    }
+    // the next frontier: the last row of the sequence to finish selects it
+    select_frontier(t, a, b, s_top, s_k2);
 }
 
 // ---------------------------------------------------------------------------
@@ -528,7 +404,7 @@ __device__ __forceinline__ void select_block(const TreeDev& t, const LevelArgs& 
     // word read as fp32 is its high element plus a fraction of one bf16 ulp
     // (the low element's bits), so the maximum over the raw words and the
     // unpacked low elements, with its low 16 bits cleared, is exactly the
-    // maximum element (logits are finite; padding words are NaN and ignored)
+    // maximum element (logits and padding are finite, so no word is a NaN)
     uint32_t vm[NM];
 #pragma unroll
     for (int q = 0; q < NM; ++q) vm[q] = 0;
@@ -776,15 +652,21 @@ static void launch_dt(const TreeDev& t, const LevelArgs& a, int v, dim3 grid, si
     }
 }
 
-hipError_t launch_expand(const TreeDev& t, const LevelArgs& a, int variant, hipStream_t s) {
+hipError_t launch_select(const TreeDev& t, const LevelArgs& a, int variant, hipStream_t s) {
     const int rows = t.B * a.P;
     const dim3 grid(t.C, rows);
     if (t.dtype) launch_dt<1>(t, a, variant, grid, 0, s);
     else launch_dt<0>(t, a, variant, grid, 0, s);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    k_pool<<<rows, NTP, (size_t)pool_lds(t.S, t.C).bytes, s>>>(t, a);
     return hipGetLastError();
 }
+
+hipError_t launch_expand(const TreeDev& t, const LevelArgs& a, int variant, hipStream_t s) {
+    hipError_t e = launch_select(t, a, variant, s);
+    if (e != hipSuccess) return e;
+    k_pool<<<t.B * a.P, NTP, (size_t)pool_lds(t.S, t.C).bytes, s>>>(t, a);
+    return hipGetLastError();
+}
+
+int expand_variant_nvc(int v) { return kNVC[v]; }
 
 }  // namespace rheo

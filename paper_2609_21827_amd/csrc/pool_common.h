@@ -1,0 +1,162 @@
+// Device helpers shared by the sparse and dense pool kernels: wave-level
+// synchronisation, ranking by counting, sums over the threads forming a
+// pool, a child record, and the frontier selection of a sequence.
+#pragma once
+
+#include "rheo_device.h"
+#include "rheo_state.h"
+
+namespace rheo {
+
+// Orders LDS accesses of the lanes of one wave (no block barrier).
+__device__ __forceinline__ void wave_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+}
+
+// Ranks of two keys at once (counts of larger keys among n unique keys in
+// LDS, 16-byte aligned); 16 keys per step keep eight loads in flight.
+__device__ __forceinline__ void count_greater2(const uint64_t* keys, int n, uint64_t k0,
+                                               uint64_t k1, int& c0, int& c1) {
+    const ulonglong2* kp = (const ulonglong2*)keys;
+    int a0 = 0, a1 = 0;
+    const int np = n >> 1;
+#pragma unroll 8
+    for (int j = 0; j < np; ++j) {
+        const ulonglong2 x = kp[j];
+        a0 += (int)(x.x > k0) + (int)(x.y > k0);
+        a1 += (int)(x.x > k1) + (int)(x.y > k1);
+    }
+    if (n & 1) {
+        const uint64_t x = keys[n - 1];
+        a0 += (int)(x > k0);
+        a1 += (int)(x > k1);
+    }
+    c0 = a0;
+    c1 = a1;
+}
+// Ranks (counts of larger keys) of keys[i] for i = tid, tid + NT, ...
+template <int NT>
+__device__ __forceinline__ void rank_all(const uint64_t* keys, int n, int16_t* rank) {
+    for (int i = threadIdx.x % NT; i < n; i += 2 * NT) {
+        const int i2 = i + NT;
+        int c0, c1;
+        count_greater2(keys, n, keys[i], i2 < n ? keys[i2] : ~0ull, c0, c1);
+        rank[i] = (int16_t)c0;
+        if (i2 < n) rank[i2] = (int16_t)c1;
+    }
+}
+
+// Synchronisation and sums over the NT threads that form a pool: one wave
+// (small supports) or the whole block.
+template <int NT>
+__device__ __forceinline__ void psync() {
+    if (NT == WAVE) wave_sync();
+    else __syncthreads();
+}
+template <int NT>
+__device__ __forceinline__ uint64_t psum(uint64_t v, uint64_t* sh) {
+    if (NT == WAVE) return wave_sum_u64(v);
+    return block_sum_u64<NT>(v, sh);
+}
+template <int NT>
+__device__ __forceinline__ bool pany(bool p) {
+    if (NT == WAVE) return __ballot(p) != 0ull;
+    return __syncthreads_or(p) != 0;
+}
+
+// One child record of expanded row j (slot s, 0-based; App. C.1): the
+// fields the frontier selection reads in other blocks (token, score, path)
+// are published with agent-scope atomics.
+__device__ __forceinline__ void emit_child(const TreeDev& t, int level, int64_t nb, int pu,
+                                           int uid, int s, int kind, int tok, double proxy,
+                                           double qtrue) {
+    double pscore = 1.0;
+    uint64_t ppath = 0;
+    if (level > 0) {
+        pscore = t.score[nb + pu];
+        ppath = t.path[nb + pu];
+    }
+    const int64_t o = nb + uid;
+    t.par[o] = pu;
+    t.meta[o] = (level + 1) | ((s + 1) << 8) | (kind << 16);
+    t.proxy[o] = proxy;
+    t.qtrue[o] = qtrue;
+    t.first_child[o] = -1;
+    t.exp_of[o] = -1;
+    __hip_atomic_store(&t.tok[o], tok, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store((uint64_t*)&t.score[o], (uint64_t)__double_as_longlong(__dmul_rn(pscore, proxy)),
+                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&t.path[o], ppath | ((uint64_t)(s + 1) << (56 - 4 * level)),
+                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// The root record (level 0 only).
+__device__ __forceinline__ void emit_root(const TreeDev& t, int64_t nb) {
+    t.tok[nb] = -1;
+    t.par[nb] = -1;
+    t.meta[nb] = 0;
+    t.proxy[nb] = 1.0;
+    t.qtrue[nb] = 1.0;
+    t.score[nb] = 1.0;
+    t.path[nb] = 0;
+}
+
+// The next frontier (Sec. 2.1; App. C.4, step 1: the next level expands the
+// best-scoring new nodes).  Called by every block of the pool kernel once
+// its children are written: the last row of sequence b to get here ranks
+// the level's P * K new children by priority and keeps the best n_expand,
+// with the Philox draw of each kept node's sampled slot.  s_hi and s_lo are
+// LDS arrays of at least 256 entries the caller no longer needs.
+__device__ __forceinline__ void select_frontier(const TreeDev& t, const LevelArgs& a, int b,
+                                                uint64_t* s_hi, uint64_t* s_lo) {
+    __shared__ int s_lastseq;
+    const int tid = threadIdx.x;
+    const int level = a.level;
+    const int K = t.K, NE = t.NE;
+    const int64_t nb = (int64_t)b * t.NN;
+    if (level + 1 >= t.D) return;
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (tid == 0) {
+        const uint32_t old = __hip_atomic_fetch_add(&t.seq_cnt[b], 1u, __ATOMIC_RELAXED,
+                                                    __HIP_MEMORY_SCOPE_AGENT);
+        s_lastseq = old == (uint32_t)(a.P - 1);
+        if (s_lastseq) __hip_atomic_store(&t.seq_cnt[b], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __syncthreads();
+    if (!s_lastseq) return;
+    const int n = a.P * K;                       // <= 225
+    const int cb = (level == 0) ? 1 : 1 + K + (level - 1) * NE * K;
+    if (tid < n) {
+        const int64_t o = nb + cb + tid;
+        const double sc = __longlong_as_double((long long)__hip_atomic_load(
+            (uint64_t*)&t.score[o], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+        const uint64_t pa = __hip_atomic_load(&t.path[o], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        uint64_t hi, lo;
+        prio_key(sc, level + 1, pa, hi, lo);
+        s_hi[tid] = hi;
+        s_lo[tid] = lo;
+    }
+    __syncthreads();
+    if (tid < n) {
+        const uint64_t hi = s_hi[tid], lo = s_lo[tid];
+        int rk = 0;
+#pragma unroll 8
+        for (int q = 0; q < n; ++q) {
+            const uint64_t h = s_hi[q], l = s_lo[q];
+            rk += (int)(h > hi) | ((int)(h == hi) & (int)(l > lo));
+        }
+        if (rk < NE) {
+            t.frontier[(int64_t)b * NE + rk] = cb + tid;
+            t.fr_u[(int64_t)b * NE + rk] =     // the draw of its sampled slot
+                philox_draw(a.rng_key, P_DRAFT, (uint64_t)b, (uint64_t)(cb + tid));
+            t.fr_parent[(int64_t)b * NE + rk] = tid / K;
+            t.fr_token[(int64_t)b * NE + rk] =
+                __hip_atomic_load(&t.tok[nb + cb + tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+    }
+}
+
+}  // namespace rheo

@@ -46,8 +46,19 @@ struct TreeDev {
     uint32_t* team_max;            // [B][GMAX] segment maxima (fp32 bits)
     uint64_t* team_chunk;          // [B][NCMAX] chunk totals of p's weights
     uint32_t* team_sp;             // [B][SPMAX] p's weights at the special tokens
+    uint64_t* team_nchunk;         // dense: [B][NCMAX][2] residual chunk totals (u128)
     // expansion: each row's C chunk lists of Sc selection keys, sorted
     uint64_t* sel;                 // [B * NE][C][Sc]
+    // dense mode (the support is all of V): per row the tail-weight totals
+    // of each 64-vector sub-chunk, the chunks' sums (w1, q) and the rank-tie
+    // flag; per expanded node the logit of x_{m+1} and the leads
+    int dense;
+    int NCH;                       // sub-chunks per row (dense)
+    uint64_t* dq;                  // [B * NE][NCH]
+    uint64_t* dpart;               // [B * NE][C][2]
+    int32_t* dflag;                // [B * NE]
+    float* dref;                   // [B][E]
+    int32_t* dleads;               // [B][E][16]
     uint32_t* row_cnt;             // [B * NE] chunk blocks arrived (0 between launches)
     uint32_t* seq_cnt;             // [B] rows whose pool is written (0 between launches)
     int C, Sc;
@@ -64,6 +75,7 @@ struct LevelArgs {
 
 struct VerifyArgs {
     const void* logits;
+    const void* draft[16];         // dense: each level's draft rows (borrowed)
     int R;
     int G;                         // blocks per sequence (a team)
     int NV;                        // chunks per segment
@@ -76,6 +88,8 @@ struct VerifyArgs {
 
 hipError_t launch_expand(const TreeDev& t, const LevelArgs& a, int variant,
                          hipStream_t s);
+hipError_t launch_select(const TreeDev& t, const LevelArgs& a, int variant, hipStream_t s);
+hipError_t launch_dense(const TreeDev& t, const LevelArgs& a, int nvc, hipStream_t s);
 hipError_t launch_prune(const TreeDev& t, int R, hipStream_t s);
 hipError_t verify_shape(const TreeDev& t, int* G, int* segch, int* grid);
 hipError_t launch_verify(const TreeDev& t, const VerifyArgs& a, int segch, int grid,
@@ -89,6 +103,7 @@ struct ExpandVariant {
     bool ok;                       // the row's C * Sc keys fit the merge
 };
 int expand_variant_count(int dtype);
+int expand_variant_nvc(int v);
 ExpandVariant expand_variant(int dtype, int v, int V, int S);
 
 }  // namespace rheo

@@ -182,7 +182,7 @@ __device__ bool team_barrier(uint64_t* flags, int g, int G, uint64_t epoch, int3
     return *s_ok != 0;
 }
 
-template <int DT>
+template <int DT, int DN>
 __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
     constexpr int VEC = DT ? 8 : 4;
     constexpr int ESZ = DT ? 2 : 4;
@@ -198,6 +198,8 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
     __shared__ uint64_t s_red[NWV];
     __shared__ float s_redf[NWV];
     __shared__ int s_c_uid[16], s_c_tok[16], s_c_slot[16], s_c_tail[16], s_c_zero[16];
+    __shared__ uint32_t s_c_q[16];               // dense: q~ weights of the candidates
+    __shared__ int s_lead[16];                   // dense: the node's leads
     __shared__ int s_nc, s_spos, s_mode, s_next, s_token, s_cstar;
     __shared__ uint64_t s_U[16], s_Ufin;         // the layer's uniforms
     __shared__ u128 s_F, s_Zrem, s_tt;
@@ -227,6 +229,12 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
     uint32_t* tmax_x = t.team_max + (int64_t)b * GMAX;
     uint64_t* chunk_x = t.team_chunk + (int64_t)b * NCMAX;
     uint32_t* sp_x = t.team_sp + (int64_t)b * SPMAX;
+    uint64_t* nchunk_x = t.team_nchunk + (int64_t)b * NCMAX * 2;   // dense residual totals
+    auto nchunk_at = [&](int c) -> u128 {
+        const uint64_t lo = __hip_atomic_load(&nchunk_x[2 * c], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const uint64_t hi = __hip_atomic_load(&nchunk_x[2 * c + 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return ((u128)hi << 64) | lo;
+    };
     const int c0 = g * SEGCH;                 // first chunk of this segment
     const int c1 = min(NC, c0 + SEGCH);
 
@@ -242,7 +250,18 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
         //      order) and all of the layer's uniforms ------------------------
         const int fc = t.first_child[nb + cur];
         const int e = t.exp_of[nb + cur];
-        const int nt = (fc >= 0) ? t.S - t.m : 0;
+        const int nt = (fc >= 0 && !DN) ? t.S - t.m : 0;
+        // dense mode: q~ at this node comes from its draft row (borrowed),
+        // the logit of its x_{m+1} and its leads
+        const char* drow = nullptr;
+        float dref = 0.0f;
+        const int nlead = (DN && fc >= 0) ? t.m : 0;
+        if (DN && fc >= 0) {
+            const int rowi = (level == 0) ? b : b * t.NE + (e - 1 - (level - 1) * t.NE);
+            drow = (const char*)a.draft[level] + (int64_t)rowi * t.stride * ESZ;
+            dref = t.dref[(int64_t)b * t.E + e];
+            if (tid < nlead) s_lead[tid] = t.dleads[((int64_t)b * t.E + e) * 16 + tid];
+        }
         if (tid < WAVE) {
             bool keep = false;
             int kind = -1, tok = -1;
@@ -250,6 +269,13 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
                 keep = t.pidx[nb + fc + lane] > 0;
                 kind = (t.meta[nb + fc + lane] >> 16) & 0xFF;
                 tok = t.tok[nb + fc + lane];
+            }
+            uint32_t cq = 0;
+            if (DN && keep) {
+                bool lead = false;
+                for (int q = 0; q < nlead; ++q)
+                    lead |= t.dleads[((int64_t)b * t.E + e) * 16 + q] == tok;
+                cq = lead ? 0u : cweight(load_logit<DT>(drow, tok), dref, a.kT);
             }
             const uint64_t msk = __ballot(keep);
             const uint64_t smk = __ballot(keep && kind == SAMPLED);
@@ -260,6 +286,7 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
                 s_c_tok[pos] = tok;
                 s_c_slot[pos] = lane + 1;
                 s_c_zero[pos] = 0;
+                s_c_q[pos] = cq;
             }
             if (lane == 0) {
                 s_nc = __popcll(msk);
@@ -292,7 +319,7 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
                 s_tq[i] = t.tail_q[tb + i];
             }
         }
-        if (!team_barrier(flags, g, G, epoch + 2 * level + 1, t.err, &s_ok)) break;
+        if (!team_barrier(flags, g, G, epoch + 3 * level + 1, t.err, &s_ok)) break;
         const int nc = s_nc, spos = s_spos;
         if (tid < WAVE) {
             float v = -INFINITY;
@@ -334,7 +361,7 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
                                        __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
         }
-        if (!team_barrier(flags, g, G, epoch + 2 * level + 2, t.err, &s_ok)) break;
+        if (!team_barrier(flags, g, G, epoch + 3 * level + 2, t.err, &s_ok)) break;
         uint64_t part = 0;
         for (int c = tid; c < NC; c += NTV) {
             const uint64_t v = __hip_atomic_load(&chunk_x[c], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -346,15 +373,15 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
         if (tid < nc) s_c_tail[tid] = find_sorted(s_tid, nt, s_c_tok[tid]);
         const uint64_t Sp = block_sum_u64<NTV>(part, s_red);
         // ---- 3. Algorithm 1 at this layer -----------------------------------
-        const uint64_t Zq = (nt > 0) ? t.zq[(int64_t)b * t.E + e] : 1;
+        const uint64_t Zq = (fc >= 0) ? t.zq[(int64_t)b * t.E + e] : 1;
         if (tid == 0) {
             int mode = 0;          // 0: residual tests follow, 1: accepted, 2: final sample
             int next = -1, token = -1;
             if (nc == 0) mode = 2;
             if (spos >= 0) {
                 const int yi = s_c_tail[spos];
-                if (yi < 0) atomicOr(t.err, 4);
-                const uint64_t QY = (yi >= 0) ? s_tq[yi] : 0;
+                if (!DN && yi < 0) atomicOr(t.err, 4);
+                const uint64_t QY = DN ? (uint64_t)s_c_q[spos] : ((yi >= 0) ? s_tq[yi] : 0);
                 const uint64_t PY = s_tp[nt + spos];
                 const uint64_t U = s_U[0];
                 if ((u128)(U + 1) * QY * Sp <= (((u128)PY * Zq) << 32)) {
@@ -370,7 +397,39 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
         }
         __syncthreads();
         const bool residual = (spos >= 0 && s_mode == 0);   // Y rejected: r from p - q~
-        if (residual) {
+        if (DN && residual) {
+            // N_v = max(0, P_v Zq - Q_v Sp) over all of V (Q_v from the draft
+            // row, 0 at the leads): chunk totals over the segment, exchanged
+            for (int c = c0 + wid; c < c1; c += NWV) {
+                const uint4 xv = load_vec<DT>(row, c * WAVE + lane, V);
+                const uint4 dv = load_vec<DT>(drow, c * WAVE + lane, V);
+                u128 sum = 0;
+#pragma unroll
+                for (int k = 0; k < VEC; ++k) {
+                    const int v = (c * WAVE + lane) * VEC + k;
+                    if (v < V) {
+                        bool lead = false;
+                        for (int q = 0; q < nlead; ++q) lead |= s_lead[q] == v;
+                        const uint64_t P = cweight(velem<DT>(xv, k), M, a.kT);
+                        const uint64_t Q = lead ? 0u : cweight(velem<DT>(dv, k), dref, a.kT);
+                        const u128 pz = (u128)P * Zq, qs = (u128)Q * Sp;
+                        sum += pz > qs ? pz - qs : (u128)0;
+                    }
+                }
+                sum = wave_sum_u128(sum);
+                if (lane == 0) {
+                    __hip_atomic_store(&nchunk_x[2 * c], (uint64_t)sum, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+                    __hip_atomic_store(&nchunk_x[2 * c + 1], (uint64_t)(sum >> 64), __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+                }
+            }
+            if (!team_barrier(flags, g, G, epoch + 3 * level + 3, t.err, &s_ok)) break;
+            u128 part = 0;
+            for (int c = tid; c < NC; c += NTV) part += nchunk_at(c);
+            const u128 tot = block_sum_u128(part, s_w128);
+            if (tid == 0) s_Zrem = tot;
+        } else if (residual) {
             // Z_r = Zq Sp - sum over the tail of min(P_v Zq, Q_v Sp)
             u128 d = 0;
             for (int i = tid; i < nt; i += NTV) {
@@ -392,7 +451,10 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
                 const int ti = s_c_tail[ci];
                 const uint64_t P = s_tp[nt + ci];
                 u128 Nu = F * (u128)P;
-                if (residual && ti >= 0) {
+                if (DN && residual) {
+                    const u128 pz = (u128)P * Zq, qs = (u128)s_c_q[ci] * Sp;
+                    Nu = pz > qs ? pz - qs : (u128)0;
+                } else if (residual && ti >= 0) {
                     const u128 pz = (u128)P * Zq, qs = (u128)s_tq[ti] * Sp;
                     Nu = pz > qs ? pz - qs : (u128)0;
                 }
@@ -456,12 +518,24 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
             }
             *def_out = d;
         };
-        u128 mysum = 0;
-        for (int c = ca; c < cz; ++c) {
+        // chunk weight of r: dense residual totals, else F times p's chunk
+        // total, less the special tokens' corrections
+        auto chunk_w = [&](int c) -> u128 {
+            if (DN && residual) {
+                u128 w = nchunk_at(c);
+                for (int ci = 0; ci < nc; ++ci) {
+                    if (!s_c_zero[ci] || s_c_tok[ci] / CH != c) continue;
+                    const u128 pz = (u128)s_tp[nt + ci] * Zq, qs = (u128)s_c_q[ci] * Sp;
+                    w -= pz > qs ? pz - qs : (u128)0;
+                }
+                return w;
+            }
             u128 d;
             special_def(c, &d);
-            mysum += F * (u128)s_chunk[c] - d;
-        }
+            return F * (u128)s_chunk[c] - d;
+        };
+        u128 mysum = 0;
+        for (int c = ca; c < cz; ++c) mysum += chunk_w(c);
         u128 total;
         const u128 pre = block_excl_scan_u128(mysum, s_w128, &total);
         if (tid == 0) s_cstar = -1;
@@ -469,9 +543,7 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
         if (tt >= pre && tt < pre + mysum) {
             u128 acc = pre;
             for (int c = ca; c < cz; ++c) {
-                u128 d;
-                special_def(c, &d);
-                const u128 w = F * (u128)s_chunk[c] - d;
+                const u128 w = chunk_w(c);
                 if (tt < acc + w) {
                     s_cstar = c;
                     s_tt = tt - acc;
@@ -492,7 +564,20 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
         const u128 t2 = s_tt;
         for (int i = tid; i < CH; i += NTV) {
             const int v = cs * CH + i;
-            s_cn[i] = (v < V) ? F * (u128)cweight(load_logit<DT>(row, v), M, a.kT) : (u128)0;
+            u128 w = 0;
+            if (v < V) {
+                const uint64_t P = cweight(load_logit<DT>(row, v), M, a.kT);
+                if (DN && residual) {
+                    bool lead = false;
+                    for (int q = 0; q < nlead; ++q) lead |= s_lead[q] == v;
+                    const uint64_t Q = lead ? 0u : cweight(load_logit<DT>(drow, v), dref, a.kT);
+                    const u128 pz = (u128)P * Zq, qs = (u128)Q * Sp;
+                    w = pz > qs ? pz - qs : (u128)0;
+                } else {
+                    w = F * (u128)P;
+                }
+            }
+            s_cn[i] = w;
         }
         __syncthreads();
         if (residual) {
@@ -538,6 +623,11 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
     if (g == 0 && tid == 0) t.team_epoch[b] = epoch + 64;   // > every epoch this call used
 }
 
+static const void* verify_fn(const TreeDev& t) {
+    if (t.dense) return t.dtype ? (const void*)&k_verify<1, 1> : (const void*)&k_verify<0, 1>;
+    return t.dtype ? (const void*)&k_verify<1, 0> : (const void*)&k_verify<0, 0>;
+}
+
 // Team shape for a tree: about `target` blocks in all (1024 by default),
 // segments of whole chunks, G <= GMAX, every block co-resident (cooperative
 // launch).
@@ -549,7 +639,7 @@ hipError_t verify_shape(const TreeDev& t, int* G_out, int* segch, int* grid) {
     int dev = 0, cus = 0, per_cu = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-    const void* fn = t.dtype ? (const void*)&k_verify<1> : (const void*)&k_verify<0>;
+    const void* fn = verify_fn(t);
     if (e == hipSuccess) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, NTV, 0);
     if (e != hipSuccess) return e;
     const int teams_per_xcd = (t.B + 7) / 8;
@@ -568,7 +658,7 @@ hipError_t verify_shape(const TreeDev& t, int* G_out, int* segch, int* grid) {
 
 hipError_t launch_verify(const TreeDev& t, const VerifyArgs& a, int segch, int grid,
                          hipStream_t s) {
-    const void* fn = t.dtype ? (const void*)&k_verify<1> : (const void*)&k_verify<0>;
+    const void* fn = verify_fn(t);
     TreeDev tt = t;
     VerifyArgs aa = a;
     aa.NV = segch;

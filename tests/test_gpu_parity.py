@@ -93,6 +93,8 @@ def test_tiny_variants(dev, over):
 @pytest.mark.parametrize("over", [
     dict(V=1001, dtype="f32", recipe="zipf", support=128, K=5, depth=4, R=20),
     dict(V=1003, dtype="bf16", recipe="zipf", support=128, K=5, depth=4, R=20),
+    # a small support makes the row's last, partial vector matter often
+    dict(V=1003, dtype="bf16", recipe="zipf", support=6, K=5, depth=4, R=20, B=3),
     dict(V=200, dtype="bf16", recipe="zipf", support=1024, K=6, depth=3, R=15),
     dict(V=300, dtype="bf16", recipe="flat", support=128, K=4, depth=3, R=12),
     dict(V=5000, dtype="bf16", recipe="zipf", quantum=0.5, support=128, K=4, depth=3, R=12),
@@ -252,3 +254,49 @@ def test_graph_replay_matches_eager(dev):
         torch.cuda.synchronize()
     assert tree.device_error() == 0
     tree.close()
+
+
+# ---- dense mode: the support is the whole vocabulary ---------------------
+
+def test_dense_tiny_many_steps(dev):
+    run_parity(W["tiny"].with_(name="tiny_dense", support=0), range(60), [0], dev=dev)
+
+
+@pytest.mark.parametrize("over", [
+    dict(), dict(K=1, m=0, R=3, n_expand=1), dict(m=0, eps_m0=2.0 ** -20),
+    dict(construct_tempered=True, T=0.6), dict(T=2.0), dict(B=3), dict(K=4, m=2, R=10),
+])
+def test_dense_tiny_variants(dev, over):
+    w = W["tiny"].with_(name="tiny_dense", support=0, **over)
+    run_parity(w, range(12), list(range(w.B)), dev=dev)
+
+
+@pytest.mark.parametrize("over", [
+    dict(V=1001, dtype="f32", recipe="zipf", K=5, depth=4, R=20),
+    dict(V=1003, dtype="bf16", recipe="zipf", K=5, depth=4, R=20),
+    dict(V=300, dtype="bf16", recipe="flat", K=4, depth=3, R=12),
+    dict(V=5000, dtype="bf16", recipe="zipf", quantum=0.5, K=4, depth=3, R=12),
+    dict(V=4099, dtype="f32", recipe="zipf_t3", K=6, depth=4, R=30, B=2, T=0.6),
+    dict(V=70001, dtype="bf16", recipe="zipf", K=8, depth=2, R=10),
+])
+def test_dense_edge_shapes(dev, over):
+    w = W["tiny"].with_(name="edge_dense", sigma=1.5, sigma_t=0.8, support=0, **over)
+    tree_kw = {}
+    if w.V % 8:
+        tree_kw["row_stride"] = (w.V + 7) // 8 * 8
+    run_parity(w, range(2), list(range(w.B)), dev=dev, tree_kw=tree_kw)
+
+
+def test_dense_llama2(dev):
+    run_parity(W["llama2"].with_(name="llama2_dense", support=0, depth=4, R=30), range(2), [0],
+               dev=dev)
+
+
+def test_dense_llama3(dev):
+    run_parity(W["llama3"].with_(name="llama3_dense", support=0, depth=3, R=20), [0], [0],
+               T=0.6, dev=dev)
+
+
+def test_dense_batched(dev):
+    w = W["headline"].with_(name="headline_dense", support=0, B=8, depth=3, R=20)
+    run_parity(w, [0], [0, 5], dev=dev)
