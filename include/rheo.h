@@ -77,8 +77,10 @@ typedef struct rheo_config {
                                     1..K (EAGLE expands K, Sec. 2.1); 0 means K         */
     int32_t support;             /* S: draft logits truncated to their top-S entries
                                     before the softmax (Sec. 3.2, sparse draft; the
-                                    paper uses 128, App. B).  K <= S <= 1024; S >= V
-                                    keeps the whole vocabulary                          */
+                                    paper uses 128, App. B).  K <= S <= 1024.
+                                    S <= 0 selects dense mode: the support is the whole
+                                    vocabulary, and verification re-reads the draft
+                                    rows (see rheo_expand_level)                        */
     int32_t construct_tempered;  /* 0: tree built on untempered q (Sec. 5.4);
                                     1: on the tempered q_T                              */
     int32_t dtype;               /* RHEO_F32 or RHEO_BF16                               */
@@ -109,7 +111,10 @@ int rheo_begin_step(rheo_tree* tree);
  * path score) and, below the last level, selects the n_expand children with
  * the highest path scores as the next frontier.  With support S, the
  * truncated distribution is kept in the tree for verification, so the
- * draft buffer may be reused as soon as this call's work has run. */
+ * draft buffer may be reused as soon as this call's work has run.  In dense
+ * mode the tree borrows draft_logits: verification re-reads the rows of the
+ * nodes it walks, so the buffer of every level must stay allocated and
+ * unchanged until the step's rheo_verify has run on its stream. */
 int rheo_expand_level(rheo_tree* tree, const void* draft_logits, float T,
                       uint64_t rng_key, void* stream);
 

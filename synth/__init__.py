@@ -21,6 +21,9 @@ fp32 row):
           token (near one-hot peaks)
   flat    all logits 0 (uniform distributions; every comparison a tie)
   quantum > 0 rounds every logit to a multiple of it (massive ties)
+  near_ties > 0 shifts the row's maximum to 0.125 and puts the next fp32
+          values below it on low token ids (distinct logits whose integer
+          weights coincide)
   target  = draft row of the same node + sigma_t * N'_v (an independent
           noise stream of the same node key), rounded like the draft
 Noise variates come from 65536-entry quantile tables indexed by a 16-bit
@@ -69,6 +72,9 @@ class Workload:
     sigma_t: float = 0.7        # target divergence (fixed)
     sigma_t_range: tuple = None  # per-sequence U(lo, hi) divergence
     quantum: float = 0.0        # > 0: logits rounded to multiples of it (ties)
+    near_ties: int = 0          # > 0: the row is shifted so its maximum is 0.125
+                                # and tokens 1, 4, 7, ... get the next values
+                                # below it, one fp32 ulp apart
     seed: int = 0x5EED0000
     n_expand: int = None
     construct_tempered: bool = False
@@ -249,6 +255,13 @@ def _draft_fp32(w, keys, device):
             for i, (pk, t) in enumerate(zip(peak, tok)):
                 if pk:
                     row[i, t] = row[i, t] + np.float32(12.0)
+    if w.near_ties:
+        mx = row.max(dim=1, keepdim=True).values
+        row = (row - mx) + np.float32(0.125)
+        x = torch.full_like(mx, 0.125)
+        for j in range(w.near_ties):
+            x = torch.nextafter(x, torch.full_like(x, -np.inf))
+            row[:, 1 + 3 * j] = x[:, 0]
     return row
 
 

@@ -287,6 +287,16 @@ def test_dense_edge_shapes(dev, over):
     run_parity(w, range(2), list(range(w.B)), dev=dev, tree_kw=tree_kw)
 
 
+@pytest.mark.parametrize("support", [0, 16])
+def test_near_ties(dev, support):
+    """Distinct logits a few ulps below the maximum share its integer weight:
+    ranks by (weight, id) then differ from ranks by logit (dense mode takes
+    its exact fallbacks; sparse mode its tie-aware ranking)."""
+    w = W["tiny"].with_(name="near_ties", V=1001, dtype="f32", recipe="zipf", sigma=1.5,
+                        sigma_t=0.8, K=3, m=1, depth=3, R=8, support=support, near_ties=6)
+    run_parity(w, range(4), [0], dev=dev, tree_kw={"row_stride": 1004})
+
+
 def test_dense_llama2(dev):
     run_parity(W["llama2"].with_(name="llama2_dense", support=0, depth=4, R=30), range(2), [0],
                dev=dev)
