@@ -13,7 +13,7 @@ Protocol
      cycling over the recorded steps, bracketed by torch.cuda.synchronize();
      every replay must reproduce the discovery outputs bit for bit.
   3. HIP events around each rheo_expand_level call (on the stream it launches
-     on) give the duration of an expand level (k_select + k_pool, the
+     on) give the duration of an expand level (k_select and the pool kernels, the
      dominant work); its algorithmic bytes are the draft rows it must read
      (rows x V x 2 bytes).  Then the same steps are captured as HIP graphs
      (one per recorded step) and replayed; `value` is the graph-replay
@@ -40,7 +40,8 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-KERNEL_SRCS = ["expand.hip", "rheo_device.h", "rheo_state.h"]
+KERNEL_SRCS = ["expand.hip", "dense.hip", "pool_common.h", "rheo_device.h", "rheo_state.h"]
+EXPAND_KERNELS = r"k_select|k_pool|k_dweights|k_dpool"
 
 
 def kernel_src_hash():
@@ -65,15 +66,20 @@ def _counter_rows(path, regex, counter):
     return list(vals.values())
 
 
-def write_traffic(paths, out, workload, copy_bytes):
+def expand_kernel_name(w):
+    return ("expand level (k_select + k_pool)" if w.support > 0
+            else "expand level (k_select + k_dweights + k_dpool)")
+
+
+def write_traffic(paths, out, w, copy_bytes):
     """Scales the expand kernel's FETCH_SIZE / WRITE_SIZE by what the same
     counters read for a plain device copy of known size."""
     exp_f, exp_w, cp_f, cp_w = paths
-    # one expand level = one k_select and one k_pool dispatch
+    # one expand level = one k_select dispatch and the pool kernel(s) after it
     nf = len(_counter_rows(exp_f, r"k_select", "FETCH_SIZE"))
     nw = len(_counter_rows(exp_w, r"k_select", "WRITE_SIZE"))
-    ef = [sum(_counter_rows(exp_f, r"k_select|k_pool", "FETCH_SIZE")) / nf]
-    ew = [sum(_counter_rows(exp_w, r"k_select|k_pool", "WRITE_SIZE")) / nw]
+    ef = [sum(_counter_rows(exp_f, EXPAND_KERNELS, "FETCH_SIZE")) / nf]
+    ew = [sum(_counter_rows(exp_w, EXPAND_KERNELS, "WRITE_SIZE")) / nw]
     cf = _counter_rows(cp_f, r"copy|Copy", "FETCH_SIZE")
     cw = _counter_rows(cp_w, r"copy|Copy", "WRITE_SIZE")
     # every copy dispatch moves copy_bytes in and copy_bytes out
@@ -81,7 +87,7 @@ def write_traffic(paths, out, workload, copy_bytes):
     k_w = copy_bytes / (sum(cw) / len(cw) * 1024)
     fetch = sum(ef) / len(ef) * 1024 * k_f
     write = sum(ew) / len(ew) * 1024 * k_w
-    res = {"workload": workload, "kernel": "expand level (k_select + k_pool)",
+    res = {"workload": w.name, "kernel": expand_kernel_name(w),
            "kernel_src_sha256": kernel_src_hash(),
            "levels": nf, "copy_dispatches": len(cf),
            "copy_bytes": copy_bytes,
@@ -108,8 +114,8 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--graph", type=int, default=1,
                     help="1: the timed loop replays each step as a captured HIP graph")
-    ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles",
-                                                      "expand_level_headline_traffic.json"))
+    ap.add_argument("--traffic", default=None,
+                    help="traffic file (default profiles/expand_level_<workload>_traffic.json)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB five times "
                          "(counter calibration under rocprofv3 --pmc)")
@@ -118,10 +124,15 @@ def main():
                     help="write the traffic file from four rocprofv3 --pmc "
                          "counter_collection.csv files, then exit")
     args = ap.parse_args()
+    if args.traffic is None:
+        args.traffic = os.path.join(ROOT, "profiles",
+                                    f"expand_level_{args.workload}_traffic.json")
 
     if args.traffic_from:
+        import synth
         assert args.copy_probe, "--traffic-from needs the --copy-probe size that was profiled"
-        write_traffic(args.traffic_from, args.traffic, args.workload, args.copy_probe << 20)
+        write_traffic(args.traffic_from, args.traffic, synth.WORKLOADS[args.workload],
+                      args.copy_probe << 20)
         return
 
     if args.gpus != 1:
@@ -305,12 +316,14 @@ def main():
         "dtype": w.dtype,
         "data": "synthetic",
         "config": {"workload": f"{w.name}: B={w.B} V={w.V} K={w.K} m={w.m} depth={w.depth} "
-                               f"budget={w.R} T={w.T} sparse top-{w.support} {w.dtype}",
+                               f"budget={w.R} T={w.T} "
+                               + (f"sparse top-{w.support}" if w.support > 0 else "dense")
+                               + f" {w.dtype}",
                    "batch": w.B, "vocab": w.V, "K": w.K, "m": w.m, "depth": w.depth,
                    "budget": w.R, "T": w.T, "support": w.support},
         "mode": mode,
         "eager_ms_per_step": round(eager_ms, 4),
-        "roofline": {"bound": "hbm", "kernel": "expand level (k_select + k_pool)",
+        "roofline": {"bound": "hbm", "kernel": expand_kernel_name(w),
                      "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS,
                      "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4),
                      "traffic": traffic,

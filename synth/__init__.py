@@ -130,6 +130,11 @@ WORKLOADS = {
                          T=1.0, dtype="bf16", support=128, recipe="zipf",
                          sigma=1.5, sigma_t_range=(0.3, 1.5), seed=0x5EED0006,
                          steps=20),
+    # the headline shape with the full-vocabulary (dense) distributions
+    "headline_dense": Workload("headline_dense", B=64, V=128256, K=8, m=1, depth=7, R=60,
+                               T=1.0, dtype="bf16", support=0, recipe="zipf",
+                               sigma=1.5, sigma_t_range=(0.3, 1.5), seed=0x5EED0007,
+                               steps=20),
 }
 
 

@@ -310,3 +310,8 @@ def test_dense_llama3(dev):
 def test_dense_batched(dev):
     w = W["headline"].with_(name="headline_dense", support=0, B=8, depth=3, R=20)
     run_parity(w, [0], [0, 5], dev=dev)
+
+
+def test_headline_dense(dev):
+    """The dense bench workload at its full size, sampled sequences."""
+    run_parity(W["headline_dense"], [0], [0, 63], dev=dev)
