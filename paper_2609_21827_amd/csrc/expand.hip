@@ -74,12 +74,12 @@ __device__ __forceinline__ uint4 load_row_vec(const char* base, int vi, int V) {
 }
 
 // ---------------------------------------------------------------------------
-// the pool of one row, formed by the last of its chunk blocks: parent,
-// support, distributions and children
+// the pool of one row: parent, support, distributions and children
 // ---------------------------------------------------------------------------
-// LDS layout of the pool phase inside the block's dynamic buffer; the
-// previous level's priority keys (<= 225 of them) share the regions of the
-// support and the ranking keys.
+// LDS layout of the pool kernel's dynamic buffer: the chunk lists and one
+// empty list after them, the support, ranking keys and per-entry
+// arrays; the level's priority keys (<= 225 of them) reuse the regions of
+// the support and the ranking keys.
 struct PoolLds {
     int m, top, k2, w1, q, tq, wr, xs, ir, tx, bytes;
 };
@@ -88,7 +88,7 @@ __host__ __device__ inline PoolLds pool_lds(int S, int C) {
     PoolLds L;
     const int S2 = S > 256 ? S : 256;
     L.m = 0;
-    L.top = L.m + pad16(8 * C * S);
+    L.top = L.m + pad16(8 * (C + 1) * S);
     L.k2 = L.top + pad16(8 * S2);
     L.w1 = L.k2 + pad16(8 * S2);
     L.q = L.w1 + pad16(4 * S);
@@ -106,8 +106,8 @@ __host__ __device__ inline PoolLds pool_lds(int S, int C) {
 // other blocks (token, score, path) are published with agent-scope atomics.
 template <int NT>
 __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, int row,
-                                          uint8_t* lds, int pu, uint64_t u, uint64_t* s_red,
-                                          int* s_yi) {
+                                          uint8_t* lds, int pu, const ParentRec& pr, uint64_t u,
+                                          uint64_t* s_red, int* s_yi) {
     const PoolLds L = pool_lds(t.S, t.C);
     uint64_t* s_top = (uint64_t*)(lds + L.top);
     uint64_t* s_k2 = (uint64_t*)(lds + L.k2);
@@ -255,7 +255,8 @@ __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, 
             proxy = __ddiv_rn((double)s_w1[item], dS1);
         }
         const double qtrue = (kind == SAMPLED) ? __ddiv_rn((double)s_q[item], (double)Zq) : proxy;
-        emit_child(t, level, nb, pu, cb + j * K + s, s, kind, key_id(s_top[item]), proxy, qtrue);
+        emit_child(t, level, nb, pu, pr, cb + j * K + s, s, kind, key_id(s_top[item]), proxy,
+                   qtrue);
     }
 }
 
@@ -283,12 +284,11 @@ __global__ __launch_bounds__(NTP) void k_pool(TreeDev t, LevelArgs a) {
     const int NE = t.NE;
     const int64_t nb = (int64_t)b * t.NN;
 
-    // the chunk lists, and the parent: frontier node j of the previous level
-    // (the n_expand children with the highest priority, chosen by the
-    // previous launch) with the Philox draw of its sampled slot
-    const uint64_t* src = t.sel + (int64_t)row * C * S;
-    for (int i = tid; i < C * S; i += NTP) s_m[i] = src[i];
-    for (int i = tid; i < S; i += NTP) s_top[i] = 0ull;   // id -1 until merged
+    // the parent: frontier node j of the previous level (the n_expand
+    // children with the highest priority, chosen by the previous launch)
+    // with the Philox draw of its sampled slot; and the chunk lists, with
+    // an empty list after them
+    const int C4 = (C + 3) & ~3;
     if (tid == 0) {
         int pu = (level == 0) ? 0 : t.frontier[(int64_t)b * NE + j];
         const int lo_uid = (level == 0) ? 0 : ((level == 1) ? 1 : 1 + K + (level - 2) * NE * K);
@@ -302,13 +302,21 @@ __global__ __launch_bounds__(NTP) void k_pool(TreeDev t, LevelArgs a) {
                            : t.fr_u[(int64_t)b * NE + j];
         if (pu == 0 && level > 0) s_u = philox_draw(a.rng_key, P_DRAFT, (uint64_t)b, 0ull);
     }
+    const uint64_t* src = t.sel + (int64_t)row * C * S;
+    for (int i = tid; i < C * S; i += NTP) s_m[i] = src[i];
+    for (int i = C * S + tid; i < (C + 1) * S; i += NTP) s_m[i] = 0ull;
+    for (int i = tid; i < S; i += NTP) s_top[i] = 0ull;   // id -1 until merged
     __syncthreads();
+    // the parent record, for the children written at the end
+    const ParentRec pr = (tid < K) ? parent_rec(t, level, nb, s_pu) : ParentRec{1.0, 0ull};
 
     // merge: a key's rank in the row is its position in its own (sorted)
     // list plus the count of larger keys in every other list (a binary
     // search per list).  Every list holds S keys (a chunk is larger than any
     // support); keys are unique and 0 marks an empty slot.  Two keys per
-    // thread and four lists at a time keep eight searches in flight.
+    // thread and four lists at a time (the empty list stands in for lists
+    // past the last), with no branches, keep eight loads in flight per
+    // search step.
     {
         int pw2 = 1;
         while (pw2 * 2 <= S) pw2 *= 2;
@@ -318,24 +326,28 @@ __global__ __launch_bounds__(NTP) void k_pool(TreeDev t, LevelArgs a) {
             const uint64_t kA = s_m[eA], kB = eB < nk ? s_m[eB] : 0ull;
             const int lA = eA / S, lB = eB / S;
             int rA = eA - lA * S, rB = eB - lB * S;
-            for (int c2 = 0; c2 < C; c2 += 4) {
+            for (int c2 = 0; c2 < C4; c2 += 4) {
+                int lb[4];
+#pragma unroll
+                for (int cc = 0; cc < 4; ++cc) lb[cc] = min(c2 + cc, C) * S;
                 int oA[4] = {0, 0, 0, 0}, oB[4] = {0, 0, 0, 0};
                 for (int half = pw2; half > 0; half >>= 1) {
+                    uint64_t xA[4], xB[4];
 #pragma unroll
                     for (int cc = 0; cc < 4; ++cc) {
-                        if (c2 + cc < C) {
-                            const uint64_t* L2 = s_m + (c2 + cc) * S;
-                            const uint64_t xA = L2[min(oA[cc] + half, S) - 1];
-                            const uint64_t xB = L2[min(oB[cc] + half, S) - 1];
-                            oA[cc] += (oA[cc] + half <= S && xA > kA) ? half : 0;
-                            oB[cc] += (oB[cc] + half <= S && xB > kB) ? half : 0;
-                        }
+                        xA[cc] = s_m[lb[cc] + min(oA[cc] + half, S) - 1];
+                        xB[cc] = s_m[lb[cc] + min(oB[cc] + half, S) - 1];
+                    }
+#pragma unroll
+                    for (int cc = 0; cc < 4; ++cc) {
+                        oA[cc] += (oA[cc] + half <= S && xA[cc] > kA) ? half : 0;
+                        oB[cc] += (oB[cc] + half <= S && xB[cc] > kB) ? half : 0;
                     }
                 }
 #pragma unroll
                 for (int cc = 0; cc < 4; ++cc) {
-                    if (c2 + cc < C && c2 + cc != lA) rA += oA[cc];
-                    if (c2 + cc < C && c2 + cc != lB) rB += oB[cc];
+                    rA += (c2 + cc != lA) ? oA[cc] : 0;
+                    rB += (c2 + cc != lB) ? oB[cc] : 0;
                 }
             }
             if (kA != 0ull && rA < S) s_top[rA] = kA;
@@ -351,12 +363,8 @@ __global__ __launch_bounds__(NTP) void k_pool(TreeDev t, LevelArgs a) {
     }
     __syncthreads();
 
-    // the pool: one wave for small supports (no block barriers), else all
-    if (S <= 256) {
-        if (tid < WAVE) pool_form<WAVE>(t, a, row, s_pdyn, s_pu, s_u, s_red, &s_yi);
-    } else {
-        pool_form<NTP>(t, a, row, s_pdyn, s_pu, s_u, s_red, &s_yi);
-    }
+    // the pool, formed by the whole block
+    pool_form<NTP>(t, a, row, s_pdyn, s_pu, pr, s_u, s_red, &s_yi);
     if (level + 1 >= t.D) return;
 
     // the next frontier: the last row of the sequence to finish selects it
@@ -366,108 +374,198 @@ __global__ __launch_bounds__(NTP) void k_pool(TreeDev t, LevelArgs a) {
 // ---------------------------------------------------------------------------
 // k_select: the exact top-Sc of one chunk of one row
 // ---------------------------------------------------------------------------
+// A bf16 chunk holds at most 65536 elements, so its candidates are ranked by
+// 32-bit keys: the 16-bit order code of the value above the complement of
+// the chunk-local index (larger key = larger logit, then smaller id).  fp32
+// chunks use the 64-bit row keys.
+__device__ __forceinline__ uint32_t chunk_key32(float v, int lid) {
+    return (ord32(v) & 0xFFFF0000u) | (uint32_t)(0xFFFF - lid);
+}
+// The row key (logit_key) of a chunk key; e0 = the chunk's first element.
+__device__ __forceinline__ uint64_t row_key_of32(uint32_t k, int e0) {
+    const uint32_t o = (k & 0xFFFF0000u) | ((k & 0x80000000u) ? 0u : 0xFFFFu);
+    const uint32_t id = (uint32_t)(e0 + 0xFFFF - (int)(k & 0xFFFFu));
+    return ((uint64_t)o << 32) | (uint64_t)(0xFFFFFFFFu - id);
+}
+
+// max(a, b, c) of finite fp32 values in one instruction (no NaN quieting:
+// the operands are never NaN).
+__device__ __forceinline__ float max3_finite(float a, float b, float c) {
+    float r;
+    asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+    return r;
+}
+
+// Exact maximum element of a vector of eight bf16 (raw word bits: a packed
+// word read as fp32 is its high element plus a fraction of one bf16 ulp made
+// of the low element's bits, so the maximum over the raw words and the
+// unpacked low elements, with its low 16 bits cleared, is exactly the
+// largest element; logits and padding are finite, so no word is a NaN).
+// Returned with garbage in the low 16 bits.
+__device__ __forceinline__ uint32_t bf16x8_max_raw(const uint4& v) {
+    float m = max3_finite(__uint_as_float(v.x), bf_lo(v.x), __uint_as_float(v.y));
+    m = max3_finite(m, bf_lo(v.y), __uint_as_float(v.z));
+    m = max3_finite(m, bf_lo(v.z), __uint_as_float(v.w));
+    m = max3_finite(m, bf_lo(v.w), bf_lo(v.w));
+    return __float_as_uint(m);
+}
+
+typedef short rs_short2 __attribute__((ext_vector_type(2)));
+typedef unsigned short rs_ushort2 __attribute__((ext_vector_type(2)));
+// Order codes of two packed bf16 values (negative: all bits flipped,
+// otherwise the sign bit set), two lanes of 16 bits at once.
+__device__ __forceinline__ rs_ushort2 bf16x2_codes(uint32_t w) {
+    const rs_short2 s = __builtin_bit_cast(rs_short2, w);
+    const uint32_t m = __builtin_bit_cast(uint32_t, (rs_short2)(s >> (short)15)) | 0x80008000u;
+    return __builtin_bit_cast(rs_ushort2, w ^ m);
+}
+
+template <int NT>
+__device__ void rank_keys32(const uint32_t* keys, int n, int16_t* rank) {
+    int npad = 1;
+    while (npad < n) npad <<= 1;
+    int F = NT / npad;
+    if (F < 1) F = 1;
+    if (F > WAVE) F = WAVE;
+    const int sub = threadIdx.x % F;
+    const int per = NT / F;
+    const uint4* k4 = (const uint4*)keys;
+    const int n4 = n >> 2;
+    for (int base = 0; base < n; base += per) {
+        const int i = base + threadIdx.x / F;
+        int cnt = 0;
+        if (i < n) {
+            const uint32_t k = keys[i];
+#pragma unroll 4
+            for (int g = sub; g < n4; g += F) {
+                const uint4 x = k4[g];
+                cnt += (int)(x.x > k) + (int)(x.y > k) + (int)(x.z > k) + (int)(x.w > k);
+            }
+            for (int j = 4 * n4 + sub; j < n; j += F) cnt += (int)(keys[j] > k);
+        }
+        for (int o = 1; o < F; o <<= 1) cnt += __shfl_xor(cnt, o);
+        if (i < n && sub == 0) rank[i] = (int16_t)cnt;
+    }
+}
+
 template <int DT, int NVC>
 __device__ __forceinline__ void select_block(const TreeDev& t, const LevelArgs& a) {
     constexpr int VEC = DT ? 8 : 4;
-    constexpr int ESZ = DT ? 2 : 4;
     constexpr int NM = DT ? (NVC + 1) / 2 : NVC;   // registers of per-vector maxima
+    constexpr int NW = NTC / WAVE;
+    constexpr int WCAP = CAPV / NW;                // candidate vectors per wave
 
-    __shared__ uint64_t s_keys[CAPC];           // candidates
-    __shared__ uint4 s_cv[CAPV];                 // candidate vectors
+    __shared__ __align__(16) uint64_t s_keys[CAPC];   // candidates (bf16: 32-bit keys)
+    __shared__ uint4 s_cv[CAPV];                 // candidate vectors, WCAP per wave
     __shared__ int16_t s_rank[CAPC];
     __shared__ int s_cvi[CAPV];                  // their vector indices
-    __shared__ uint32_t s_off[2 * NTC];          // threshold offers
-    __shared__ int s_bc[2][NTC / WAVE];
-    __shared__ uint32_t s_h;
-    __shared__ int s_cnt, s_nv;
-    __shared__ int s_redi[NTC / WAVE];
+    __shared__ uint32_t s_hist[2 * NTC];         // threshold histograms
+    __shared__ int s_bc[2][NW];
+    __shared__ int s_wn[NW];
+    __shared__ uint32_t s_h, s_h2;
+    __shared__ int s_above, s_cnt;
+    __shared__ int s_redi[NW];
+    uint32_t* s_k32 = (uint32_t*)s_keys;
 
     const int tid = threadIdx.x;
+    const int lane = tid % WAVE, wid = tid / WAVE;
     const int c = blockIdx.x;
     const int row = blockIdx.y;
     const int V = t.V;
     const int v0 = c * NTC * NVC;                           // first vector of the chunk
     const int nvalid = min(V - v0 * VEC, NTC * NVC * VEC);  // >= 1: C = ceil(V / chunk)
     const int nsel = min(t.Sc, nvalid);
-    const char* base = (const char*)a.logits + (int64_t)row * t.stride * ESZ;
+    const char* base = (const char*)a.logits + (int64_t)row * t.stride * (DT ? 2 : 4);
     uint64_t* out = t.sel + ((int64_t)row * t.C + c) * t.Sc;
 
+    // the chunk, NVC 16-byte vectors per thread; every chunk but a row's
+    // last is whole, so its loads need no bounds checks
     uint4 r[NVC];
+    if ((v0 + NTC * NVC) * VEC <= V) {
+        const uint32_t toff = (uint32_t)tid * 16u;
 #pragma unroll
-    for (int i = 0; i < NVC; ++i) r[i] = load_row_vec<DT>(base, v0 + i * NTC + tid, V);
-    if (tid == 0) {
-        s_cnt = 0;
-        s_nv = 0;
+        for (int i = 0; i < NVC; ++i)
+            r[i] = load_stream16(base + (int64_t)(v0 + i * NTC) * 16 + toff);
+    } else {
+#pragma unroll
+        for (int i = 0; i < NVC; ++i) r[i] = load_row_vec<DT>(base, v0 + i * NTC + tid, V);
     }
+    if (tid == 0) s_cnt = 0;
 
-    // per-vector maxima (exact) and this thread's maximum.  bf16: a packed
-    // word read as fp32 is its high element plus a fraction of one bf16 ulp
-    // (the low element's bits), so the maximum over the raw words and the
-    // unpacked low elements, with its low 16 bits cleared, is exactly the
-    // maximum element (logits and padding are finite, so no word is a NaN)
+    // per-vector maxima (exact; bf16: two per register, high halves) and
+    // every thread's two largest as 16-bit order codes
     uint32_t vm[NM];
+    uint32_t c1 = 0, c2 = 0;
+    if (DT) {
+        rs_ushort2 p1 = {0, 0}, p2 = {0, 0};
 #pragma unroll
-    for (int q = 0; q < NM; ++q) vm[q] = 0;
-    float tmax = -INFINITY;
-#pragma unroll
-    for (int i = 0; i < NVC; ++i) {
-        float mx;
-        if (DT) {
-            const uint32_t* w = &r[i].x;
-            mx = fmaxf(fmaxf(__uint_as_float(w[0]), bf_lo(w[0])), __uint_as_float(w[1]));
-            mx = fmaxf(fmaxf(mx, bf_lo(w[1])), __uint_as_float(w[2]));
-            mx = fmaxf(fmaxf(mx, bf_lo(w[2])), __uint_as_float(w[3]));
-            mx = fmaxf(mx, bf_lo(w[3]));
-            const uint32_t hb = __float_as_uint(mx) & 0xFFFF0000u;
-            mx = __uint_as_float(hb);
-            vm[i / 2] |= (i & 1) ? hb : (hb >> 16);
-        } else {
-            mx = fmaxf(fmaxf(elem<DT>(r[i], 0), elem<DT>(r[i], 1)),
-                       fmaxf(elem<DT>(r[i], 2), elem<DT>(r[i], 3)));
-            vm[i] = __float_as_uint(mx);
+        for (int q = 0; q < NM; ++q) {
+            const uint32_t lo = bf16x8_max_raw(r[2 * q]);
+            const uint32_t hi = (2 * q + 1 < NVC) ? bf16x8_max_raw(r[2 * q + 1]) : lo;
+            vm[q] = __builtin_amdgcn_perm(hi, lo, 0x07060302u);
+            const rs_ushort2 cq = bf16x2_codes(vm[q]);
+            p2 = __builtin_elementwise_max(p2, __builtin_elementwise_min(p1, cq));
+            p1 = __builtin_elementwise_max(p1, cq);
         }
-        tmax = fmaxf(tmax, mx);
+        c1 = max((uint32_t)p1.x, (uint32_t)p1.y);
+        c2 = max(min((uint32_t)p1.x, (uint32_t)p1.y), max((uint32_t)p2.x, (uint32_t)p2.y));
+    } else {
+#pragma unroll
+        for (int i = 0; i < NVC; ++i) {
+            const float mx = fmaxf(fmaxf(elem<DT>(r[i], 0), elem<DT>(r[i], 1)),
+                                   fmaxf(elem<DT>(r[i], 2), elem<DT>(r[i], 3)));
+            vm[i] = __float_as_uint(mx);
+            const uint32_t cv = ord32(mx) >> 16;
+            c2 = max(c2, min(c1, cv));
+            c1 = max(c1, cv);
+        }
     }
 
     // threshold tau: at least nsel elements of the chunk are >= tau.  Every
-    // thread offers the 16-bit order-preserving codes of its two largest
-    // vector maxima; the largest code h that nsel offered codes reach gives
-    // tau = the smallest value with code h (each offered maximum is a
-    // distinct vector holding an element >= tau).  One wave finds h by
-    // bisection over the 2 * NTC offers.  Vectors past the row end read as
-    // -inf, so tau may fall to -inf: then every element of the chunk is a
-    // candidate.  Supports larger than the offers use all vector maxima.
-    const int lane = tid % WAVE, wid = tid / WAVE;
-    uint32_t c1 = 0, c2 = 0;
-#pragma unroll
-    for (int i = 0; i < NVC; ++i) {
-        const float v = DT ? ((i & 1) ? bf_hi(vm[i / 2]) : bf_lo(vm[i / 2]))
-                           : __uint_as_float(vm[i]);
-        const uint32_t cv = ord32(v) >> 16;
-        c2 = max(c2, min(c1, cv));
-        c1 = max(c1, cv);
-    }
+    // thread offers the order codes of its two largest vector maxima; h =
+    // the nsel-th largest offered code gives tau = the smallest value with
+    // code h (each offered maximum is a distinct vector holding an element
+    // >= tau).  h comes from two 8-bit histogram passes over the 2 * NTC
+    // offers (high byte, then low byte inside the bin that holds the nsel-th
+    // offer), one bin per thread.  Elements past the row end read as -inf
+    // (fp32) or the lowest finite bf16, so tau may fall to that value: then
+    // every element of the chunk is a candidate.  Supports larger than the
+    // offers use all vector maxima.
+    static_assert(NTC == 256, "one histogram bin per thread");
     uint32_t h = 0;
     if (nsel <= 2 * NTC) {
-        s_off[tid] = c1;
-        s_off[NTC + tid] = c2;
+        s_hist[tid] = 0u;
+        s_hist[NTC + tid] = 0u;
         __syncthreads();
-        if (wid == 0) {
-            uint32_t o[2 * NTC / WAVE];
+        atomicAdd(&s_hist[c1 >> 8], 1u);
+        atomicAdd(&s_hist[c2 >> 8], 1u);
+        __syncthreads();
+        // thread tid holds bin NTC-1-tid: inclusive prefix = offers in bins >= it
+        int n = (int)s_hist[NTC - 1 - tid];
+        int incl = wave_excl_scan(n) + n;
+        if (lane == WAVE - 1) s_bc[0][wid] = incl;
+        __syncthreads();
 #pragma unroll
-            for (int q = 0; q < 2 * NTC / WAVE; ++q) o[q] = s_off[q * WAVE + lane];
-#pragma unroll 1
-            for (int bit = 15; bit >= 0; --bit) {
-                const uint32_t cand = h | (1u << bit);
-                int n = 0;
-#pragma unroll
-                for (int q = 0; q < 2 * NTC / WAVE; ++q) n += __popcll(__ballot(o[q] >= cand));
-                if (n >= nsel) h = cand;
-            }
-            if (lane == 0) s_h = h;
+        for (int w = 0; w < NW; ++w) incl += (w < wid) ? s_bc[0][w] : 0;
+        if (incl >= nsel && incl - n < nsel) {
+            s_h = (uint32_t)(NTC - 1 - tid);
+            s_above = incl - n;
         }
         __syncthreads();
-        h = s_h;
+        const uint32_t hb = s_h;
+        if ((c1 >> 8) == hb) atomicAdd(&s_hist[NTC + (c1 & 0xFFu)], 1u);
+        if ((c2 >> 8) == hb) atomicAdd(&s_hist[NTC + (c2 & 0xFFu)], 1u);
+        __syncthreads();
+        n = (int)s_hist[2 * NTC - 1 - tid];
+        incl = wave_excl_scan(n) + n;
+        if (lane == WAVE - 1) s_bc[1][wid] = incl;
+        __syncthreads();
+        incl += s_above;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) incl += (w < wid) ? s_bc[1][w] : 0;
+        if (incl >= nsel && incl - n < nsel) s_h2 = (hb << 8) | (uint32_t)(NTC - 1 - tid);
+        __syncthreads();
+        h = s_h2;
     } else {
 #pragma unroll 1
         for (int bit = 15; bit >= 0; --bit) {
@@ -484,66 +582,104 @@ __device__ __forceinline__ void select_block(const TreeDev& t, const LevelArgs& 
             __syncthreads();
             int tot = 0;
 #pragma unroll
-            for (int w = 0; w < NTC / WAVE; ++w) tot += s_bc[bit & 1][w];
+            for (int w = 0; w < NW; ++w) tot += s_bc[bit & 1][w];
             if (tot >= nsel) h = cand;
         }
     }
     const float tau = (h << 16) > ord32(-INFINITY) ? unord32(h << 16) : -INFINITY;
 
     // candidates >= tau in two compactions, so the per-element work touches
-    // only the few vectors whose maximum reaches tau: (1) every wave counts
-    // its candidate vectors with ballots, reserves LDS slots with one atomic
-    // and copies them there; (2) each thread scans whole candidate vectors
-    // and appends their elements >= tau the same way.
-    int wn = 0;
+    // only the few vectors whose maximum reaches tau: (1) every wave appends
+    // its candidate vectors to its own LDS region (ballot and bit count);
+    // (2) the threads take the candidate vectors of all regions in turn and
+    // append their elements >= tau to the candidate list.  If a wave has more
+    // candidate vectors than its region holds, but all fit, they are written
+    // again into one list with slots reserved per wave; more than that sends
+    // the chunk to the exact fallback below.
+    {
+        int wpos = 0;
 #pragma unroll
-    for (int i = 0; i < NVC; ++i) {
-        const float vmax = DT ? ((i & 1) ? bf_hi(vm[i / 2]) : bf_lo(vm[i / 2]))
-                              : __uint_as_float(vm[i]);
-        wn += __popcll(__ballot(vmax >= tau));
+        for (int i = 0; i < NVC; ++i) {
+            const float vmax = DT ? ((i & 1) ? bf_hi(vm[i / 2]) : bf_lo(vm[i / 2]))
+                                  : __uint_as_float(vm[i]);
+            const bool take = vmax >= tau;
+            const uint64_t msk = __ballot(take);
+            if (take) {
+                const int pos = wpos + (int)__builtin_amdgcn_mbcnt_hi(
+                    (uint32_t)(msk >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)msk, 0u));
+                if (pos < WCAP) {
+                    s_cv[wid * WCAP + pos] = r[i];
+                    s_cvi[wid * WCAP + pos] = v0 + i * NTC + tid;
+                }
+            }
+            wpos += __popcll(msk);
+        }
+        if (lane == 0) s_wn[wid] = wpos;
     }
-    int wbase = 0;
-    if (lane == 0) wbase = atomicAdd(&s_nv, wn);
-    wbase = (int)lane_u32((uint32_t)wbase, 0);
+    __syncthreads();
+    int wn[NW], nv = 0, wbefore = 0;
+    bool ovf = false;
 #pragma unroll
-    for (int i = 0; i < NVC; ++i) {
-        const float vmax = DT ? ((i & 1) ? bf_hi(vm[i / 2]) : bf_lo(vm[i / 2]))
-                              : __uint_as_float(vm[i]);
-        const bool take = vmax >= tau;
-        const uint64_t msk = __ballot(take);
-        if (take) {
-            const int pos = wbase + (int)__builtin_amdgcn_mbcnt_hi(
-                (uint32_t)(msk >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)msk, 0u));
-            if (pos < CAPV) {
+    for (int w = 0; w < NW; ++w) {
+        wn[w] = s_wn[w];
+        ovf |= wn[w] > WCAP;
+        wbefore += (w < wid) ? wn[w] : 0;
+        nv += wn[w];
+    }
+    const bool contig = ovf && nv <= CAPV;
+    if (contig) {
+        // one list: each wave's vectors after those of the waves before it
+        int wpos = wbefore;
+#pragma unroll
+        for (int i = 0; i < NVC; ++i) {
+            const float vmax = DT ? ((i & 1) ? bf_hi(vm[i / 2]) : bf_lo(vm[i / 2]))
+                                  : __uint_as_float(vm[i]);
+            const bool take = vmax >= tau;
+            const uint64_t msk = __ballot(take);
+            if (take) {
+                const int pos = wpos + (int)__builtin_amdgcn_mbcnt_hi(
+                    (uint32_t)(msk >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)msk, 0u));
                 s_cv[pos] = r[i];
                 s_cvi[pos] = v0 + i * NTC + tid;
             }
+            wpos += __popcll(msk);
         }
-        wbase += __popcll(msk);
+        __syncthreads();
     }
-    __syncthreads();
-    const int nv = s_nv;
-    if (nv <= CAPV) {
+    if (!ovf || contig) {
         for (int j0 = 0; j0 < nv; j0 += NTC) {
             const int j = j0 + tid;
+            // entry j of the concatenated regions (or of the one list)
+            int w = 0, off = j;
+            if (!contig) {
+#pragma unroll
+                for (int q = 0; q < NW - 1; ++q) {
+                    const bool past = off >= wn[q] && w == q;
+                    off -= past ? wn[q] : 0;
+                    w += past ? 1 : 0;
+                }
+            }
             uint4 x = make_uint4(0, 0, 0, 0);
             int e0 = V;
             if (j < nv) {
-                x = s_cv[j];
-                e0 = s_cvi[j] * VEC;
+                x = s_cv[w * WCAP + off];
+                e0 = s_cvi[w * WCAP + off] * VEC;
             }
             int n = 0;
 #pragma unroll
             for (int k = 0; k < VEC; ++k) n += (elem<DT>(x, k) >= tau) & (e0 + k < V);
             const int excl = wave_excl_scan(n);
-            int base = 0;
-            if (lane == WAVE - 1) base = atomicAdd(&s_cnt, excl + n);
-            int pos = (int)lane_u32((uint32_t)base, WAVE - 1) + excl;
+            int cbase = 0;
+            if (lane == WAVE - 1) cbase = atomicAdd(&s_cnt, excl + n);
+            int pos = (int)lane_u32((uint32_t)cbase, WAVE - 1) + excl;
 #pragma unroll
             for (int k = 0; k < VEC; ++k) {
                 const float v = elem<DT>(x, k);
                 if (v >= tau && e0 + k < V) {
-                    if (pos < CAPC) s_keys[pos] = logit_key(v, (uint32_t)(e0 + k));
+                    if (pos < CAPC) {
+                        if (DT) s_k32[pos] = chunk_key32(v, e0 + k - v0 * VEC);
+                        else s_keys[pos] = logit_key(v, (uint32_t)(e0 + k));
+                    }
                     ++pos;
                 }
             }
@@ -555,45 +691,154 @@ __device__ __forceinline__ void select_block(const TreeDev& t, const LevelArgs& 
     int cnt = s_cnt;
 
     if (cnt > CAPC) {
-        // Degenerate chunk (massive ties at the threshold): the nsel-th
-        // largest selection key, exactly, by bisection on the 64-bit key.
-        // Rare, so it re-reads the chunk from memory rather than holding more
-        // registers.
-        const int e_end = min(V, (v0 + NTC * NVC) * VEC);
-        uint64_t x = 0;
-        for (int bit = 63; bit >= 0; --bit) {
-            const uint64_t cand = x | (1ull << bit);
-            int n = 0;
-#pragma unroll 1
-            for (int i = 0; i < NVC; ++i) {
-                const int vi = v0 + i * NTC + tid;
-                if (vi * VEC >= e_end) continue;
-                const uint4 w = load_row_vec<DT>(base, vi, V);
-#pragma unroll
-                for (int k = 0; k < VEC; ++k) {
-                    const int id = vi * VEC + k;
-                    n += (id < V) && (logit_key(elem<DT>(w, k), (uint32_t)id) >= cand);
-                }
+        // Degenerate chunk: more candidates than LDS holds (massive ties at
+        // the threshold, or large values crowded into few threads).  Exact;
+        // rare, so it re-reads the chunk, four vectors at a time, rather than
+        // keeping it in registers.  bf16: count the elements whose code lies
+        // above the threshold code h; if the nsel-th largest element has code
+        // h, take everything above h and the smallest ids among those at h
+        // (ranks of the ties in id order from per-wave counts and wave
+        // scans); if it lies above h and the elements above h fit, take
+        // those.  Otherwise, and for fp32, find the nsel-th largest key by
+        // bisection.
+        const int eb = v0 * VEC;                 // first element of the chunk
+        auto push = [&](float v, int l) {
+            const int pos = atomicAdd(&s_cnt, 1);
+            if (pos < CAPC) {
+                if (DT) s_k32[pos] = chunk_key32(v, l);
+                else s_keys[pos] = logit_key(v, (uint32_t)(eb + l));
             }
-            n = block_sum_i32<NTC>(n, s_redi);
-            if (n >= nsel) x = cand;
-        }
+        };
         __syncthreads();
         if (tid == 0) s_cnt = 0;
-        __syncthreads();
+        bool done = false;
+        if (DT) {
+            int ngt = 0;
 #pragma unroll 1
-        for (int i = 0; i < NVC; ++i) {
-            const int vi = v0 + i * NTC + tid;
-            if (vi * VEC >= e_end) continue;
-            const uint4 w = load_row_vec<DT>(base, vi, V);
+            for (int i0 = 0; i0 < NVC; i0 += 4) {
+                uint4 w[4];
 #pragma unroll
-            for (int k = 0; k < VEC; ++k) {
-                const int id = vi * VEC + k;
-                if (id < V) {
-                    const uint64_t key = logit_key(elem<DT>(w, k), (uint32_t)id);
-                    if (key >= x) {
-                        const int pos = atomicAdd(&s_cnt, 1);
-                        if (pos < CAPC) s_keys[pos] = key;
+                for (int q = 0; q < 4; ++q) w[q] = load_row_vec<DT>(base, v0 + (i0 + q) * NTC + tid, V);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int l0 = ((i0 + q) * NTC + tid) * VEC;
+#pragma unroll
+                    for (int k = 0; k < VEC; ++k)
+                        ngt += (eb + l0 + k < V && (ord32(elem<DT>(w[q], k)) >> 16) > h) ? 1 : 0;
+                }
+            }
+            ngt = block_sum_i32<NTC>(ngt, s_redi);
+            if (ngt < nsel) {
+                // ties at h, in id order: vector i, then thread, then element
+                __shared__ int s_tie[32][NW];            // ties per (vector, wave)
+                const int need = nsel - ngt;
+#pragma unroll 1
+                for (int i0 = 0; i0 < NVC; i0 += 4) {
+                    uint4 w[4];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) w[q] = load_row_vec<DT>(base, v0 + (i0 + q) * NTC + tid, V);
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const int l0 = ((i0 + q) * NTC + tid) * VEC;
+                        int nt = 0;
+#pragma unroll
+                        for (int k = 0; k < VEC; ++k)
+                            nt += (eb + l0 + k < V && (ord32(elem<DT>(w[q], k)) >> 16) == h) ? 1 : 0;
+                        const int tot = wave_sum_i32(nt);
+                        if (lane == 0) s_tie[i0 + q][wid] = tot;
+                    }
+                }
+                __syncthreads();
+                int prior = 0;                   // ties in the vectors before i, all threads
+#pragma unroll 1
+                for (int i0 = 0; i0 < NVC; i0 += 4) {
+                    uint4 w[4];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) w[q] = load_row_vec<DT>(base, v0 + (i0 + q) * NTC + tid, V);
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const int i = i0 + q;
+                        const int l0 = (i * NTC + tid) * VEC;
+                        int nt = 0;
+#pragma unroll
+                        for (int k = 0; k < VEC; ++k)
+                            nt += (eb + l0 + k < V && (ord32(elem<DT>(w[q], k)) >> 16) == h) ? 1 : 0;
+                        int rk = prior + wave_excl_scan(nt);
+#pragma unroll
+                        for (int ww = 0; ww < NW; ++ww) {
+                            rk += (ww < wid) ? s_tie[i][ww] : 0;
+                            prior += s_tie[i][ww];
+                        }
+#pragma unroll
+                        for (int k = 0; k < VEC; ++k) {
+                            const float v = elem<DT>(w[q], k);
+                            const uint32_t cd = ord32(v) >> 16;
+                            if (eb + l0 + k < V) {
+                                if (cd > h) {
+                                    push(v, l0 + k);
+                                } else if (cd == h) {
+                                    if (rk < need) push(v, l0 + k);
+                                    ++rk;
+                                }
+                            }
+                        }
+                    }
+                }
+                done = true;
+            } else if (ngt <= CAPC) {
+#pragma unroll 1
+                for (int i0 = 0; i0 < NVC; i0 += 4) {
+                    uint4 w[4];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) w[q] = load_row_vec<DT>(base, v0 + (i0 + q) * NTC + tid, V);
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const int l0 = ((i0 + q) * NTC + tid) * VEC;
+#pragma unroll
+                        for (int k = 0; k < VEC; ++k) {
+                            const float v = elem<DT>(w[q], k);
+                            if (eb + l0 + k < V && (ord32(v) >> 16) > h) push(v, l0 + k);
+                        }
+                    }
+                }
+                done = true;
+            }
+        }
+        if (!done) {
+            uint64_t x = 0;
+#pragma unroll 1
+            for (int bit = 63; bit >= 0; --bit) {
+                const uint64_t cand = x | (1ull << bit);
+                int n = 0;
+#pragma unroll 1
+                for (int i0 = 0; i0 < NVC; i0 += 4) {
+                    uint4 w[4];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) w[q] = load_row_vec<DT>(base, v0 + (i0 + q) * NTC + tid, V);
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const int l0 = ((i0 + q) * NTC + tid) * VEC;
+#pragma unroll
+                        for (int k = 0; k < VEC; ++k)
+                            n += (eb + l0 + k < V &&
+                                  logit_key(elem<DT>(w[q], k), (uint32_t)(eb + l0 + k)) >= cand) ? 1 : 0;
+                    }
+                }
+                n = block_sum_i32<NTC>(n, s_redi);
+                if (n >= nsel) x = cand;
+            }
+#pragma unroll 1
+            for (int i0 = 0; i0 < NVC; i0 += 4) {
+                uint4 w[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) w[q] = load_row_vec<DT>(base, v0 + (i0 + q) * NTC + tid, V);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int l0 = ((i0 + q) * NTC + tid) * VEC;
+#pragma unroll
+                    for (int k = 0; k < VEC; ++k) {
+                        const float v = elem<DT>(w[q], k);
+                        if (eb + l0 + k < V && logit_key(v, (uint32_t)(eb + l0 + k)) >= x) push(v, l0 + k);
                     }
                 }
             }
@@ -604,14 +849,14 @@ __device__ __forceinline__ void select_block(const TreeDev& t, const LevelArgs& 
 
     // exact top-nsel of the candidates, written sorted; unused slots are 0
     // (below every real key)
-    rank_keys<NTC>(s_keys, cnt, s_rank);
+    if (DT) rank_keys32<NTC>(s_k32, cnt, s_rank);
+    else rank_keys<NTC>(s_keys, cnt, s_rank);
     __syncthreads();
     for (int i = tid; i < cnt; i += NTC) {
         const int rk = s_rank[i];
-        if (rk < nsel) out[rk] = s_keys[i];
+        if (rk < nsel) out[rk] = DT ? row_key_of32(s_k32[i], v0 * VEC) : s_keys[i];
     }
     for (int i = nsel + tid; i < t.Sc; i += NTC) out[i] = 0ull;
-
 }
 
 // Four blocks per CU keep enough loads in flight; the largest chunk variant

@@ -35,16 +35,39 @@ __device__ __forceinline__ void count_greater2(const uint64_t* keys, int n, uint
     c0 = a0;
     c1 = a1;
 }
-// Ranks (counts of larger keys) of keys[i] for i = tid, tid + NT, ...
+// Ranks (counts of larger keys) of the n unique keys in LDS (16-byte
+// aligned) by NT threads.  When the threads outnumber the keys, F adjacent
+// lanes share a key (F a power of two, F * n <= NT, F <= 16), each counting
+// over every F-th pair of keys, and their counts are added across the
+// lanes; otherwise every thread ranks two keys at a time.
 template <int NT>
 __device__ __forceinline__ void rank_all(const uint64_t* keys, int n, int16_t* rank) {
-    for (int i = threadIdx.x % NT; i < n; i += 2 * NT) {
-        const int i2 = i + NT;
-        int c0, c1;
-        count_greater2(keys, n, keys[i], i2 < n ? keys[i2] : ~0ull, c0, c1);
-        rank[i] = (int16_t)c0;
-        if (i2 < n) rank[i2] = (int16_t)c1;
+    const int t = threadIdx.x % NT;
+    int F = 1;
+    while (F < 16 && 2 * F * n <= NT) F *= 2;
+    if (F == 1) {
+        for (int i = t; i < n; i += 2 * NT) {
+            const int i2 = i + NT;
+            int c0, c1;
+            count_greater2(keys, n, keys[i], i2 < n ? keys[i2] : ~0ull, c0, c1);
+            rank[i] = (int16_t)c0;
+            if (i2 < n) rank[i2] = (int16_t)c1;
+        }
+        return;
     }
+    const ulonglong2* kp = (const ulonglong2*)keys;
+    const int i = t / F, sub = t % F;
+    const uint64_t k = keys[i < n ? i : 0];
+    const int np = n >> 1;
+    int c = 0;
+#pragma unroll 4
+    for (int j = sub; j < np; j += F) {
+        const ulonglong2 x = kp[j];
+        c += (int)(x.x > k) + (int)(x.y > k);
+    }
+    if ((n & 1) && sub == 0) c += (int)(keys[n - 1] > k);
+    for (int o = 1; o < F; o <<= 1) c += __shfl_xor(c, o);
+    if (i < n && sub == 0) rank[i] = (int16_t)c;
 }
 
 // Synchronisation and sums over the NT threads that form a pool: one wave
@@ -65,18 +88,29 @@ __device__ __forceinline__ bool pany(bool p) {
     return __syncthreads_or(p) != 0;
 }
 
+// The parent's path score and slot path (1 and 0 for the root), read early
+// by the threads that later write the children.
+struct ParentRec {
+    double score;
+    uint64_t path;
+};
+__device__ __forceinline__ ParentRec parent_rec(const TreeDev& t, int level, int64_t nb, int pu) {
+    ParentRec p{1.0, 0ull};
+    if (level > 0) {
+        p.score = t.score[nb + pu];
+        p.path = t.path[nb + pu];
+    }
+    return p;
+}
+
 // One child record of expanded row j (slot s, 0-based; App. C.1): the
 // fields the frontier selection reads in other blocks (token, score, path)
 // are published with agent-scope atomics.
 __device__ __forceinline__ void emit_child(const TreeDev& t, int level, int64_t nb, int pu,
-                                           int uid, int s, int kind, int tok, double proxy,
-                                           double qtrue) {
-    double pscore = 1.0;
-    uint64_t ppath = 0;
-    if (level > 0) {
-        pscore = t.score[nb + pu];
-        ppath = t.path[nb + pu];
-    }
+                                           const ParentRec& pr, int uid, int s, int kind,
+                                           int tok, double proxy, double qtrue) {
+    const double pscore = pr.score;
+    const uint64_t ppath = pr.path;
     const int64_t o = nb + uid;
     t.par[o] = pu;
     t.meta[o] = (level + 1) | ((s + 1) << 8) | (kind << 16);
