@@ -137,7 +137,7 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
     d.eps = c.eps_m0;
     d.NN = 1 + c.pool + (c.depth - 1) * c.n_expand * c.pool;
     d.E = 1 + (c.depth - 1) * c.n_expand;
-    if ((16 + 2) * (size_t)(d.NN - 1) > 64 * 1024) {
+    if (16 * (size_t)(d.NN - 1) > 64 * 1024) {
         delete t;
         return fail(RHEO_EINVAL, "tree too large (%d nodes per sequence)", d.NN);
     }

@@ -1,18 +1,12 @@
-// Device helpers shared by the sparse and dense pool kernels: wave-level
-// synchronisation, ranking by counting, sums over the threads forming a
-// pool, a child record, and the frontier selection of a sequence.
+// Device helpers shared by the sparse and dense pool kernels: ranking by
+// counting, sums over the threads forming a pool, a child record, and the
+// frontier selection of a sequence.
 #pragma once
 
 #include "rheo_device.h"
 #include "rheo_state.h"
 
 namespace rheo {
-
-// Orders LDS accesses of the lanes of one wave (no block barrier).
-__device__ __forceinline__ void wave_sync() {
-    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-}
 
 // Ranks of two keys at once (counts of larger keys among n unique keys in
 // LDS, 16-byte aligned); 16 keys per step keep eight loads in flight.

@@ -4,114 +4,75 @@
 // sibling order.  Scores never grow along a path (Lemma 2) and the tie-break
 // ranks a parent before its children, so the kept set is ancestor-closed.
 //
-// One block per sequence orders all nodes by their 128-bit priority key
-// (keys are unique): a bitonic sort in LDS, or, for trees too large for it,
-// a counting rank (each node's rank is the number of larger keys).
+// PSPLIT blocks per sequence each load all of its nodes' 128-bit priority
+// keys (unique) into LDS and rank their share of the nodes by counting the
+// larger keys, several lanes per node.  Every block also checks, for its
+// nodes, that a parent's key is larger than its child's: that is what makes
+// the kept set ancestor-closed, checked without waiting for other blocks.
 #include "rheo_device.h"
 #include "rheo_state.h"
 
 namespace rheo {
 
 constexpr int NTR = 256;
-constexpr int SORT_MAX = 2048;   // nodes the bitonic sort holds in LDS
-
-__device__ __forceinline__ bool key_gt(const ulonglong2& a, const ulonglong2& b) {
-    return a.x > b.x || (a.x == b.x && a.y > b.y);
-}
+constexpr int PSPLIT = 4;          // blocks per sequence
 
 __global__ __launch_bounds__(NTR) void k_prune(TreeDev t, int R) {
-    extern __shared__ ulonglong2 s_dyn[];
-    const int b = blockIdx.x;
+    extern __shared__ ulonglong2 s_key[];    // the sequence's n keys
+    const int b = blockIdx.x / PSPLIT, part = blockIdx.x % PSPLIT;
     const int tid = threadIdx.x;
     const int n = t.NN - 1;               // non-root nodes, uids 1..NN-1
     const int64_t nb = (int64_t)b * t.NN;
-    if (tid == 0) {
+    if (part == 0 && tid == 0) {
         t.pidx[nb] = 0;
         t.porder[nb] = 0;
     }
-    if (n <= SORT_MAX) {
-        int N = 1;
-        while (N < n) N <<= 1;
-        ulonglong2* s_key = s_dyn;
-        uint16_t* s_idx = (uint16_t*)(s_dyn + N);
-        for (int i = tid; i < N; i += NTR) {
-            if (i < n) {
-                const int64_t o = nb + 1 + i;
-                uint64_t hi, lo;
-                prio_key(t.score[o], t.meta[o] & 0xFF, t.path[o], hi, lo);
-                s_key[i] = make_ulonglong2(hi, lo);
-            } else {
-                s_key[i] = make_ulonglong2(0ull, 0ull);   // below every node
-            }
-            s_idx[i] = (uint16_t)i;
-        }
-        __syncthreads();
-        // descending bitonic sort of N keys (N / 2 compare-exchanges a stage)
-        for (int k = 2; k <= N; k <<= 1) {
-            for (int j = k >> 1; j > 0; j >>= 1) {
-                for (int p = tid; p < N / 2; p += NTR) {
-                    const int i = 2 * p - (p & (j - 1));      // lower index of the pair
-                    const int l = i + j;
-                    const bool desc = (i & k) == 0;
-                    const ulonglong2 x = s_key[i], y = s_key[l];
-                    if (key_gt(y, x) == desc) {
-                        s_key[i] = y;
-                        s_key[l] = x;
-                        const uint16_t ti = s_idx[i];
-                        s_idx[i] = s_idx[l];
-                        s_idx[l] = ti;
-                    }
-                }
-                __syncthreads();
-            }
-        }
-        for (int r = tid; r < n; r += NTR) {
-            const int i = s_idx[r];
-            if (r < R) {
-                t.pidx[nb + 1 + i] = r + 1;
-                t.porder[nb + r + 1] = 1 + i;
-            } else {
-                t.pidx[nb + 1 + i] = -1;
-            }
-        }
-    } else {
-        ulonglong2* s_key = s_dyn;
-        int16_t* s_rank = (int16_t*)(s_dyn + n);
-        for (int i = tid; i < n; i += NTR) {
-            const int64_t o = nb + 1 + i;
-            uint64_t hi, lo;
-            prio_key(t.score[o], t.meta[o] & 0xFF, t.path[o], hi, lo);
-            s_key[i] = make_ulonglong2(hi, lo);
-        }
-        __syncthreads();
-        rank_keys128<NTR>(s_key, n, s_rank);
-        __syncthreads();
-        for (int i = tid; i < n; i += NTR) {
-            const int rk = s_rank[i];
-            if (rk < R) {
-                t.pidx[nb + 1 + i] = rk + 1;
-                t.porder[nb + rk + 1] = 1 + i;
-            } else {
-                t.pidx[nb + 1 + i] = -1;
-            }
-        }
-    }
-    __syncthreads();
-    // ancestor closure (a violated invariant raises the sticky error flag)
     for (int i = tid; i < n; i += NTR) {
         const int64_t o = nb + 1 + i;
-        if (t.pidx[o] > 0 && t.pidx[nb + t.par[o]] < 0) atomicOr(t.err, 2);
+        uint64_t hi, lo;
+        prio_key(t.score[o], t.meta[o] & 0xFF, t.path[o], hi, lo);
+        s_key[i] = make_ulonglong2(hi, lo);
+    }
+    __syncthreads();
+    // this block's nodes [i0, i1), F lanes per node, each over every F-th key
+    const int per = (n + PSPLIT - 1) / PSPLIT;
+    const int i0 = min(n, part * per), i1 = min(n, i0 + per);
+    const int m = i1 - i0;
+    int F = 1;
+    while (F < 16 && 2 * F * m <= NTR) F *= 2;
+    const int sub = tid % F;
+    for (int base = 0; base < m; base += NTR / F) {
+        const int i = i0 + base + tid / F;
+        int cnt = 0;
+        ulonglong2 k = make_ulonglong2(~0ull, ~0ull);
+        if (i < i1) k = s_key[i];
+#pragma unroll 8
+        for (int j = sub; j < n; j += F) {
+            const ulonglong2 x = s_key[j];
+            cnt += (int)(x.x > k.x) | ((int)(x.x == k.x) & (int)(x.y > k.y));
+        }
+        for (int o = 1; o < F; o <<= 1) cnt += __shfl_xor(cnt, o);
+        if (i < i1 && sub == 0) {
+            const int64_t o = nb + 1 + i;
+            if (cnt < R) {
+                t.pidx[o] = cnt + 1;
+                t.porder[nb + cnt + 1] = 1 + i;
+            } else {
+                t.pidx[o] = -1;
+            }
+            // a parent outranks its child (raises the sticky error flag if not)
+            const int p = t.par[o];
+            if (p > 0) {
+                const ulonglong2 pk = s_key[p - 1];
+                if (!(pk.x > k.x || (pk.x == k.x && pk.y > k.y))) atomicOr(t.err, 2);
+            }
+        }
     }
 }
 
 hipError_t launch_prune(const TreeDev& t, int R, hipStream_t s) {
     const int n = t.NN - 1;
-    int N = 1;
-    while (N < n) N <<= 1;
-    const size_t shm = n <= SORT_MAX
-        ? (sizeof(ulonglong2) + sizeof(uint16_t)) * (size_t)N + 16
-        : (sizeof(ulonglong2) + sizeof(int16_t)) * (size_t)n + 16;
-    k_prune<<<t.B, NTR, shm, s>>>(t, R);
+    k_prune<<<t.B * PSPLIT, NTR, sizeof(ulonglong2) * (size_t)n, s>>>(t, R);
     return hipGetLastError();
 }
 

@@ -45,12 +45,13 @@ __device__ inline uint64_t philox_draw(uint64_t key, uint64_t purpose,
 // weight 0 below t = -31.  2^t = 2^n * P(f), n = rint(t), f = t - n, P the
 // degree-6 Taylor polynomial of 2^f with coefficients (ln 2)^k / k! * 2^30
 // rounded to fp32, evaluated in Horner form with separately rounded
-// products and sums.  Result: (uint32)(2^30 P) >> -n.
+// products and sums.  Result: floor(2^30 P 2^n) = (uint32)(2^30 P) >> -n,
+// taken as the truncating conversion of the exact product 2^30 P * 2^n
+// (a scaling by a power of two, exact; below t = -31 it is < 1, so 0).
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ uint32_t cweight(float l, float ref, float kT) {
     float t = __fmul_rn(__fsub_rn(l, ref), kT);
-    t = fminf(t, 0.0f);
-    if (t < -31.0f) return 0u;
+    t = fmaxf(fminf(t, 0.0f), -64.0f);
     const float n = rintf(t);
     const float f = __fsub_rn(t, n);
     float p = 0x1.430912p+17f;
@@ -60,8 +61,7 @@ __device__ __forceinline__ uint32_t cweight(float l, float ref, float kT) {
     p = __fadd_rn(__fmul_rn(p, f), 0x1.ebfbe0p+27f);
     p = __fadd_rn(__fmul_rn(p, f), 0x1.62e430p+29f);
     p = __fadd_rn(__fmul_rn(p, f), 0x1.000000p+30f);
-    const uint32_t u = (uint32_t)p;
-    return u >> (uint32_t)(-(int)n);
+    return (uint32_t)__builtin_amdgcn_ldexpf(p, (int)n);
 }
 
 // Order-preserving map of an fp32 value to uint32 (-0 folded onto +0).
@@ -130,6 +130,11 @@ __device__ __forceinline__ uint64_t row_ror64(uint64_t v) {
 template <int N>
 __device__ __forceinline__ uint64_t row_shr64(uint64_t v) {
     return ((uint64_t)row_shr<N>((uint32_t)(v >> 32)) << 32) | row_shr<N>((uint32_t)v);
+}
+// Orders LDS accesses of the lanes of one wave (no block barrier).
+__device__ __forceinline__ void wave_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
 }
 __device__ __forceinline__ uint32_t lane_u32(uint32_t v, int l) {
     return (uint32_t)__builtin_amdgcn_readlane((int)v, l);

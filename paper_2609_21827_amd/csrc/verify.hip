@@ -187,6 +187,7 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
     constexpr int VEC = DT ? 8 : 4;
     constexpr int ESZ = DT ? 2 : 4;
     constexpr int CH = WAVE * VEC;           // tokens per chunk
+    constexpr int JREG = 4;                  // chunks per wave held in registers
     const int SEGCH = a.NV;                  // chunks per segment
 
     __shared__ uint64_t s_chunk[NCMAX];
@@ -198,9 +199,14 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
     __shared__ uint64_t s_red[NWV];
     __shared__ float s_redf[NWV];
     __shared__ int s_c_uid[16], s_c_tok[16], s_c_slot[16], s_c_tail[16], s_c_zero[16];
+    __shared__ int s_c_pidx[16], s_c_fc[16], s_c_e[16];   // candidates' pruned index, first
+                                                           // child and expanded index
     __shared__ uint32_t s_c_q[16];               // dense: q~ weights of the candidates
     __shared__ int s_lead[16];                   // dense: the node's leads
     __shared__ int s_nc, s_spos, s_mode, s_next, s_token, s_cstar;
+    __shared__ int s_cur, s_curp, s_fc, s_e;     // the node this layer verifies
+    __shared__ int s_resid;                      // the sampled child was rejected
+    __shared__ uint64_t s_Sp;
     __shared__ uint64_t s_U[16], s_Ufin;         // the layer's uniforms
     __shared__ u128 s_F, s_Zrem, s_tt;
     __shared__ float s_M;
@@ -237,20 +243,57 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
     };
     const int c0 = g * SEGCH;                 // first chunk of this segment
     const int c1 = min(NC, c0 + SEGCH);
+    const int lo_tok = c0 * CH, hi_tok = min(V, c1 * CH);
 
-    int cur = 0, level = 0, nacc = 0;
+    // the root: pruned index 0; its first child and expanded index
+    if (tid == 0) {
+        s_cur = 0;
+        s_curp = 0;
+        s_fc = t.first_child[nb];
+        s_e = t.exp_of[nb];
+    }
+    __syncthreads();
+    int level = 0, nacc = 0;
     for (;;) {
-        int cur_p = t.pidx[nb + cur];
+        const int cur_p = s_curp, fc = s_fc, e = s_e;
         if (level > t.D || cur_p < 0 || cur_p > a.R) {   // unreachable
             if (tid == 0) atomicOr(t.err, 32);
             break;
         }
         const char* row = (const char*)a.logits + ((int64_t)b * (a.R + 1) + cur_p) * t.stride * ESZ;
-        // ---- this layer's candidates (one lane per slot, compacted in slot
-        //      order) and all of the layer's uniforms ------------------------
-        const int fc = t.first_child[nb + cur];
-        const int e = t.exp_of[nb + cur];
+        // ---- the node's data, then the segment (registers for the first
+        //      JREG chunks of each wave), then the logits of the special
+        //      tokens this block owns: all in flight together --------------
         const int nt = (fc >= 0 && !DN) ? t.S - t.m : 0;
+        const int64_t tb = ((int64_t)b * t.E + (e >= 0 ? e : 0)) * t.S;
+        int sp_id = -1;                      // tail entry tid (sparse)
+        uint32_t sp_q = 0;
+        if (tid < nt) {
+            sp_id = t.tail_id[tb + tid];
+            sp_q = t.tail_q[tb + tid];
+        }
+        bool keep = false;
+        int kind = -1, ctok = -1, cpidx = -1, cfc = -1, ce = -1;
+        if (tid < WAVE && fc >= 0 && lane < K) {
+            const int64_t o = nb + fc + lane;
+            cpidx = t.pidx[o];
+            kind = (t.meta[o] >> 16) & 0xFF;
+            ctok = t.tok[o];
+            cfc = t.first_child[o];
+            ce = t.exp_of[o];
+            keep = cpidx > 0;
+        }
+        const uint64_t Zq = (fc >= 0) ? t.zq[(int64_t)b * t.E + e] : 1;
+        uint4 xr[JREG];
+#pragma unroll
+        for (int j = 0; j < JREG; ++j) {
+            const int c = c0 + wid + NWV * j;
+            xr[j] = (c < c1) ? load_vec<DT>(row, c * WAVE + lane, V) : make_uint4(0, 0, 0, 0);
+        }
+        float sp_l = 0.0f;                   // logit of this thread's tail token, if owned
+        if (sp_id >= lo_tok && sp_id < hi_tok) sp_l = load_logit<DT>(row, sp_id);
+        float c_l = 0.0f;                    // logit of this lane's candidate, if owned
+        if (keep && ctok >= lo_tok && ctok < hi_tok) c_l = load_logit<DT>(row, ctok);
         // dense mode: q~ at this node comes from its draft row (borrowed),
         // the logit of its x_{m+1} and its leads
         const char* drow = nullptr;
@@ -262,47 +305,62 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
             dref = t.dref[(int64_t)b * t.E + e];
             if (tid < nlead) s_lead[tid] = t.dleads[((int64_t)b * t.E + e) * 16 + tid];
         }
+        // ---- candidates: the kept children in slot order (wave 0), the
+        //      layer's uniforms, and the stored tail into LDS ---------------
+        if (tid < nt) {
+            s_tid[tid] = sp_id;
+            s_tq[tid] = sp_q;
+        }
+        for (int i = tid + NTV; i < nt; i += NTV) {
+            s_tid[i] = t.tail_id[tb + i];
+            s_tq[i] = t.tail_q[tb + i];
+        }
+        int cpos = -1;
         if (tid < WAVE) {
-            bool keep = false;
-            int kind = -1, tok = -1;
-            if (fc >= 0 && lane < K) {
-                keep = t.pidx[nb + fc + lane] > 0;
-                kind = (t.meta[nb + fc + lane] >> 16) & 0xFF;
-                tok = t.tok[nb + fc + lane];
-            }
             uint32_t cq = 0;
             if (DN && keep) {
                 bool lead = false;
                 for (int q = 0; q < nlead; ++q)
-                    lead |= t.dleads[((int64_t)b * t.E + e) * 16 + q] == tok;
-                cq = lead ? 0u : cweight(load_logit<DT>(drow, tok), dref, a.kT);
+                    lead |= t.dleads[((int64_t)b * t.E + e) * 16 + q] == ctok;
+                cq = lead ? 0u : cweight(load_logit<DT>(drow, ctok), dref, a.kT);
             }
             const uint64_t msk = __ballot(keep);
             const uint64_t smk = __ballot(keep && kind == SAMPLED);
             if (keep) {
-                const int pos = (int)__builtin_amdgcn_mbcnt_hi(
+                cpos = (int)__builtin_amdgcn_mbcnt_hi(
                     (uint32_t)(msk >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)msk, 0u));
-                s_c_uid[pos] = fc + lane;
-                s_c_tok[pos] = tok;
-                s_c_slot[pos] = lane + 1;
-                s_c_zero[pos] = 0;
-                s_c_q[pos] = cq;
+                s_c_uid[cpos] = fc + lane;
+                s_c_tok[cpos] = ctok;
+                s_c_slot[cpos] = lane + 1;
+                s_c_zero[cpos] = 0;
+                s_c_q[cpos] = cq;
+                s_c_pidx[cpos] = cpidx;
+                s_c_fc[cpos] = cfc;
+                s_c_e[cpos] = ce;
             }
             if (lane == 0) {
                 s_nc = __popcll(msk);
                 s_spos = smk ? __popcll(msk & ((smk & (~smk + 1)) - 1)) : -1;
             }
-            // draw j of this layer: j = 0 the sampled-token test, j = slot
-            // for the candidate tests; then the final sample
-            if (lane <= K)
-                s_U[lane] = philox_draw(a.rng_key, P_VERIFY, (uint64_t)b,
-                                        (uint64_t)(32 * level + lane)) >> 32;
-            if (lane == K + 1) s_Ufin = philox_draw(a.rng_key, P_FINAL, (uint64_t)b, (uint64_t)level);
+        } else if (wid == 1 && lane <= K + 1) {
+            // the layer's draws, one per lane: j = 0 the sampled-token test,
+            // j = slot for the candidate tests, then the final sample
+            const bool fin = lane == K + 1;
+            const uint64_t d = philox_draw(a.rng_key, fin ? P_FINAL : P_VERIFY, (uint64_t)b,
+                                           fin ? (uint64_t)level : (uint64_t)(32 * level + lane));
+            if (fin) s_Ufin = d;
+            else s_U[lane] = d >> 32;
         }
-        // ---- 1. row maximum (each wave streams whole chunks of the segment) ----
+        // ---- 1. row maximum over the segment -------------------------------
         float mx = -INFINITY;
-#pragma unroll 4
-        for (int c = c0 + wid; c < c1; c += NWV) {
+#pragma unroll
+        for (int j = 0; j < JREG; ++j) {
+            if (c0 + wid + NWV * j < c1) {
+#pragma unroll
+                for (int k = 0; k < VEC; ++k) mx = fmaxf(mx, velem<DT>(xr[j], k));
+            }
+        }
+        for (int c = c0 + wid + NWV * JREG; c < c1; c += NWV) {
             const uint4 xv = load_vec<DT>(row, c * WAVE + lane, V);
 #pragma unroll
             for (int k = 0; k < VEC; ++k) mx = fmaxf(mx, velem<DT>(xv, k));
@@ -311,14 +369,6 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
         if (tid == 0)
             __hip_atomic_store(&tmax_x[g], __float_as_uint(mx), __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
-        // the stored tail of q~ at this node (read-only tree data)
-        if (nt > 0) {
-            const int64_t tb = ((int64_t)b * t.E + e) * t.S;
-            for (int i = tid; i < nt; i += NTV) {
-                s_tid[i] = t.tail_id[tb + i];
-                s_tq[i] = t.tail_q[tb + i];
-            }
-        }
         if (!team_barrier(flags, g, G, epoch + 3 * level + 1, t.err, &s_ok)) break;
         const int nc = s_nc, spos = s_spos;
         if (tid < WAVE) {
@@ -331,10 +381,24 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
         }
         __syncthreads();
         const float M = s_M;
-        // ---- 2. weights of the segment (second pass, from L2), chunk totals,
-        //         p's weights at the special tokens ---------------------------
-#pragma unroll 2
-        for (int c = c0 + wid; c < c1; c += NWV) {
+        // ---- 2. weights of the segment, chunk totals, and p's weights at
+        //         the special tokens this block owns ---------------------------
+#pragma unroll
+        for (int j = 0; j < JREG; ++j) {
+            const int c = c0 + wid + NWV * j;
+            if (c < c1) {
+                uint64_t sum = 0;
+#pragma unroll
+                for (int k = 0; k < VEC; ++k) {
+                    const int v = (c * WAVE + lane) * VEC + k;
+                    if (v < V) sum += cweight(velem<DT>(xr[j], k), M, a.kT);
+                }
+                sum = wave_sum_u64(sum);
+                if (lane == 0)
+                    __hip_atomic_store(&chunk_x[c], sum, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+        for (int c = c0 + wid + NWV * JREG; c < c1; c += NWV) {
             const uint4 xv = load_vec<DT>(row, c * WAVE + lane, V);
             uint64_t sum = 0;
 #pragma unroll
@@ -346,58 +410,146 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
             if (lane == 0)
                 __hip_atomic_store(&chunk_x[c], sum, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
-        {
-            const int lo_tok = c0 * CH, hi_tok = min(V, c1 * CH);
-            for (int i = tid; i < nt; i += NTV) {
-                const int v = s_tid[i];
-                if (v >= lo_tok && v < hi_tok)
-                    __hip_atomic_store(&sp_x[i], cweight(load_logit<DT>(row, v), M, a.kT),
-                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            }
-            if (tid < nc) {
-                const int v = s_c_tok[tid];
-                if (v >= lo_tok && v < hi_tok)
-                    __hip_atomic_store(&sp_x[nt + tid], cweight(load_logit<DT>(row, v), M, a.kT),
-                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            }
+        if (sp_id >= lo_tok && sp_id < hi_tok)
+            __hip_atomic_store(&sp_x[tid], cweight(sp_l, M, a.kT), __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+        for (int i = tid + NTV; i < nt; i += NTV) {
+            const int v = s_tid[i];
+            if (v >= lo_tok && v < hi_tok)
+                __hip_atomic_store(&sp_x[i], cweight(load_logit<DT>(row, v), M, a.kT),
+                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
+        if (cpos >= 0 && ctok >= lo_tok && ctok < hi_tok)
+            __hip_atomic_store(&sp_x[nt + cpos], cweight(c_l, M, a.kT), __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
         if (!team_barrier(flags, g, G, epoch + 3 * level + 2, t.err, &s_ok)) break;
-        uint64_t part = 0;
-        for (int c = tid; c < NC; c += NTV) {
-            const uint64_t v = __hip_atomic_load(&chunk_x[c], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            s_chunk[c] = v;
-            part += v;
-        }
-        for (int i = tid; i < nt + nc; i += NTV)
-            s_tp[i] = __hip_atomic_load(&sp_x[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (tid < nc) s_c_tail[tid] = find_sorted(s_tid, nt, s_c_tok[tid]);
-        const uint64_t Sp = block_sum_u64<NTV>(part, s_red);
-        // ---- 3. Algorithm 1 at this layer -----------------------------------
-        const uint64_t Zq = (fc >= 0) ? t.zq[(int64_t)b * t.E + e] : 1;
-        if (tid == 0) {
-            int mode = 0;          // 0: residual tests follow, 1: accepted, 2: final sample
-            int next = -1, token = -1;
-            if (nc == 0) mode = 2;
+        // ---- 3. Algorithm 1 at this layer, by wave 0 (the chunk totals and
+        //         the special weights from the team, S_p, the tail deficit,
+        //         and the decisions of lane 0) ---------------------------------
+        uint64_t Sp = 0;
+        // The remaining candidates' tests in slot order (Algorithm 1), one
+        // lane per candidate: lane ci holds N_ci (0 for the sampled child);
+        // the residual mass before candidate ci is Zrem less the N of the
+        // candidates before it (all rejected if ci is reached), so the
+        // first lane whose test passes is the accepted candidate.  Returns
+        // its index, or -1 with *zrem reduced by every candidate's N; marks
+        // the rejected candidates.  Wave 0 only.
+        auto cand_tests = [&](int nc_, int spos_, u128 Nu, u128* zrem) -> int {
+            const bool cand = lane < nc_ && lane != spos_;
+            if (!cand) Nu = 0;
+            const u128 before = wave_incl_scan_u128(Nu) - Nu;
+            const u128 zr = *zrem - before;
+            const uint64_t U = cand ? s_U[s_c_slot[lane]] : 0ull;
+            const bool pass = cand && ((u128)(U + 1) * zr <= (Nu << 32));
+            const uint64_t pm = __ballot(pass);
+            const int first = pm ? (int)__builtin_ctzll(pm) : WAVE;
+            if (cand && lane < first) s_c_zero[lane] = 1;
+            if (pm) return first;
+            *zrem -= wave_sum_u128(Nu);
+            return -1;
+        };
+        if (tid < WAVE) {
+            // latency-critical single-wave section: issue ahead of the
+            // weight passes of other blocks on this compute unit
+            __builtin_amdgcn_s_setprio(3);
+            uint64_t part = 0;
+            for (int cb = 0; cb < NC; cb += 4 * WAVE) {
+                uint64_t cv[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int c = cb + q * WAVE + lane;
+                    cv[q] = (c < NC) ? __hip_atomic_load(&chunk_x[c], __ATOMIC_RELAXED,
+                                                         __HIP_MEMORY_SCOPE_AGENT) : 0ull;
+                }
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int c = cb + q * WAVE + lane;
+                    if (c < NC) s_chunk[c] = cv[q];
+                    part += cv[q];
+                }
+            }
+            const int nsp = nt + nc;
+            for (int ib = 0; ib < nsp; ib += 4 * WAVE) {
+                uint32_t pv[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int i = ib + q * WAVE + lane;
+                    pv[q] = (i < nsp) ? __hip_atomic_load(&sp_x[i], __ATOMIC_RELAXED,
+                                                          __HIP_MEMORY_SCOPE_AGENT) : 0u;
+                }
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int i = ib + q * WAVE + lane;
+                    if (i < nsp) s_tp[i] = pv[q];
+                }
+            }
+            Sp = wave_sum_u64(part);
+            wave_sync();
+            if (lane < nc) s_c_tail[lane] = DN ? -1 : find_sorted(s_tid, nt, s_c_tok[lane]);
+            wave_sync();
+            // the sampled child first (every lane takes the same decision)
+            int mode = (nc == 0) ? 2 : 0;      // 0: candidate tests follow, 1: accepted, 2: final sample
+            int next = -1;
             if (spos >= 0) {
                 const int yi = s_c_tail[spos];
-                if (!DN && yi < 0) atomicOr(t.err, 4);
+                if (!DN && yi < 0 && lane == 0) atomicOr(t.err, 4);
                 const uint64_t QY = DN ? (uint64_t)s_c_q[spos] : ((yi >= 0) ? s_tq[yi] : 0);
                 const uint64_t PY = s_tp[nt + spos];
                 const uint64_t U = s_U[0];
                 if ((u128)(U + 1) * QY * Sp <= (((u128)PY * Zq) << 32)) {
                     mode = 1;
-                    next = s_c_uid[spos];
-                    token = s_c_tok[spos];
+                    next = spos;
                 }
             }
-            s_mode = mode;
-            s_next = next;
-            s_token = token;
-            s_F = (spos >= 0 && mode == 0) ? (u128)Zq : (u128)1;
+            const bool resid = spos >= 0 && mode == 0;
+            const u128 F = resid ? (u128)Zq : (u128)1;
+            // no rejected Y: r = p, mass S_p.  Sparse rejection: Z_r = Zq Sp
+            // less the sum over the tail of min(P_v Zq, Q_v Sp).  Dense
+            // rejection: the residual totals come from a third pass.
+            u128 Zrem = Sp;
+            if (resid && !DN) {
+                u128 d = 0;
+                for (int i = lane; i < nt; i += WAVE) {
+                    const u128 pz = (u128)s_tp[i] * Zq, qs = (u128)s_tq[i] * Sp;
+                    d += pz < qs ? pz : qs;
+                }
+                Zrem = (u128)Zq * Sp - wave_sum_u128(d);
+            }
+            if (mode == 0 && !(DN && resid)) {
+                u128 Nu = 0;
+                if (lane < nc) {
+                    const uint64_t P = s_tp[nt + lane];
+                    const int ti = s_c_tail[lane];
+                    Nu = F * (u128)P;
+                    if (resid && ti >= 0) {
+                        const u128 pz = (u128)P * Zq, qs = (u128)s_tq[ti] * Sp;
+                        Nu = pz > qs ? pz - qs : (u128)0;
+                    }
+                }
+                next = cand_tests(nc, spos, Nu, &Zrem);
+                mode = next >= 0 ? 1 : 2;
+            }
+            if (lane == 0) {
+                s_Sp = Sp;
+                s_mode = mode;
+                s_resid = resid ? 1 : 0;
+                s_F = F;
+                s_Zrem = Zrem;
+                if (mode == 2) s_tt = mulhi_64x128(s_Ufin, Zrem);
+                if (mode == 1) {
+                    s_token = s_c_tok[next];
+                    s_cur = s_c_uid[next];
+                    s_curp = s_c_pidx[next];
+                    s_fc = s_c_fc[next];
+                    s_e = s_c_e[next];
+                }
+            }
+            __builtin_amdgcn_s_setprio(0);
         }
         __syncthreads();
-        const bool residual = (spos >= 0 && s_mode == 0);   // Y rejected: r from p - q~
-        if (DN && residual) {
+        Sp = s_Sp;
+        const bool residual = s_resid != 0;
+        if (DN && s_mode == 0) {
             // N_v = max(0, P_v Zq - Q_v Sp) over all of V (Q_v from the draft
             // row, 0 at the leads): chunk totals over the segment, exchanged
             for (int c = c0 + wid; c < c1; c += NWV) {
@@ -425,62 +577,37 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
                 }
             }
             if (!team_barrier(flags, g, G, epoch + 3 * level + 3, t.err, &s_ok)) break;
-            u128 part = 0;
-            for (int c = tid; c < NC; c += NTV) part += nchunk_at(c);
-            const u128 tot = block_sum_u128(part, s_w128);
-            if (tid == 0) s_Zrem = tot;
-        } else if (residual) {
-            // Z_r = Zq Sp - sum over the tail of min(P_v Zq, Q_v Sp)
-            u128 d = 0;
-            for (int i = tid; i < nt; i += NTV) {
-                const u128 pz = (u128)s_tp[i] * Zq, qs = (u128)s_tq[i] * Sp;
-                d += pz < qs ? pz : qs;
-            }
-            const u128 tot = block_sum_u128(d, s_w128);
-            if (tid == 0) s_Zrem = (u128)Zq * Sp - tot;
-        } else if (tid == 0) {
-            s_Zrem = Sp;
-        }
-        __syncthreads();
-        if (tid == 0 && s_mode == 0) {
-            const u128 F = s_F;
-            u128 Zrem = s_Zrem;
-            int mode = 2, next = -1, token = -1;
-            for (int ci = 0; ci < nc; ++ci) {
-                if (ci == spos) continue;
-                const int ti = s_c_tail[ci];
-                const uint64_t P = s_tp[nt + ci];
-                u128 Nu = F * (u128)P;
-                if (DN && residual) {
-                    const u128 pz = (u128)P * Zq, qs = (u128)s_c_q[ci] * Sp;
-                    Nu = pz > qs ? pz - qs : (u128)0;
-                } else if (residual && ti >= 0) {
-                    const u128 pz = (u128)P * Zq, qs = (u128)s_tq[ti] * Sp;
+            if (tid < WAVE) {
+                __builtin_amdgcn_s_setprio(3);
+                u128 part = 0;
+                for (int c = lane; c < NC; c += WAVE) part += nchunk_at(c);
+                u128 Zrem = wave_sum_u128(part);
+                u128 Nu = 0;
+                if (lane < nc) {
+                    const uint64_t P = s_tp[nt + lane];
+                    const u128 pz = (u128)P * Zq, qs = (u128)s_c_q[lane] * Sp;
                     Nu = pz > qs ? pz - qs : (u128)0;
                 }
-                const uint64_t U = s_U[s_c_slot[ci]];
-                if ((u128)(U + 1) * Zrem <= (Nu << 32)) {
-                    mode = 1;
-                    next = s_c_uid[ci];
-                    token = s_c_tok[ci];
-                    break;
+                const int next = cand_tests(nc, spos, Nu, &Zrem);
+                if (lane == 0) {
+                    s_mode = next >= 0 ? 1 : 2;
+                    s_Zrem = Zrem;
+                    if (next < 0) s_tt = mulhi_64x128(s_Ufin, Zrem);
+                    if (next >= 0) {
+                        s_token = s_c_tok[next];
+                        s_cur = s_c_uid[next];
+                        s_curp = s_c_pidx[next];
+                        s_fc = s_c_fc[next];
+                        s_e = s_c_e[next];
+                    }
                 }
-                Zrem -= Nu;
-                s_c_zero[ci] = 1;
+                __builtin_amdgcn_s_setprio(0);
             }
-            s_mode = mode;
-            s_next = next;
-            s_token = token;
-            s_Zrem = Zrem;
+            __syncthreads();
         }
-        if (tid == 0 && s_mode == 2) {
-            s_tt = mulhi_64x128(s_Ufin, s_Zrem);
-        }
-        __syncthreads();
         if (s_mode == 1) {
             if (g == 0 && tid == 0) a.accepted[(int64_t)b * t.D + nacc] = s_token;
             ++nacc;
-            cur = s_next;
             ++level;
             __syncthreads();
             continue;
