@@ -13,7 +13,7 @@ Protocol
      cycling over the recorded steps, bracketed by torch.cuda.synchronize();
      every replay must reproduce the discovery outputs bit for bit.
   3. HIP events around each rheo_expand_level call (on the stream it launches
-     on) give the duration of an expand level (k_select and the pool kernels, the
+     on) give the duration of an expand level (its selection and pool kernels, the
      dominant work); its algorithmic bytes are the draft rows it must read
      (rows x V x 2 bytes).  Then the same steps are captured as HIP graphs
      (one per recorded step) and replayed; `value` is the graph-replay
@@ -41,7 +41,7 @@ def log(*a):
 
 
 KERNEL_SRCS = ["expand.hip", "dense.hip", "pool_common.h", "rheo_device.h", "rheo_state.h"]
-EXPAND_KERNELS = r"k_select|k_pool|k_dweights|k_dpool"
+EXPAND_KERNELS = r"k_select|k_pool|k_dweights|k_dpool|k_expand_row"
 
 
 def kernel_src_hash():
@@ -67,7 +67,7 @@ def _counter_rows(path, regex, counter):
 
 
 def expand_kernel_name(w):
-    return ("expand level (k_select + k_pool)" if w.support > 0
+    return ("expand level (k_expand_row; k_select + k_pool below 128 rows)" if w.support > 0
             else "expand level (k_select + k_dweights + k_dpool)")
 
 
@@ -75,9 +75,10 @@ def write_traffic(paths, out, w, copy_bytes):
     """Scales the expand kernel's FETCH_SIZE / WRITE_SIZE by what the same
     counters read for a plain device copy of known size."""
     exp_f, exp_w, cp_f, cp_w = paths
-    # one expand level = one k_select dispatch and the pool kernel(s) after it
-    nf = len(_counter_rows(exp_f, r"k_select", "FETCH_SIZE"))
-    nw = len(_counter_rows(exp_w, r"k_select", "WRITE_SIZE"))
+    # one expand level = one k_expand_row dispatch, or one k_select dispatch
+    # and the pool kernel(s) after it
+    nf = len(_counter_rows(exp_f, r"k_select|k_expand_row", "FETCH_SIZE"))
+    nw = len(_counter_rows(exp_w, r"k_select|k_expand_row", "WRITE_SIZE"))
     ef = [sum(_counter_rows(exp_f, EXPAND_KERNELS, "FETCH_SIZE")) / nf]
     ew = [sum(_counter_rows(exp_w, EXPAND_KERNELS, "WRITE_SIZE")) / nw]
     cf = _counter_rows(cp_f, r"copy|Copy", "FETCH_SIZE")

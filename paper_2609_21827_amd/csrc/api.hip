@@ -38,6 +38,9 @@ constexpr int kMaxV = 262143;
 float k_of_T(float T) { return (float)(1.4426950408889634 / (double)T); }
 
 // tokens of one 64-vector sub-chunk (16-byte vectors of bf16 or fp32)
+// Rows in a level from which one block per row fills the chip.
+constexpr int kRowMin = 128;
+
 int WAVE_TOKENS(int dtype) { return 64 * (dtype == RHEO_BF16 ? 8 : 4); }
 
 // A chunk size fits when the row's chunk lists fit the merge (and, in dense
@@ -56,6 +59,8 @@ struct rheo_tree {
     int level = 0;
     int R = 0;
     int variant = 0;
+    int row_mode = 0;                     // sparse levels: 1 one block per row, 0 chunks,
+                                          // -1 by the number of rows
     int vG = 1, v_segch = 1, v_grid = 1;  // verification team shape
     float T_expand = 1.0f;
     void* blocks[48] = {};
@@ -154,6 +159,14 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
         delete t;
         return fail(RHEO_EINVAL, "vocab %d with support %d exceeds the expand merge capacity",
                     c.vocab, SL);
+    }
+    // sparse levels with at least kRowMin rows run one block per row (the
+    // row streamed once, no chunk lists) when the row fits it;
+    // RHEO_EXPAND_ROW=0 or 1 forces the chunked or the per-row kernel
+    t->row_mode = (!dense && expand_row_nq(c.dtype, c.vocab) > 0) ? -1 : 0;
+    if (const char* er = getenv("RHEO_EXPAND_ROW")) {
+        if (er[0] == '0') t->row_mode = 0;
+        else if (er[0] == '1' && t->row_mode != 0) t->row_mode = 1;
     }
     const char* env = getenv("RHEO_EXPAND_VARIANT");
     if (env) {
@@ -274,6 +287,8 @@ int rheo_expand_level(rheo_tree* t, const void* logits, float T, uint64_t key, v
         e = launch_select(t->dev, a, t->variant, (hipStream_t)stream);
         if (e == hipSuccess)
             e = launch_dense(t->dev, a, expand_variant_nvc(t->variant), (hipStream_t)stream);
+    } else if (t->row_mode == 1 || (t->row_mode < 0 && t->dev.B * a.P >= kRowMin)) {
+        e = launch_expand_row(t->dev, a, (hipStream_t)stream);
     } else {
         e = launch_expand(t->dev, a, t->variant, (hipStream_t)stream);
     }

@@ -37,6 +37,8 @@ constexpr int CAPC = 1024;    // candidates a chunk collects in LDS
 constexpr int CAPV = 512;     // candidate vectors a chunk collects in LDS
 constexpr int SMAX = 1024;    // largest support
 constexpr int MERGE_MAX = 2048;  // chunk-list keys one row merges (C * Sc)
+constexpr int NTE = 512;      // threads per k_expand_row block
+constexpr int EBATCH = 8;     // 16-byte vectors per thread and batch of k_expand_row
 
 template <int DT>
 __device__ __forceinline__ float elem(const uint4& v, int k) {
@@ -106,9 +108,9 @@ __host__ __device__ inline PoolLds pool_lds(int S, int C) {
 // other blocks (token, score, path) are published with agent-scope atomics.
 template <int NT>
 __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, int row,
-                                          uint8_t* lds, int pu, const ParentRec& pr, uint64_t u,
-                                          uint64_t* s_red, int* s_yi) {
-    const PoolLds L = pool_lds(t.S, t.C);
+                                          uint8_t* lds, const PoolLds& L, int pu,
+                                          const ParentRec& pr, uint64_t u, uint64_t* s_red,
+                                          int* s_yi) {
     uint64_t* s_top = (uint64_t*)(lds + L.top);
     uint64_t* s_k2 = (uint64_t*)(lds + L.k2);
     uint32_t* s_w1 = (uint32_t*)(lds + L.w1);
@@ -260,6 +262,26 @@ __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, 
     }
 }
 
+// The parent of row j of sequence b: frontier node j of the previous level
+// (the n_expand children with the highest priority, chosen by the previous
+// launch), with the Philox draw of its sampled slot.  One thread.
+__device__ __forceinline__ void row_parent(const TreeDev& t, const LevelArgs& a, int b, int j,
+                                           int* s_pu, uint64_t* s_u) {
+    const int level = a.level, K = t.K, NE = t.NE;
+    int pu = (level == 0) ? 0 : t.frontier[(int64_t)b * NE + j];
+    const int lo_uid = (level == 0) ? 0 : ((level == 1) ? 1 : 1 + K + (level - 2) * NE * K);
+    const int hi_uid = (level == 0) ? 1 : lo_uid + ((level == 1) ? 1 : NE) * K;
+    if (pu < lo_uid || pu >= hi_uid) {
+        atomicOr(t.err, 16);
+        pu = 0;
+    }
+    *s_pu = pu;
+    uint64_t u = (level == 0) ? philox_draw(a.rng_key, P_DRAFT, (uint64_t)b, 0ull)
+                              : t.fr_u[(int64_t)b * NE + j];
+    if (pu == 0 && level > 0) u = philox_draw(a.rng_key, P_DRAFT, (uint64_t)b, 0ull);
+    *s_u = u;
+}
+
 // ---------------------------------------------------------------------------
 // k_pool: one block per row: parent, support (merge of the chunk lists),
 // pool, and, by the last row of each sequence, the next frontier
@@ -289,19 +311,7 @@ __global__ __launch_bounds__(NTP) void k_pool(TreeDev t, LevelArgs a) {
     // with the Philox draw of its sampled slot; and the chunk lists, with
     // an empty list after them
     const int C4 = (C + 3) & ~3;
-    if (tid == 0) {
-        int pu = (level == 0) ? 0 : t.frontier[(int64_t)b * NE + j];
-        const int lo_uid = (level == 0) ? 0 : ((level == 1) ? 1 : 1 + K + (level - 2) * NE * K);
-        const int hi_uid = (level == 0) ? 1 : lo_uid + ((level == 1) ? 1 : NE) * K;
-        if (pu < lo_uid || pu >= hi_uid) {
-            atomicOr(t.err, 16);
-            pu = 0;
-        }
-        s_pu = pu;
-        s_u = (level == 0) ? philox_draw(a.rng_key, P_DRAFT, (uint64_t)b, 0ull)
-                           : t.fr_u[(int64_t)b * NE + j];
-        if (pu == 0 && level > 0) s_u = philox_draw(a.rng_key, P_DRAFT, (uint64_t)b, 0ull);
-    }
+    if (tid == 0) row_parent(t, a, b, j, &s_pu, &s_u);
     const uint64_t* src = t.sel + (int64_t)row * C * S;
     for (int i = tid; i < C * S; i += NTP) s_m[i] = src[i];
     for (int i = C * S + tid; i < (C + 1) * S; i += NTP) s_m[i] = 0ull;
@@ -364,7 +374,7 @@ __global__ __launch_bounds__(NTP) void k_pool(TreeDev t, LevelArgs a) {
     __syncthreads();
 
     // the pool, formed by the whole block
-    pool_form<NTP>(t, a, row, s_pdyn, s_pu, pr, s_u, s_red, &s_yi);
+    pool_form<NTP>(t, a, row, s_pdyn, L, s_pu, pr, s_u, s_red, &s_yi);
     if (level + 1 >= t.D) return;
 
     // the next frontier: the last row of the sequence to finish selects it
@@ -446,6 +456,164 @@ __device__ void rank_keys32(const uint32_t* keys, int n, int16_t* rank) {
         for (int o = 1; o < F; o <<= 1) cnt += __shfl_xor(cnt, o);
         if (i < n && sub == 0) rank[i] = (int16_t)cnt;
     }
+}
+
+// Exact selection for a degenerate range: more candidates than LDS holds
+// (massive ties at the threshold, or large values crowded into few
+// threads).  The range is NQ vectors per thread, vector q of this thread at
+// index vfirst + q * NT + tid; elements at V and beyond do not count;
+// push(v, id) records an element.  Rare, so it re-reads the range, four
+// vectors at a time.  bf16: count the elements whose code lies above the
+// threshold code h; if the nsel-th largest element has code h, take
+// everything above h and the smallest ids among those at h (ranks of the
+// ties in id order from per-wave counts and wave scans); if it lies above h
+// and the elements above h fit (at most cap), take those.  Otherwise, and for
+// fp32, find the nsel-th largest key by bisection.  Ends with a barrier.
+template <int DT, int NT, int NQ, typename Push>
+__device__ void exact_select_fallback(const char* base, int V, int vfirst, uint32_t h, int nsel,
+                                      int cap, Push push, int* s_redi,
+                                      int (*s_tie)[NT / WAVE]) {
+    constexpr int VEC = DT ? 8 : 4;
+    constexpr int NW = NT / WAVE;
+    static_assert(NQ % 4 == 0 && NQ <= 32, "re-read in groups of four vectors");
+    const int tid = threadIdx.x, lane = tid % WAVE, wid = tid / WAVE;
+    // an opaque trip count keeps each pass a loop (re-reading per pass)
+    // rather than one straight-line block holding every element
+    int nq = NQ;
+    asm volatile("" : "+s"(nq));
+    auto group = [&](int q0, uint4 (&w)[4]) {
+        // an opaque index keeps every pass's loads (and what is computed
+        // from them) inside its loop instead of live across the passes
+        int vf = vfirst;
+        asm volatile("" : "+v"(vf));
+#pragma unroll
+        for (int q = 0; q < 4; ++q) w[q] = load_row_vec<DT>(base, vf + (q0 + q) * NT + tid, V);
+    };
+    bool done = false;
+    if (DT) {
+        int ngt = 0;
+#pragma unroll 1
+        for (int q0 = 0; q0 < nq; q0 += 4) {
+            uint4 w[4];
+            group(q0, w);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int e0 = (vfirst + (q0 + q) * NT + tid) * VEC;
+#pragma unroll
+                for (int k = 0; k < VEC; ++k)
+                    ngt += (e0 + k < V && (ord32(elem<DT>(w[q], k)) >> 16) > h) ? 1 : 0;
+            }
+        }
+        ngt = block_sum_i32<NT>(ngt, s_redi);
+        if (ngt < nsel) {
+            // ties at h, in id order: vector q, then thread, then element
+            const int need = nsel - ngt;
+#pragma unroll 1
+            for (int q0 = 0; q0 < nq; q0 += 4) {
+                uint4 w[4];
+                group(q0, w);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int e0 = (vfirst + (q0 + q) * NT + tid) * VEC;
+                    int nt = 0;
+#pragma unroll
+                    for (int k = 0; k < VEC; ++k)
+                        nt += (e0 + k < V && (ord32(elem<DT>(w[q], k)) >> 16) == h) ? 1 : 0;
+                    const int tot = wave_sum_i32(nt);
+                    if (lane == 0) s_tie[q0 + q][wid] = tot;
+                }
+            }
+            __syncthreads();
+            int prior = 0;                   // ties in the vectors before q, all threads
+#pragma unroll 1
+            for (int q0 = 0; q0 < nq; q0 += 4) {
+                uint4 w[4];
+                group(q0, w);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int e0 = (vfirst + (q0 + q) * NT + tid) * VEC;
+                    int nt = 0;
+#pragma unroll
+                    for (int k = 0; k < VEC; ++k)
+                        nt += (e0 + k < V && (ord32(elem<DT>(w[q], k)) >> 16) == h) ? 1 : 0;
+                    int rk = prior + wave_excl_scan(nt);
+#pragma unroll
+                    for (int ww = 0; ww < NW; ++ww) {
+                        rk += (ww < wid) ? s_tie[q0 + q][ww] : 0;
+                        prior += s_tie[q0 + q][ww];
+                    }
+#pragma unroll
+                    for (int k = 0; k < VEC; ++k) {
+                        const float v = elem<DT>(w[q], k);
+                        const uint32_t cd = ord32(v) >> 16;
+                        if (e0 + k < V) {
+                            if (cd > h) {
+                                push(v, e0 + k);
+                            } else if (cd == h) {
+                                if (rk < need) push(v, e0 + k);
+                                ++rk;
+                            }
+                        }
+                    }
+                }
+            }
+            done = true;
+        } else if (ngt <= cap) {
+#pragma unroll 1
+            for (int q0 = 0; q0 < nq; q0 += 4) {
+                uint4 w[4];
+                group(q0, w);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int e0 = (vfirst + (q0 + q) * NT + tid) * VEC;
+#pragma unroll
+                    for (int k = 0; k < VEC; ++k) {
+                        const float v = elem<DT>(w[q], k);
+                        if (e0 + k < V && (ord32(v) >> 16) > h) push(v, e0 + k);
+                    }
+                }
+            }
+            done = true;
+        }
+    }
+    if (!done) {
+        uint64_t x = 0;
+#pragma unroll 1
+        for (int bit = 63; bit >= 0; --bit) {
+            const uint64_t cand = x | (1ull << bit);
+            int n = 0;
+#pragma unroll 1
+            for (int q0 = 0; q0 < nq; q0 += 4) {
+                uint4 w[4];
+                group(q0, w);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int e0 = (vfirst + (q0 + q) * NT + tid) * VEC;
+#pragma unroll
+                    for (int k = 0; k < VEC; ++k)
+                        n += (e0 + k < V &&
+                              logit_key(elem<DT>(w[q], k), (uint32_t)(e0 + k)) >= cand) ? 1 : 0;
+                }
+            }
+            n = block_sum_i32<NT>(n, s_redi);
+            if (n >= nsel) x = cand;
+        }
+#pragma unroll 1
+        for (int q0 = 0; q0 < nq; q0 += 4) {
+            uint4 w[4];
+            group(q0, w);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int e0 = (vfirst + (q0 + q) * NT + tid) * VEC;
+#pragma unroll
+                for (int k = 0; k < VEC; ++k) {
+                    const float v = elem<DT>(w[q], k);
+                    if (e0 + k < V && logit_key(v, (uint32_t)(e0 + k)) >= x) push(v, e0 + k);
+                }
+            }
+        }
+    }
+    __syncthreads();
 }
 
 template <int DT, int NVC>
@@ -691,159 +859,21 @@ __device__ __forceinline__ void select_block(const TreeDev& t, const LevelArgs& 
     int cnt = s_cnt;
 
     if (cnt > CAPC) {
-        // Degenerate chunk: more candidates than LDS holds (massive ties at
-        // the threshold, or large values crowded into few threads).  Exact;
-        // rare, so it re-reads the chunk, four vectors at a time, rather than
-        // keeping it in registers.  bf16: count the elements whose code lies
-        // above the threshold code h; if the nsel-th largest element has code
-        // h, take everything above h and the smallest ids among those at h
-        // (ranks of the ties in id order from per-wave counts and wave
-        // scans); if it lies above h and the elements above h fit, take
-        // those.  Otherwise, and for fp32, find the nsel-th largest key by
-        // bisection.
+        // degenerate chunk: exact selection from the chunk in memory
         const int eb = v0 * VEC;                 // first element of the chunk
-        auto push = [&](float v, int l) {
-            const int pos = atomicAdd(&s_cnt, 1);
-            if (pos < CAPC) {
-                if (DT) s_k32[pos] = chunk_key32(v, l);
-                else s_keys[pos] = logit_key(v, (uint32_t)(eb + l));
-            }
-        };
+        __shared__ int s_tie[32][NW];
         __syncthreads();
         if (tid == 0) s_cnt = 0;
-        bool done = false;
-        if (DT) {
-            int ngt = 0;
-#pragma unroll 1
-            for (int i0 = 0; i0 < NVC; i0 += 4) {
-                uint4 w[4];
-#pragma unroll
-                for (int q = 0; q < 4; ++q) w[q] = load_row_vec<DT>(base, v0 + (i0 + q) * NTC + tid, V);
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const int l0 = ((i0 + q) * NTC + tid) * VEC;
-#pragma unroll
-                    for (int k = 0; k < VEC; ++k)
-                        ngt += (eb + l0 + k < V && (ord32(elem<DT>(w[q], k)) >> 16) > h) ? 1 : 0;
+        exact_select_fallback<DT, NTC, NVC>(
+            base, V, v0, h, nsel, CAPC,
+            [&](float v, int id) {
+                const int pos = atomicAdd(&s_cnt, 1);
+                if (pos < CAPC) {
+                    if (DT) s_k32[pos] = chunk_key32(v, id - eb);
+                    else s_keys[pos] = logit_key(v, (uint32_t)id);
                 }
-            }
-            ngt = block_sum_i32<NTC>(ngt, s_redi);
-            if (ngt < nsel) {
-                // ties at h, in id order: vector i, then thread, then element
-                __shared__ int s_tie[32][NW];            // ties per (vector, wave)
-                const int need = nsel - ngt;
-#pragma unroll 1
-                for (int i0 = 0; i0 < NVC; i0 += 4) {
-                    uint4 w[4];
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) w[q] = load_row_vec<DT>(base, v0 + (i0 + q) * NTC + tid, V);
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        const int l0 = ((i0 + q) * NTC + tid) * VEC;
-                        int nt = 0;
-#pragma unroll
-                        for (int k = 0; k < VEC; ++k)
-                            nt += (eb + l0 + k < V && (ord32(elem<DT>(w[q], k)) >> 16) == h) ? 1 : 0;
-                        const int tot = wave_sum_i32(nt);
-                        if (lane == 0) s_tie[i0 + q][wid] = tot;
-                    }
-                }
-                __syncthreads();
-                int prior = 0;                   // ties in the vectors before i, all threads
-#pragma unroll 1
-                for (int i0 = 0; i0 < NVC; i0 += 4) {
-                    uint4 w[4];
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) w[q] = load_row_vec<DT>(base, v0 + (i0 + q) * NTC + tid, V);
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        const int i = i0 + q;
-                        const int l0 = (i * NTC + tid) * VEC;
-                        int nt = 0;
-#pragma unroll
-                        for (int k = 0; k < VEC; ++k)
-                            nt += (eb + l0 + k < V && (ord32(elem<DT>(w[q], k)) >> 16) == h) ? 1 : 0;
-                        int rk = prior + wave_excl_scan(nt);
-#pragma unroll
-                        for (int ww = 0; ww < NW; ++ww) {
-                            rk += (ww < wid) ? s_tie[i][ww] : 0;
-                            prior += s_tie[i][ww];
-                        }
-#pragma unroll
-                        for (int k = 0; k < VEC; ++k) {
-                            const float v = elem<DT>(w[q], k);
-                            const uint32_t cd = ord32(v) >> 16;
-                            if (eb + l0 + k < V) {
-                                if (cd > h) {
-                                    push(v, l0 + k);
-                                } else if (cd == h) {
-                                    if (rk < need) push(v, l0 + k);
-                                    ++rk;
-                                }
-                            }
-                        }
-                    }
-                }
-                done = true;
-            } else if (ngt <= CAPC) {
-#pragma unroll 1
-                for (int i0 = 0; i0 < NVC; i0 += 4) {
-                    uint4 w[4];
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) w[q] = load_row_vec<DT>(base, v0 + (i0 + q) * NTC + tid, V);
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        const int l0 = ((i0 + q) * NTC + tid) * VEC;
-#pragma unroll
-                        for (int k = 0; k < VEC; ++k) {
-                            const float v = elem<DT>(w[q], k);
-                            if (eb + l0 + k < V && (ord32(v) >> 16) > h) push(v, l0 + k);
-                        }
-                    }
-                }
-                done = true;
-            }
-        }
-        if (!done) {
-            uint64_t x = 0;
-#pragma unroll 1
-            for (int bit = 63; bit >= 0; --bit) {
-                const uint64_t cand = x | (1ull << bit);
-                int n = 0;
-#pragma unroll 1
-                for (int i0 = 0; i0 < NVC; i0 += 4) {
-                    uint4 w[4];
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) w[q] = load_row_vec<DT>(base, v0 + (i0 + q) * NTC + tid, V);
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        const int l0 = ((i0 + q) * NTC + tid) * VEC;
-#pragma unroll
-                        for (int k = 0; k < VEC; ++k)
-                            n += (eb + l0 + k < V &&
-                                  logit_key(elem<DT>(w[q], k), (uint32_t)(eb + l0 + k)) >= cand) ? 1 : 0;
-                    }
-                }
-                n = block_sum_i32<NTC>(n, s_redi);
-                if (n >= nsel) x = cand;
-            }
-#pragma unroll 1
-            for (int i0 = 0; i0 < NVC; i0 += 4) {
-                uint4 w[4];
-#pragma unroll
-                for (int q = 0; q < 4; ++q) w[q] = load_row_vec<DT>(base, v0 + (i0 + q) * NTC + tid, V);
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const int l0 = ((i0 + q) * NTC + tid) * VEC;
-#pragma unroll
-                    for (int k = 0; k < VEC; ++k) {
-                        const float v = elem<DT>(w[q], k);
-                        if (eb + l0 + k < V && logit_key(v, (uint32_t)(eb + l0 + k)) >= x) push(v, l0 + k);
-                    }
-                }
-            }
-        }
-        __syncthreads();
+            },
+            s_redi, s_tie);
         cnt = min(s_cnt, CAPC);
     }
 
@@ -857,6 +887,249 @@ __device__ __forceinline__ void select_block(const TreeDev& t, const LevelArgs& 
         if (rk < nsel) out[rk] = DT ? row_key_of32(s_k32[i], v0 * VEC) : s_keys[i];
     }
     for (int i = nsel + tid; i < t.Sc; i += NTC) out[i] = 0ull;
+}
+
+
+// ---------------------------------------------------------------------------
+// k_expand_row: the whole level for one row per block.  The row is streamed
+// once (double-buffered batches of 16-byte vectors; only each vector's
+// exact maximum is kept, as a 16-bit order code in registers); the
+// threshold comes from every thread's two largest vector maxima as in
+// k_select; only the candidate vectors are read again; their elements above
+// the threshold are ranked into the support, then the pool (App. C.1) and,
+// by the last row of each sequence, the next frontier -- with no chunk
+// lists, no merge and no second launch.  Used when the row fits NQ vectors
+// per thread and the level has enough rows to fill the chip.
+// ---------------------------------------------------------------------------
+template <int DT, int NQ>
+__global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
+    constexpr int VEC = DT ? 8 : 4;
+    constexpr int NW = NTE / WAVE;
+    constexpr int NB = NQ / EBATCH;
+    constexpr int NM = DT ? NQ / 2 : NQ;
+    static_assert(NQ % (2 * EBATCH) == 0 && NQ <= 32, "batches come in pairs");
+    static_assert(CAPV <= NTE, "one candidate vector per thread");
+    extern __shared__ __align__(16) uint8_t s_pdyn[];
+    __shared__ __align__(16) uint64_t s_keys[CAPC];
+    __shared__ int16_t s_rank[CAPC];
+    __shared__ int s_cvi[CAPV];
+    __shared__ uint32_t s_hist[512];
+    __shared__ int s_bc[2][4];
+    __shared__ uint32_t s_h, s_h2;
+    __shared__ int s_above, s_cnt, s_nv;
+    __shared__ uint64_t s_red[NW];
+    __shared__ int s_redi[NW];
+    __shared__ int s_tie[32][NW];
+    __shared__ int s_pu, s_yi;
+    __shared__ uint64_t s_u;
+    const PoolLds L = pool_lds(t.S, 0);
+    uint64_t* s_top = (uint64_t*)(s_pdyn + L.top);
+    uint64_t* s_k2 = (uint64_t*)(s_pdyn + L.k2);
+
+    const int tid = threadIdx.x, lane = tid % WAVE, wid = tid / WAVE;
+    const int row = blockIdx.x;
+    const int b = row / a.P, j = row % a.P;
+    const int S = t.S, K = t.K, V = t.V;
+    const int level = a.level;
+    const int64_t nb = (int64_t)b * t.NN;
+    const int NVR = (V + VEC - 1) / VEC;          // vectors of the row, <= NTE * NQ
+    const int NVF = V / VEC;                       // whole vectors
+    const int nsel = S;                            // S <= V
+    const char* base = (const char*)a.logits + (int64_t)row * t.stride * (DT ? 2 : 4);
+
+    if (tid == 0) {
+        row_parent(t, a, b, j, &s_pu, &s_u);
+        s_cnt = 0;
+        s_nv = 0;
+    }
+    for (int i = tid; i < S; i += NTE) s_top[i] = 0ull;   // id -1 until ranked
+
+    // ---- the row, streamed: vector q of this thread is tid + NTE * q ------
+    uint32_t vm[NM];
+    uint32_t c1 = 0, c2 = 0;
+    rs_ushort2 p1 = {0, 0}, p2 = {0, 0};
+    const int wfirst = __builtin_amdgcn_readfirstlane(wid) * WAVE;
+    auto load_batch = [&](uint4 (&r)[EBATCH], int bt) {
+        // plain loads when every lane of the wave reads whole vectors
+        if (wfirst + WAVE - 1 + NTE * (bt * EBATCH + EBATCH - 1) < NVF) {
+#pragma unroll
+            for (int e = 0; e < EBATCH; ++e)
+                r[e] = load_stream16(base + (int64_t)(tid + NTE * (bt * EBATCH + e)) * 16);
+        } else {
+#pragma unroll
+            for (int e = 0; e < EBATCH; ++e)
+                r[e] = load_row_vec<DT>(base, tid + NTE * (bt * EBATCH + e), V);
+        }
+    };
+    auto proc_batch = [&](const uint4 (&r)[EBATCH], int bt) {
+        if (DT) {
+#pragma unroll
+            for (int e = 0; e < EBATCH; e += 2) {
+                const uint32_t lo = bf16x8_max_raw(r[e]);
+                const uint32_t hi = bf16x8_max_raw(r[e + 1]);
+                const int qi = (bt * EBATCH + e) / 2;
+                vm[qi] = __builtin_amdgcn_perm(hi, lo, 0x07060302u);
+                const rs_ushort2 cq = bf16x2_codes(vm[qi]);
+                p2 = __builtin_elementwise_max(p2, __builtin_elementwise_min(p1, cq));
+                p1 = __builtin_elementwise_max(p1, cq);
+            }
+        } else {
+#pragma unroll
+            for (int e = 0; e < EBATCH; ++e) {
+                const float mx = fmaxf(fmaxf(elem<DT>(r[e], 0), elem<DT>(r[e], 1)),
+                                       fmaxf(elem<DT>(r[e], 2), elem<DT>(r[e], 3)));
+                vm[bt * EBATCH + e] = __float_as_uint(mx);
+                const uint32_t cv = ord32(mx) >> 16;
+                c2 = max(c2, min(c1, cv));
+                c1 = max(c1, cv);
+            }
+        }
+    };
+    {
+        uint4 ra[EBATCH], rb[EBATCH];
+        load_batch(ra, 0);
+#pragma unroll
+        for (int bt = 0; bt < NB; bt += 2) {
+            load_batch(rb, bt + 1);
+            proc_batch(ra, bt);
+            if (bt + 2 < NB) load_batch(ra, bt + 2);
+            proc_batch(rb, bt + 1);
+        }
+    }
+    if (DT) {
+        c1 = max((uint32_t)p1.x, (uint32_t)p1.y);
+        c2 = max(min((uint32_t)p1.x, (uint32_t)p1.y), max((uint32_t)p2.x, (uint32_t)p2.y));
+    }
+
+    // ---- threshold: h = the nsel-th largest of the 2 * NTE offered codes,
+    //      by two 8-bit histogram passes (bins held by the first 256 threads) -
+    if (tid < 256) {
+        s_hist[tid] = 0u;
+        s_hist[256 + tid] = 0u;
+    }
+    __syncthreads();
+    atomicAdd(&s_hist[c1 >> 8], 1u);
+    atomicAdd(&s_hist[c2 >> 8], 1u);
+    __syncthreads();
+    int hn = 0, hincl = 0;
+    if (tid < 256) {
+        hn = (int)s_hist[255 - tid];
+        hincl = wave_excl_scan(hn) + hn;
+        if (lane == WAVE - 1) s_bc[0][wid] = hincl;
+    }
+    __syncthreads();
+    if (tid < 256) {
+#pragma unroll
+        for (int w = 0; w < 4; ++w) hincl += (w < wid) ? s_bc[0][w] : 0;
+        if (hincl >= nsel && hincl - hn < nsel) {
+            s_h = (uint32_t)(255 - tid);
+            s_above = hincl - hn;
+        }
+    }
+    __syncthreads();
+    const uint32_t hb = s_h;
+    if ((c1 >> 8) == hb) atomicAdd(&s_hist[256 + (c1 & 0xFFu)], 1u);
+    if ((c2 >> 8) == hb) atomicAdd(&s_hist[256 + (c2 & 0xFFu)], 1u);
+    __syncthreads();
+    if (tid < 256) {
+        hn = (int)s_hist[511 - tid];
+        hincl = wave_excl_scan(hn) + hn;
+        if (lane == WAVE - 1) s_bc[1][wid] = hincl;
+    }
+    __syncthreads();
+    if (tid < 256) {
+        hincl += s_above;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) hincl += (w < wid) ? s_bc[1][w] : 0;
+        if (hincl >= nsel && hincl - hn < nsel) s_h2 = (hb << 8) | (uint32_t)(255 - tid);
+    }
+    __syncthreads();
+    const uint32_t h = s_h2;
+    const float tau = (h << 16) > ord32(-INFINITY) ? unord32(h << 16) : -INFINITY;
+
+    // ---- candidate vectors (maximum >= tau): their indices, appended per wave
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+        const float vmax = DT ? ((q & 1) ? bf_hi(vm[q / 2]) : bf_lo(vm[q / 2]))
+                              : __uint_as_float(vm[q]);
+        const int vi = tid + NTE * q;
+        const bool take = vmax >= tau && vi < NVR;
+        const uint64_t msk = __ballot(take);
+        if (msk) {
+            int wb = 0;
+            if (lane == 0) wb = atomicAdd(&s_nv, (int)__popcll(msk));
+            wb = (int)lane_u32((uint32_t)wb, 0);
+            if (take) {
+                const int pos = wb + (int)__builtin_amdgcn_mbcnt_hi(
+                    (uint32_t)(msk >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)msk, 0u));
+                if (pos < CAPV) s_cvi[pos] = vi;
+            }
+        }
+    }
+    __syncthreads();
+    const int nv = s_nv;
+    // ---- their elements >= tau (one candidate vector per thread, read again)
+    if (nv <= CAPV) {
+        uint4 x = make_uint4(0, 0, 0, 0);
+        int e0 = V;
+        if (tid < nv) {
+            const int vi = s_cvi[tid];
+            x = load_row_vec<DT>(base, vi, V);
+            e0 = vi * VEC;
+        }
+        int n = 0;
+#pragma unroll
+        for (int k = 0; k < VEC; ++k) n += (elem<DT>(x, k) >= tau) & (e0 + k < V);
+        const int excl = wave_excl_scan(n);
+        int cb = 0;
+        if (lane == WAVE - 1) cb = atomicAdd(&s_cnt, excl + n);
+        int pos = (int)lane_u32((uint32_t)cb, WAVE - 1) + excl;
+#pragma unroll
+        for (int k = 0; k < VEC; ++k) {
+            const float v = elem<DT>(x, k);
+            if (v >= tau && e0 + k < V) {
+                if (pos < CAPC) s_keys[pos] = logit_key(v, (uint32_t)(e0 + k));
+                ++pos;
+            }
+        }
+    } else if (tid == 0) {
+        s_cnt = CAPC + 1;                        // too many: exact fallback below
+    }
+    __syncthreads();
+    int cnt = s_cnt;
+    if (cnt > CAPC) {
+        __syncthreads();
+        if (tid == 0) s_cnt = 0;
+        exact_select_fallback<DT, NTE, NQ>(
+            base, V, 0, h, nsel, CAPC,
+            [&](float v, int id) {
+                const int pos = atomicAdd(&s_cnt, 1);
+                if (pos < CAPC) s_keys[pos] = logit_key(v, (uint32_t)id);
+            },
+            s_redi, s_tie);
+        cnt = min(s_cnt, CAPC);
+    }
+
+    // ---- the support: the top nsel candidates in (logit desc, id asc) order
+    rank_keys<NTE>(s_keys, cnt, s_rank);
+    __syncthreads();
+    for (int i = tid; i < cnt; i += NTE) {
+        const int rk = s_rank[i];
+        if (rk < nsel) s_top[rk] = s_keys[i];
+    }
+    __syncthreads();
+    for (int i = tid; i < S; i += NTE) {
+        if ((uint32_t)key_id(s_top[i]) >= (uint32_t)V) {   // a support slot left empty
+            atomicOr(t.err, 256);
+            s_top[i] = logit_key(-INFINITY, 0u);
+        }
+    }
+    const ParentRec pr = (tid < K) ? parent_rec(t, level, nb, s_pu) : ParentRec{1.0, 0ull};
+    __syncthreads();
+
+    pool_form<NTE>(t, a, row, s_pdyn, L, s_pu, pr, s_u, s_red, &s_yi);
+    if (level + 1 >= t.D) return;
+    select_frontier(t, a, b, s_top, s_k2);
 }
 
 // Four blocks per CU keep enough loads in flight; the largest chunk variant
@@ -913,5 +1186,30 @@ hipError_t launch_expand(const TreeDev& t, const LevelArgs& a, int variant, hipS
 }
 
 int expand_variant_nvc(int v) { return kNVC[v]; }
+
+// Vectors per thread k_expand_row needs for a row of V elements (16 or 32),
+// or 0 if the row is too long for it.
+int expand_row_nq(int dtype, int V) {
+    const int nvr = (V + (dtype ? 8 : 4) - 1) / (dtype ? 8 : 4);
+    if (nvr <= NTE * 16) return 16;
+    if (nvr <= NTE * 32) return 32;
+    return 0;
+}
+
+hipError_t launch_expand_row(const TreeDev& t, const LevelArgs& a, hipStream_t s) {
+    const int nq = expand_row_nq(t.dtype, t.V);
+    const dim3 grid(t.B * a.P);
+    const size_t shm = (size_t)pool_lds(t.S, 0).bytes;
+    if (t.dtype) {
+        if (nq == 16) k_expand_row<1, 16><<<grid, NTE, shm, s>>>(t, a);
+        else if (nq == 32) k_expand_row<1, 32><<<grid, NTE, shm, s>>>(t, a);
+        else return hipErrorInvalidValue;
+    } else {
+        if (nq == 16) k_expand_row<0, 16><<<grid, NTE, shm, s>>>(t, a);
+        else if (nq == 32) k_expand_row<0, 32><<<grid, NTE, shm, s>>>(t, a);
+        else return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
 
 }  // namespace rheo

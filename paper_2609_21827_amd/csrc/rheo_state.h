@@ -102,6 +102,8 @@ struct ExpandVariant {
     int Sc;                        // selection keys kept per chunk
     bool ok;                       // the row's C * Sc keys fit the merge
 };
+hipError_t launch_expand_row(const TreeDev& t, const LevelArgs& a, hipStream_t s);
+int expand_row_nq(int dtype, int V);
 int expand_variant_count(int dtype);
 int expand_variant_nvc(int v);
 ExpandVariant expand_variant(int dtype, int v, int V, int S);

@@ -54,10 +54,15 @@ def _check_seq(w, tree_nodes, ppar, ptok, acc, alen, fin, b, step, T):
     assert int(fin[b]) == ou
 
 
-def run_parity(w, steps, seqs, T=None, dev="cuda", tree_kw=None):
+def run_parity(w, steps, seqs, T=None, dev="cuda", tree_kw=None, env=None):
     from paper_2609_21827_amd.driver import make_tree, run_step
     T = w.T if T is None else T
-    tree = make_tree(w, device=dev, **(tree_kw or {}))
+    os.environ.update(env or {})
+    try:
+        tree = make_tree(w, device=dev, **(tree_kw or {}))
+    finally:
+        for k in env or {}:
+            del os.environ[k]
     try:
         for step in steps:
             print(f"gpu step {w.name} step={step} T={T}", flush=True)
@@ -103,12 +108,15 @@ def test_tiny_variants(dev, over):
     dict(V=128256, dtype="bf16", recipe="zipf", support=512, K=8, depth=2, R=10),
     dict(V=70001, dtype="bf16", recipe="zipf", quantum=2.0, support=128, K=4, depth=2, R=6),
 ])
-def test_edge_shapes(dev, over):
+@pytest.mark.parametrize("row", ["auto", "1"])
+def test_edge_shapes(dev, over, row):
+    """row "1": every sparse level on the one-block-per-row kernel."""
     w = W["tiny"].with_(name="edge", sigma=1.5, sigma_t=0.8, **over)
     tree_kw = {}
     if w.V % 8:
         tree_kw["row_stride"] = (w.V + 7) // 8 * 8
-    run_parity(w, range(3), list(range(w.B)), dev=dev, tree_kw=tree_kw)
+    env = {"RHEO_EXPAND_ROW": row} if row != "auto" else None
+    run_parity(w, range(3), list(range(w.B)), dev=dev, tree_kw=tree_kw, env=env)
 
 
 def test_llama2(dev):
@@ -132,17 +140,30 @@ def test_headline(dev):
     run_parity(W["headline"], [0, 1], [0, 31, 63], dev=dev)
 
 
-def test_launch_shape_independence(dev):
-    """Results do not depend on the expand chunk size or verification team size."""
+SHAPES = (
+    {},
+    {"RHEO_EXPAND_VARIANT": "0", "RHEO_VERIFY_BLOCKS": "4"},
+    {"RHEO_EXPAND_VARIANT": "3", "RHEO_VERIFY_BLOCKS": "64"},
+    {"RHEO_EXPAND_VARIANT": "1", "RHEO_VERIFY_BLOCKS": "1024"},
+    {"RHEO_EXPAND_ROW": "1"},
+    {"RHEO_EXPAND_ROW": "0", "RHEO_VERIFY_BLOCKS": "256"},
+)
+
+
+@pytest.mark.parametrize("wl", ["llama3", "llama2", "quantum_bf16"])
+def test_launch_shape_independence(dev, wl):
+    """Results do not depend on the expand kernels (chunk size, one block per
+    row) or the verification team size."""
     from paper_2609_21827_amd.driver import make_tree, run_step
-    w = W["llama3"].with_(B=4)
+    if wl == "llama3":
+        w = W["llama3"].with_(B=4)
+    elif wl == "llama2":
+        w = W["llama2"].with_(B=2, depth=4, R=30)
+    else:   # massive ties: the exact fallbacks of both selection kernels
+        w = W["llama3"].with_(name="quantum_bf16", B=2, depth=3, R=20, recipe="zipf",
+                              quantum=2.0)
     outs = []
-    for variant, vblocks in ((None, None), ("0", "4"), ("3", "64"), ("1", "1024")):
-        env = {}
-        if variant:
-            env["RHEO_EXPAND_VARIANT"] = variant
-        if vblocks:
-            env["RHEO_VERIFY_BLOCKS"] = vblocks
+    for env in SHAPES:
         os.environ.update(env)
         try:
             tree = make_tree(w, device=dev)
