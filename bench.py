@@ -67,7 +67,7 @@ def _counter_rows(path, regex, counter):
 
 
 def expand_kernel_name(w):
-    return ("expand level (k_expand_row; k_select + k_pool below 128 rows)" if w.support > 0
+    return ("expand level (k_expand_row; k_select + k_pool below 64 rows)" if w.support > 0
             else "expand level (k_select + k_dweights + k_dpool)")
 
 

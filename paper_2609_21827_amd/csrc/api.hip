@@ -39,7 +39,7 @@ float k_of_T(float T) { return (float)(1.4426950408889634 / (double)T); }
 
 // tokens of one 64-vector sub-chunk (16-byte vectors of bf16 or fp32)
 // Rows in a level from which one block per row fills the chip.
-constexpr int kRowMin = 128;
+constexpr int kRowMin = 64;
 
 int WAVE_TOKENS(int dtype) { return 64 * (dtype == RHEO_BF16 ? 8 : 4); }
 

@@ -128,48 +128,65 @@ __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, 
     const int NE = t.NE;
     const int64_t nb = (int64_t)b * t.NN;
 
-    // construction weights (untempered unless asked), S1, rank by (w1 desc, id asc)
+    // Construction weights w1 (untempered unless asked) and, taking the rank
+    // by (w1 desc, id asc) to be the support order, the tail weights of q~_T
+    // relative to x_{m+1} = s_top[m], both totals in one exchange, and the
+    // tail's id keys.  The support is in (logit desc, id asc) order and the
+    // weight never grows along it, so the rank differs from the position
+    // only where two different logits share a weight: then the ranks and
+    // the tail are computed again.
     const int cb = (level == 0) ? 1 : 1 + K + (level - 1) * NE * K;
     const int e_idx = (level == 0) ? 0 : 1 + (level - 1) * NE + j;
     const float M = key_value(s_top[0]);
-    uint64_t part = 0;
+    const float ref0 = key_value(s_top[m]);
+    uint64_t part1 = 0, partq = 0;
     for (int i = tid; i < S; i += NT) {
         const uint64_t tk = s_top[i];
-        const uint32_t w = cweight(key_value(tk), M, a.k1);
+        const float v = key_value(tk);
+        const uint32_t w = cweight(v, M, a.k1);
         s_w1[i] = w;
-        s_k2[i] = ((uint64_t)w << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)key_id(tk));
-        part += w;
+        part1 += w;
+        const bool tail = i >= m;
+        const uint32_t q = tail ? cweight(v, ref0, a.kT) : 0u;
+        s_q[i] = q;
+        partq += q;
+        s_k2[i] = tail ? (uint64_t)(0xFFFFFFFFu - (uint32_t)key_id(tk)) + 1 : 0ull;
     }
-    const uint64_t S1 = psum<NT>(part, s_red);
+    uint64_t S1, Zq;
+    psum2<NT>(part1, partq, s_red, &S1, &Zq);
     psync<NT>();
-    // The support is in (logit desc, id asc) order and the weight never
-    // grows along it, so ranks by (w1 desc, id asc) differ from positions
-    // only where two different logits share a weight.
     bool tie = false;
     for (int i = tid + 1; i < S; i += NT)
         tie |= s_w1[i] == s_w1[i - 1] && (s_top[i] >> 32) != (s_top[i - 1] >> 32);
     if (pany<NT>(tie)) {
+        for (int i = tid; i < S; i += NT)
+            s_k2[i] = ((uint64_t)s_w1[i] << 32) |
+                      (uint64_t)(0xFFFFFFFFu - (uint32_t)key_id(s_top[i]));
+        psync<NT>();
         rank_all<NT>(s_k2, S, s_wr);
+        psync<NT>();
+        for (int i = tid; i < S; i += NT) s_xs[s_wr[i]] = (int16_t)i;
+        psync<NT>();
+        const float ref_t = key_value(s_top[s_xs[m]]);
+        partq = 0;
+        for (int i = tid; i < S; i += NT) {
+            const bool tail = s_wr[i] >= m;
+            const uint64_t tk = s_top[i];
+            const uint32_t q = tail ? cweight(key_value(tk), ref_t, a.kT) : 0u;
+            s_q[i] = q;
+            partq += q;
+            s_k2[i] = tail ? (uint64_t)(0xFFFFFFFFu - (uint32_t)key_id(tk)) + 1 : 0ull;
+        }
+        Zq = psum<NT>(partq, s_red);
+        psync<NT>();
     } else {
-        for (int i = tid; i < S; i += NT) s_wr[i] = (int16_t)i;
+        for (int i = tid; i < S; i += NT) {
+            s_wr[i] = (int16_t)i;
+            s_xs[i] = (int16_t)i;
+        }
+        psync<NT>();
     }
-    psync<NT>();
-    for (int i = tid; i < S; i += NT) s_xs[s_wr[i]] = (int16_t)i;
-    psync<NT>();
-
-    // tail q~_T (relative to x_{m+1}), its total, and its order by token id
-    const float ref_t = key_value(s_top[s_xs[m]]);
-    part = 0;
-    for (int i = tid; i < S; i += NT) {
-        const bool tail = s_wr[i] >= m;
-        const uint64_t tk = s_top[i];
-        const uint32_t w = tail ? cweight(key_value(tk), ref_t, a.kT) : 0u;
-        s_q[i] = w;
-        part += w;
-        s_k2[i] = tail ? (uint64_t)(0xFFFFFFFFu - (uint32_t)key_id(tk)) + 1 : 0ull;
-    }
-    const uint64_t Zq = psum<NT>(part, s_red);
-    psync<NT>();
+    // the tail's order by token id
     rank_all<NT>(s_k2, S, s_ir);
     psync<NT>();
     // id-sorted tail, written straight to the tree (q~ for verification)
@@ -288,7 +305,7 @@ __device__ __forceinline__ void row_parent(const TreeDev& t, const LevelArgs& a,
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(NTP) void k_pool(TreeDev t, LevelArgs a) {
     extern __shared__ __align__(16) uint8_t s_pdyn[];
-    __shared__ uint64_t s_red[NTP / WAVE];
+    __shared__ uint64_t s_red[2 * NTP / WAVE];
     __shared__ int s_pu, s_yi;
     __shared__ uint64_t s_u;
     const PoolLds L = pool_lds(t.S, t.C);
@@ -456,6 +473,44 @@ __device__ void rank_keys32(const uint32_t* keys, int n, int16_t* rank) {
         for (int o = 1; o < F; o <<= 1) cnt += __shfl_xor(cnt, o);
         if (i < n && sub == 0) rank[i] = (int16_t)cnt;
     }
+}
+
+// h = the largest 16-bit code that at least nsel of the 2 * NT offered codes
+// (c1 and c2 of every thread) reach, four bits per round: each wave counts
+// its offers >= h | d << sh for d = 1..15 with ballots, lane d of the wave
+// stores that count, the waves' counts are added, and d is the largest one
+// whose count still reaches nsel.  s_cnt holds 2 * (NT / WAVE) * 16 ints.
+// Needs nsel <= 2 * NT; all threads of the block call it.
+template <int NT>
+__device__ __forceinline__ uint32_t offer_threshold(uint32_t c1, uint32_t c2, int nsel,
+                                                    int* s_cnt) {
+    constexpr int NW = NT / WAVE;
+    const int lane = threadIdx.x % WAVE, wid = threadIdx.x / WAVE;
+    uint32_t h = 0;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int sh = 12 - 4 * r;
+        int* buf = s_cnt + (r & 1) * NW * 16;
+        uint32_t mine = 0;
+#pragma unroll
+        for (int d = 1; d < 16; ++d) {
+            const uint32_t cand = h | ((uint32_t)d << sh);
+            const uint32_t n = (uint32_t)(__popcll(__ballot(c1 >= cand)) +
+                                          __popcll(__ballot(c2 >= cand)));
+            mine = (lane == d) ? n : mine;
+        }
+        if (lane < 16) buf[wid * 16 + lane] = (int)mine;
+        __syncthreads();
+        int tot = 0;
+        if (lane < 16) {
+#pragma unroll
+            for (int w = 0; w < NW; ++w) tot += buf[w * 16 + lane];
+        }
+        const uint64_t ok = __ballot(lane >= 1 && lane < 16 && tot >= nsel);
+        const uint32_t d = ok ? (uint32_t)(63 - __builtin_clzll(ok)) : 0u;
+        h |= d << sh;
+    }
+    return h;
 }
 
 // Exact selection for a degenerate range: more candidates than LDS holds
@@ -627,11 +682,10 @@ __device__ __forceinline__ void select_block(const TreeDev& t, const LevelArgs& 
     __shared__ uint4 s_cv[CAPV];                 // candidate vectors, WCAP per wave
     __shared__ int16_t s_rank[CAPC];
     __shared__ int s_cvi[CAPV];                  // their vector indices
-    __shared__ uint32_t s_hist[2 * NTC];         // threshold histograms
+    __shared__ int s_thr[2 * NW * 16];          // threshold counts
     __shared__ int s_bc[2][NW];
     __shared__ int s_wn[NW];
-    __shared__ uint32_t s_h, s_h2;
-    __shared__ int s_above, s_cnt;
+    __shared__ int s_cnt;
     __shared__ int s_redi[NW];
     uint32_t* s_k32 = (uint32_t*)s_keys;
 
@@ -693,47 +747,15 @@ __device__ __forceinline__ void select_block(const TreeDev& t, const LevelArgs& 
     // thread offers the order codes of its two largest vector maxima; h =
     // the nsel-th largest offered code gives tau = the smallest value with
     // code h (each offered maximum is a distinct vector holding an element
-    // >= tau).  h comes from two 8-bit histogram passes over the 2 * NTC
-    // offers (high byte, then low byte inside the bin that holds the nsel-th
-    // offer), one bin per thread.  Elements past the row end read as -inf
+    // >= tau), found four bits at a time (offer_threshold).  Elements past
+    // the row end read as -inf
     // (fp32) or the lowest finite bf16, so tau may fall to that value: then
     // every element of the chunk is a candidate.  Supports larger than the
     // offers use all vector maxima.
     static_assert(NTC == 256, "one histogram bin per thread");
     uint32_t h = 0;
     if (nsel <= 2 * NTC) {
-        s_hist[tid] = 0u;
-        s_hist[NTC + tid] = 0u;
-        __syncthreads();
-        atomicAdd(&s_hist[c1 >> 8], 1u);
-        atomicAdd(&s_hist[c2 >> 8], 1u);
-        __syncthreads();
-        // thread tid holds bin NTC-1-tid: inclusive prefix = offers in bins >= it
-        int n = (int)s_hist[NTC - 1 - tid];
-        int incl = wave_excl_scan(n) + n;
-        if (lane == WAVE - 1) s_bc[0][wid] = incl;
-        __syncthreads();
-#pragma unroll
-        for (int w = 0; w < NW; ++w) incl += (w < wid) ? s_bc[0][w] : 0;
-        if (incl >= nsel && incl - n < nsel) {
-            s_h = (uint32_t)(NTC - 1 - tid);
-            s_above = incl - n;
-        }
-        __syncthreads();
-        const uint32_t hb = s_h;
-        if ((c1 >> 8) == hb) atomicAdd(&s_hist[NTC + (c1 & 0xFFu)], 1u);
-        if ((c2 >> 8) == hb) atomicAdd(&s_hist[NTC + (c2 & 0xFFu)], 1u);
-        __syncthreads();
-        n = (int)s_hist[2 * NTC - 1 - tid];
-        incl = wave_excl_scan(n) + n;
-        if (lane == WAVE - 1) s_bc[1][wid] = incl;
-        __syncthreads();
-        incl += s_above;
-#pragma unroll
-        for (int w = 0; w < NW; ++w) incl += (w < wid) ? s_bc[1][w] : 0;
-        if (incl >= nsel && incl - n < nsel) s_h2 = (hb << 8) | (uint32_t)(NTC - 1 - tid);
-        __syncthreads();
-        h = s_h2;
+        h = offer_threshold<NTC>(c1, c2, nsel, s_thr);
     } else {
 #pragma unroll 1
         for (int bit = 15; bit >= 0; --bit) {
@@ -913,11 +935,10 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
     __shared__ __align__(16) uint64_t s_keys[CAPC];
     __shared__ int16_t s_rank[CAPC];
     __shared__ int s_cvi[CAPV];
-    __shared__ uint32_t s_hist[512];
-    __shared__ int s_bc[2][4];
-    __shared__ uint32_t s_h, s_h2;
-    __shared__ int s_above, s_cnt, s_nv;
-    __shared__ uint64_t s_red[NW];
+    __shared__ int s_thr[2 * NW * 16];
+    __shared__ int s_wn[NW];
+    __shared__ int s_cnt;
+    __shared__ uint64_t s_red[2 * NW];
     __shared__ int s_redi[NW];
     __shared__ int s_tie[32][NW];
     __shared__ int s_pu, s_yi;
@@ -940,7 +961,6 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
     if (tid == 0) {
         row_parent(t, a, b, j, &s_pu, &s_u);
         s_cnt = 0;
-        s_nv = 0;
     }
     for (int i = tid; i < S; i += NTE) s_top[i] = 0ull;   // id -1 until ranked
 
@@ -1001,79 +1021,79 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
         c2 = max(min((uint32_t)p1.x, (uint32_t)p1.y), max((uint32_t)p2.x, (uint32_t)p2.y));
     }
 
-    // ---- threshold: h = the nsel-th largest of the 2 * NTE offered codes,
-    //      by two 8-bit histogram passes (bins held by the first 256 threads) -
-    if (tid < 256) {
-        s_hist[tid] = 0u;
-        s_hist[256 + tid] = 0u;
-    }
-    __syncthreads();
-    atomicAdd(&s_hist[c1 >> 8], 1u);
-    atomicAdd(&s_hist[c2 >> 8], 1u);
-    __syncthreads();
-    int hn = 0, hincl = 0;
-    if (tid < 256) {
-        hn = (int)s_hist[255 - tid];
-        hincl = wave_excl_scan(hn) + hn;
-        if (lane == WAVE - 1) s_bc[0][wid] = hincl;
-    }
-    __syncthreads();
-    if (tid < 256) {
-#pragma unroll
-        for (int w = 0; w < 4; ++w) hincl += (w < wid) ? s_bc[0][w] : 0;
-        if (hincl >= nsel && hincl - hn < nsel) {
-            s_h = (uint32_t)(255 - tid);
-            s_above = hincl - hn;
-        }
-    }
-    __syncthreads();
-    const uint32_t hb = s_h;
-    if ((c1 >> 8) == hb) atomicAdd(&s_hist[256 + (c1 & 0xFFu)], 1u);
-    if ((c2 >> 8) == hb) atomicAdd(&s_hist[256 + (c2 & 0xFFu)], 1u);
-    __syncthreads();
-    if (tid < 256) {
-        hn = (int)s_hist[511 - tid];
-        hincl = wave_excl_scan(hn) + hn;
-        if (lane == WAVE - 1) s_bc[1][wid] = hincl;
-    }
-    __syncthreads();
-    if (tid < 256) {
-        hincl += s_above;
-#pragma unroll
-        for (int w = 0; w < 4; ++w) hincl += (w < wid) ? s_bc[1][w] : 0;
-        if (hincl >= nsel && hincl - hn < nsel) s_h2 = (hb << 8) | (uint32_t)(255 - tid);
-    }
-    __syncthreads();
-    const uint32_t h = s_h2;
+    // ---- threshold: h = the nsel-th largest of the 2 * NTE offered codes
+    const uint32_t h = offer_threshold<NTE>(c1, c2, nsel, s_thr);
+    // the parent record, for the children written at the end
+    const ParentRec pr = (tid < K) ? parent_rec(t, level, nb, s_pu) : ParentRec{1.0, 0ull};
     const float tau = (h << 16) > ord32(-INFINITY) ? unord32(h << 16) : -INFINITY;
 
-    // ---- candidate vectors (maximum >= tau): their indices, appended per wave
+    // ---- candidate vectors (maximum >= tau): every wave appends the indices
+    //      of its own to its region of s_cvi; if a wave has more than its
+    //      region holds, but all fit, they are written again into one list
+    //      with slots reserved per wave
+    constexpr int WCAPR = CAPV / NW;
+    auto vmax_of = [&](int q) -> float {
+        return DT ? ((q & 1) ? bf_hi(vm[q / 2]) : bf_lo(vm[q / 2])) : __uint_as_float(vm[q]);
+    };
+    {
+        int wpos = 0;
 #pragma unroll
-    for (int q = 0; q < NQ; ++q) {
-        const float vmax = DT ? ((q & 1) ? bf_hi(vm[q / 2]) : bf_lo(vm[q / 2]))
-                              : __uint_as_float(vm[q]);
-        const int vi = tid + NTE * q;
-        const bool take = vmax >= tau && vi < NVR;
-        const uint64_t msk = __ballot(take);
-        if (msk) {
-            int wb = 0;
-            if (lane == 0) wb = atomicAdd(&s_nv, (int)__popcll(msk));
-            wb = (int)lane_u32((uint32_t)wb, 0);
+        for (int q = 0; q < NQ; ++q) {
+            const int vi = tid + NTE * q;
+            const bool take = vmax_of(q) >= tau && vi < NVR;
+            const uint64_t msk = __ballot(take);
             if (take) {
-                const int pos = wb + (int)__builtin_amdgcn_mbcnt_hi(
+                const int pos = wpos + (int)__builtin_amdgcn_mbcnt_hi(
                     (uint32_t)(msk >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)msk, 0u));
-                if (pos < CAPV) s_cvi[pos] = vi;
+                if (pos < WCAPR) s_cvi[wid * WCAPR + pos] = vi;
             }
+            wpos += __popcll(msk);
         }
+        if (lane == 0) s_wn[wid] = wpos;
     }
     __syncthreads();
-    const int nv = s_nv;
+    int wn[NW], nv = 0, wbefore = 0;
+    bool ovf = false;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+        wn[w] = s_wn[w];
+        ovf |= wn[w] > WCAPR;
+        wbefore += (w < wid) ? wn[w] : 0;
+        nv += wn[w];
+    }
+    const bool contig = ovf && nv <= CAPV;
+    if (contig) {
+        int wpos = wbefore;
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+            const int vi = tid + NTE * q;
+            const bool take = vmax_of(q) >= tau && vi < NVR;
+            const uint64_t msk = __ballot(take);
+            if (take) {
+                const int pos = wpos + (int)__builtin_amdgcn_mbcnt_hi(
+                    (uint32_t)(msk >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)msk, 0u));
+                s_cvi[pos] = vi;
+            }
+            wpos += __popcll(msk);
+        }
+        __syncthreads();
+    }
     // ---- their elements >= tau (one candidate vector per thread, read again)
-    if (nv <= CAPV) {
+    if (!ovf || contig) {
         uint4 x = make_uint4(0, 0, 0, 0);
         int e0 = V;
         if (tid < nv) {
-            const int vi = s_cvi[tid];
+            // entry tid of the concatenated regions (or of the one list)
+            int w = 0, off = tid;
+            if (!contig) {
+#pragma unroll
+                for (int q = 0; q < NW - 1; ++q) {
+                    const bool past = off >= wn[q] && w == q;
+                    off -= past ? wn[q] : 0;
+                    w += past ? 1 : 0;
+                }
+            }
+            const int vi = s_cvi[w * WCAPR + off];
             x = load_row_vec<DT>(base, vi, V);
             e0 = vi * VEC;
         }
@@ -1124,7 +1144,6 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
             s_top[i] = logit_key(-INFINITY, 0u);
         }
     }
-    const ParentRec pr = (tid < K) ? parent_rec(t, level, nb, s_pu) : ParentRec{1.0, 0ull};
     __syncthreads();
 
     pool_form<NTE>(t, a, row, s_pdyn, L, s_pu, pr, s_u, s_red, &s_yi);

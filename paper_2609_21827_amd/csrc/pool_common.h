@@ -77,6 +77,16 @@ __device__ __forceinline__ uint64_t psum(uint64_t v, uint64_t* sh) {
     return block_sum_u64<NT>(v, sh);
 }
 template <int NT>
+__device__ __forceinline__ void psum2(uint64_t a, uint64_t b, uint64_t* sh, uint64_t* ra,
+                                      uint64_t* rb) {
+    if (NT == WAVE) {
+        *ra = wave_sum_u64(a);
+        *rb = wave_sum_u64(b);
+    } else {
+        block_sum2_u64<NT>(a, b, sh, ra, rb);
+    }
+}
+template <int NT>
 __device__ __forceinline__ bool pany(bool p) {
     if (NT == WAVE) return __ballot(p) != 0ull;
     return __syncthreads_or(p) != 0;

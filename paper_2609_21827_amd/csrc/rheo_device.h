@@ -194,6 +194,29 @@ __device__ uint64_t block_sum_u64(uint64_t v, uint64_t* sh) {
     return r;
 }
 
+// Two block sums in one exchange; sh holds 2 * NT / WAVE words.
+template <int NT>
+__device__ void block_sum2_u64(uint64_t a, uint64_t b, uint64_t* sh, uint64_t* ra, uint64_t* rb) {
+    constexpr int NW = NT / WAVE;
+    a = wave_sum_u64(a);
+    b = wave_sum_u64(b);
+    const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE;
+    __syncthreads();
+    if (l == 0) {
+        sh[w] = a;
+        sh[NW + w] = b;
+    }
+    __syncthreads();
+    uint64_t x = 0, y = 0;
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+        x += sh[i];
+        y += sh[NW + i];
+    }
+    *ra = x;
+    *rb = y;
+}
+
 template <int NT>
 __device__ int block_sum_i32(int v, int* sh) {
     v = wave_sum_i32(v);
