@@ -103,9 +103,9 @@ __host__ __device__ inline PoolLds pool_lds(int S, int C) {
     return L;
 }
 
-// The pool of one row from its merged support s_top (App. C.1), formed by
-// NT threads (tid < NT).  Children fields the frontier selection reads in
-// other blocks (token, score, path) are published with agent-scope atomics.
+// The pool of one row from its support s_top (App. C.1), formed by NT
+// threads (tid < NT).  Children fields the frontier selection reads in other
+// blocks (token, score, path) are published with agent-scope atomics.
 template <int NT>
 __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, int row,
                                           uint8_t* lds, const PoolLds& L, int pu,
@@ -115,11 +115,8 @@ __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, 
     uint64_t* s_k2 = (uint64_t*)(lds + L.k2);
     uint32_t* s_w1 = (uint32_t*)(lds + L.w1);
     uint32_t* s_q = (uint32_t*)(lds + L.q);
-    uint32_t* s_tq = (uint32_t*)(lds + L.tq);
     int16_t* s_wr = (int16_t*)(lds + L.wr);
     int16_t* s_xs = (int16_t*)(lds + L.xs);
-    int16_t* s_ir = (int16_t*)(lds + L.ir);
-    int16_t* s_tx = (int16_t*)(lds + L.tx);
     const int tid = threadIdx.x;
     const int b = row / a.P;
     const int j = row % a.P;
@@ -127,16 +124,17 @@ __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, 
     const int level = a.level;
     const int NE = t.NE;
     const int64_t nb = (int64_t)b * t.NN;
+    const int cb = (level == 0) ? 1 : 1 + K + (level - 1) * NE * K;
+    const int e_idx = (level == 0) ? 0 : 1 + (level - 1) * NE + j;
+    if (tid == 0) *s_yi = -1;
 
     // Construction weights w1 (untempered unless asked) and, taking the rank
     // by (w1 desc, id asc) to be the support order, the tail weights of q~_T
     // relative to x_{m+1} = s_top[m], both totals in one exchange, and the
-    // tail's id keys.  The support is in (logit desc, id asc) order and the
-    // weight never grows along it, so the rank differs from the position
-    // only where two different logits share a weight: then the ranks and
-    // the tail are computed again.
-    const int cb = (level == 0) ? 1 : 1 + K + (level - 1) * NE * K;
-    const int e_idx = (level == 0) ? 0 : 1 + (level - 1) * NE + j;
+    // tail's id keys (larger key = smaller id; 0 off the tail).  The support
+    // is in (logit desc, id asc) order and the weight never grows along it,
+    // so the rank differs from the position only where two different logits
+    // share a weight: then the ranks and the tail are computed again.
     const float M = key_value(s_top[0]);
     const float ref0 = key_value(s_top[m]);
     uint64_t part1 = 0, partq = 0;
@@ -154,11 +152,12 @@ __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, 
     }
     uint64_t S1, Zq;
     psum2<NT>(part1, partq, s_red, &S1, &Zq);
-    psync<NT>();
+    if (NT == WAVE) wave_sync();             // (a block sum has synchronised)
     bool tie = false;
     for (int i = tid + 1; i < S; i += NT)
         tie |= s_w1[i] == s_w1[i - 1] && (s_top[i] >> 32) != (s_top[i - 1] >> 32);
-    if (pany<NT>(tie)) {
+    const bool ident = !pany<NT>(tie);
+    if (!ident) {
         for (int i = tid; i < S; i += NT)
             s_k2[i] = ((uint64_t)s_w1[i] << 32) |
                       (uint64_t)(0xFFFFFFFFu - (uint32_t)key_id(s_top[i]));
@@ -178,61 +177,31 @@ __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, 
             s_k2[i] = tail ? (uint64_t)(0xFFFFFFFFu - (uint32_t)key_id(tk)) + 1 : 0ull;
         }
         Zq = psum<NT>(partq, s_red);
-        psync<NT>();
-    } else {
-        for (int i = tid; i < S; i += NT) {
-            s_wr[i] = (int16_t)i;
-            s_xs[i] = (int16_t)i;
-        }
-        psync<NT>();
     }
-    // the tail's order by token id
-    rank_all<NT>(s_k2, S, s_ir);
-    psync<NT>();
-    // id-sorted tail, written straight to the tree (q~ for verification)
-    const int ntail = S - m;
-    const int64_t tail_base = ((int64_t)b * t.E + e_idx) * S;
-    for (int i = tid; i < S; i += NT) {
-        if (s_wr[i] >= m) {
-            const int idr = s_ir[i];
-            s_tq[idr] = s_q[i];
-            s_tx[idr] = (int16_t)i;
-            t.tail_id[tail_base + idr] = key_id(s_top[i]);
-            t.tail_q[tail_base + idr] = s_q[i];
-        }
-    }
-    if (tid == 0) *s_yi = -1;
-    psync<NT>();
+    // position in the support of rank r, and rank of position i
+    auto xs = [&](int r) -> int { return ident ? r : (int)s_xs[r]; };
+    auto wr = [&](int i) -> int { return ident ? i : (int)s_wr[i]; };
 
-    // Y ~ q~_T: t = floor(U64 Zq / 2^64), the first id-ordered tail entry
-    // whose inclusive prefix exceeds t (each thread scans a contiguous block)
+    // The tail in token-id order: every tail entry's place among the tail
+    // ids and the q~ mass of the entries before it.  The tail is written to
+    // the tree in that order (q~ for verification), and Y ~ q~_T is the
+    // entry whose interval [mass before, mass before + q) holds
+    // t = floor(U64 Zq / 2^64): the inverse CDF over token ids.
     const uint64_t tt = __umul64hi(u, Zq);
-    const int IPT = (ntail + NT - 1) / NT;
-    const int lo = min(ntail, tid * IPT), hi = min(ntail, lo + IPT);
-    uint64_t mysum = 0;
-    for (int i = lo; i < hi; ++i) mysum += s_tq[i];
-    uint64_t acc;
-    if (NT == WAVE) {
-        acc = wave_incl_scan_u64(mysum) - mysum;
-    } else {
-        uint64_t total;
-        acc = block_excl_scan_u64<NT>(mysum, s_red, &total);
-    }
-    if (acc <= tt && tt < acc + mysum) {
-        for (int i = lo; i < hi; ++i) {
-            const uint64_t w = s_tq[i];
-            if (tt < acc + w) {
-                *s_yi = s_tx[i];
-                break;
-            }
-            acc += w;
+    const int64_t tail_base = ((int64_t)b * t.E + e_idx) * S;
+    rank_prefix<NT>(s_k2, s_q, S, [&](int i, int ir, uint64_t pre) {
+        if (s_k2[i] != 0ull) {
+            const uint32_t q = s_q[i];
+            t.tail_id[tail_base + ir] = key_id(s_top[i]);
+            t.tail_q[tail_base + ir] = q;
+            if (pre <= tt && tt - pre < (uint64_t)q) *s_yi = i;
         }
-    }
+    });
     psync<NT>();
     int yi = *s_yi;
     if (yi < 0) {
         if (tid == 0) atomicOr(t.err, 1);
-        yi = s_xs[m];                            // unreachable fallback
+        yi = xs(m);                              // unreachable fallback
     }
 
     if (tid == 0) {
@@ -244,10 +213,10 @@ __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, 
     // the K children: top-m leads, Y, fills (App. C.1)
     if (tid < K) {
         const int s = tid;
-        const int yr = s_wr[yi];
+        const int yr = wr(yi);
         int item, kind;
         if (s < m) {
-            item = s_xs[s];
+            item = xs(s);
             kind = LEAD;
         } else if (s == m) {
             item = yi;
@@ -255,7 +224,7 @@ __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, 
         } else {
             const int f = s - m - 1;
             const int rk = m + f + ((m + f) >= yr ? 1 : 0);
-            item = s_xs[rk];
+            item = xs(rk);
             kind = FILL;
         }
         double proxy;
@@ -263,12 +232,12 @@ __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, 
         if (kind == SAMPLED) {
             if (m >= 1) {
                 uint64_t lead = 0;
-                for (int q2 = 0; q2 < m; ++q2) lead += s_w1[s_xs[q2]];
+                for (int q2 = 0; q2 < m; ++q2) lead += s_w1[xs(q2)];
                 const uint64_t z = S1 - lead;
-                const uint64_t wm = s_w1[s_xs[m - 1]];
+                const uint64_t wm = s_w1[xs(m - 1)];
                 proxy = __ddiv_rn((double)(wm < z ? wm : z), dS1);
             } else {
-                proxy = fmin(1.0, __dadd_rn(__ddiv_rn((double)s_w1[s_xs[0]], dS1), t.eps));
+                proxy = fmin(1.0, __dadd_rn(__ddiv_rn((double)s_w1[xs(0)], dS1), t.eps));
             }
         } else {
             proxy = __ddiv_rn((double)s_w1[item], dS1);

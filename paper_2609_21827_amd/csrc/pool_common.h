@@ -64,6 +64,41 @@ __device__ __forceinline__ void rank_all(const uint64_t* keys, int n, int16_t* r
     if (i < n && sub == 0) rank[i] = (int16_t)c;
 }
 
+// Ranks and prefix masses of n keys in LDS: for every key i, the count of
+// larger keys and the sum of w over them, split over F lanes as in rank_all;
+// fn(i, count, mass) is called once per key by one lane.  Keys larger than
+// every other (e.g. 0 for "none") may repeat; the others must be unique.
+template <int NT, typename Fn>
+__device__ __forceinline__ void rank_prefix(const uint64_t* keys, const uint32_t* w, int n,
+                                            Fn fn) {
+    const int t = threadIdx.x % NT;
+    int F = 1;
+    while (F < 16 && 2 * F * n <= NT) F *= 2;
+    const int sub = t % F;
+    for (int base = 0; base < n; base += NT / F) {
+        const int i = base + t / F;
+        const uint64_t k = keys[i < n ? i : 0];
+        int c = 0;
+        uint64_t pre = 0;
+        // branch-free, so that the loads of several keys are in flight
+#pragma unroll 4
+        for (int j = sub; j < n; j += F) {
+            const uint64_t x = keys[j];
+            const uint64_t wj = w[j];
+            const uint64_t gt = x > k ? 1ull : 0ull;
+            c += (int)gt;
+            pre += wj & (0ull - gt);
+        }
+        for (int o = 1; o < F; o <<= 1) {
+            c += __shfl_xor(c, o);
+            const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)pre, o);
+            const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(pre >> 32), o);
+            pre += ((uint64_t)hi << 32) | lo;
+        }
+        if (i < n && sub == 0) fn(i, c, pre);
+    }
+}
+
 // Synchronisation and sums over the NT threads that form a pool: one wave
 // (small supports) or the whole block.
 template <int NT>
