@@ -15,7 +15,8 @@ from .drivers import run_philox
 def tree_config(w, **over):
     kw = dict(K=w.K, m=w.m, depth=w.depth, n_expand=w.n_expand,
               support=w.support, construct_tempered=w.construct_tempered,
-              eps=w.eps_m0)
+              eps=w.eps_m0, mode="topk" if w.method == "topk" else "rheo",
+              verifier="rrsw" if w.method == "rrsw" else "rheo")
     kw.update(over)
     return rheo.TreeConfig(**kw)
 

@@ -340,6 +340,7 @@ class TreeConfig:
     construct_tempered: bool = False
     eps: float = 2.0 ** -40
     mode: str = "rheo"           # "rheo" or "topk" (pure top-K baseline)
+    verifier: str = "rheo"       # "rheo" (Algorithm 1) or "rrsw" (App. D.2 baseline)
     proxy_rule: str = "rheo"     # "adhoc" only for the negative control
     adhoc_proxy: float = None
     model: str = "canonical"
@@ -427,7 +428,24 @@ def prune(nodes, R):
 # RheoVerification (Algorithm 1), layer by layer (Thm. 1)
 # ---------------------------------------------------------------------------
 
-def verify(nodes, pt, target_P):
+def _candidate_tests(nodes, pt, cand, level, r, z_rem):
+    """Sequential tests of ``cand`` (pruned indices, slot order) under the
+    residual ``r`` of mass ``z_rem``: accept the first candidate u with
+    eta <= r(u); a rejected candidate gets r(u) = 0 (renormalised).  Yields
+    Bern requests; returns (accepted index or None, remaining mass)."""
+    for j in cand:
+        tok = nodes[pt.order[j]].token
+        nv = r.weight(tok)
+        ok = yield Bern(VERIFY, 32 * level + nodes[pt.order[j]].slot, nv, z_rem)
+        if ok:
+            return j, z_rem
+        r.override[tok] = 0
+        r._total -= nv
+        z_rem -= nv
+    return None, z_rem
+
+
+def verify(nodes, pt, target_P, verifier="rheo"):
     """Walk the pruned tree from the root.  ``target_P(i)`` returns the
     target weights P over the vocabulary at pruned node i (p = P / sum P).
     Yields Bern / Cat requests; returns (accepted tokens, final token).
@@ -438,7 +456,14 @@ def verify(nodes, pt, target_P):
     r = norm(max(0, p - q~)).  If s == -1: r = p.  Then for each remaining
     candidate in order: accept iff eta <= r(u_i), else r(u_i) = 0 and
     renormalise.  If none is accepted, emit u* ~ r.  With integer weights
-    r(v) = N_v / Z and the tests are exact integer comparisons."""
+    r(v) = N_v / Z and the tests are exact integer comparisons.
+
+    ``verifier='rrsw'``: the recursive rejection baseline of App. D.2, which
+    keeps the pool but tests the sampled child after the leads: the leads
+    (the candidates before u_s) under p, then u_s under the remaining
+    target r (accept iff eta <= r(u_s) / q~(u_s)), then, after a rejection,
+    the fills under norm(max(0, r - q~)).  Without a sampled child both
+    verifiers are the same sequential test under p."""
     accepted = []
     cur = 0
     level = 0
@@ -453,36 +478,38 @@ def verify(nodes, pt, target_P):
         s = pt.sampled[cur]
         F = 1
         override = {}
+        z_y = Sp                   # mass of the target r when u_s is tested
+        if s != -1 and verifier == "rrsw":
+            r = ResidualDist(P, 1, {})
+            hit, z_y = yield from _candidate_tests(nodes, pt, cand[:s], level, r, Sp)
+            if hit is not None:
+                accepted.append(nodes[pt.order[hit]].token)
+                cur = hit
+                level += 1
+                continue
+            override = dict(r.override)          # the rejected leads, zeroed
+            cand = cand[s:]
+            s = 0
         if s != -1:
             tail = node_cur.dist.tail
             Zq = tail.total()
             y_idx = cand[s]
             Y = nodes[pt.order[y_idx]].token
             ok = yield Bern(VERIFY, 32 * level, _num(P[Y]) * Zq,
-                            tail.weight(Y) * Sp)
+                            tail.weight(Y) * z_y)
             if ok:
                 accepted.append(Y)
                 cur = y_idx
                 level += 1
                 continue
             del cand[s]
-            # r = norm(max(0, p - q~)): numerators P_v Zq - Q_v Sp over S_p Zq
+            # r = norm(max(0, r - q~)): numerators P_v Zq - Q_v z_y over
+            # z_y Zq (rejected leads stay at 0)
             F = Zq
             for v, qv in zip(tail.ids, tail.weights):
-                override[v] = max(0, _num(P[v]) * Zq - qv * Sp)
+                override[v] = max(0, _num(P[v]) * Zq - qv * z_y)
         r = ResidualDist(P, F, override)
-        z_rem = r.total()
-        hit = None
-        for j in cand:
-            tok = nodes[pt.order[j]].token
-            nv = r.weight(tok)
-            ok = yield Bern(VERIFY, 32 * level + nodes[pt.order[j]].slot, nv, z_rem)
-            if ok:
-                hit = j
-                break
-            r.override[tok] = 0
-            r._total -= nv
-            z_rem -= nv
+        hit, _ = yield from _candidate_tests(nodes, pt, cand, level, r, r.total())
         if hit is not None:
             accepted.append(nodes[pt.order[hit]].token)
             cur = hit
@@ -497,5 +524,5 @@ def rheo_step(cfg, T, R, draft_dist, target_P, seq=0):
     (nodes, pruned tree, accepted tokens, final token)."""
     nodes = yield from build_tree(cfg, T, draft_dist, seq)
     pt = prune(nodes, R)
-    acc, u = yield from verify(nodes, pt, target_P)
+    acc, u = yield from verify(nodes, pt, target_P, cfg.verifier)
     return nodes, pt, acc, u

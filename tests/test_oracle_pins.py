@@ -251,6 +251,83 @@ def test_thm2_single_layer_acceptance(seed):
     assert out == {v: F(p[v]) / ps for v in range(V)}
 
 
+def _rrsw(q, p, n, m):
+    """eq. (rrsw-acc), App. D.2: the pool of Thm. 2 verified leads-first."""
+    V = len(q)
+    qs, ps = F(sum(q)), F(sum(p))
+    order = rheo.rank_order(list(range(V)), q)
+    top = order[:n - 1]
+    lead = order[:m]
+    z = 1 - sum(F(q[v]) / qs for v in lead)
+    qt = {v: (F(q[v]) / qs / z if v not in lead else F(0)) for v in range(V)}
+    pp = {v: F(p[v]) / ps for v in range(V)}
+    A = sum(pp[v] for v in lead)
+    pt = {v: (pp[v] / (1 - A) if v not in lead else F(0)) for v in range(V)}
+    rnum = {v: max(F(0), pt[v] - qt[v]) for v in range(V)}
+    rz = sum(rnum.values())
+    xn = order[n - 1]
+    r_xn = rnum[xn] / rz if rz else F(0)
+    return (sum(pp[v] for v in top)
+            + sum(min(pp[v], (1 - A) * qt[v]) for v in range(V) if v not in top)
+            + (1 - A) * r_xn * sum(max(F(0), qt[v] - pt[v]) for v in top))
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_rrsw_single_layer_acceptance(seed):
+    # App. D.2: the same pool verified leads-first (RRSw) accepts exactly
+    # eq. (rrsw-acc) and stays lossless
+    rng = np.random.default_rng(300 + seed)
+    V = int(rng.integers(4, 9))
+    n = int(rng.integers(2, min(V, 5)))
+    m = int(rng.integers(1, n))
+    q = _rand_weights(rng, V)
+    p = _rand_weights(rng, V)
+    nd = rheo.node_dist_from_weights(list(range(V)), q, m=m)
+    cfg = rheo.TreeConfig(K=n, m=m, depth=1, verifier="rrsw")
+    fac = lambda: rheo.rheo_step(cfg, 1.0, n, lambda a, b: nd, lambda i: list(p))
+    out, acc = _first_token_stats(enumerate_all(fac))
+    assert acc == _rrsw(q, p, n, m)
+    ps = F(sum(p))
+    assert out == {v: F(p[v]) / ps for v in range(V)}
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_rrsw_equals_rheo_without_leads(seed):
+    # m = 0: no lead precedes the sampled child, so both verifiers take the
+    # same decisions (eq. (rrsw-acc) reduces to eq. (rheo-acc) with A = 0)
+    rng = np.random.default_rng(400 + seed)
+    V = int(rng.integers(4, 8))
+    n = int(rng.integers(2, min(V, 5)))
+    q = _rand_weights(rng, V)
+    p = _rand_weights(rng, V)
+    nd = rheo.node_dist_from_weights(list(range(V)), q, m=0)
+    res = {}
+    for ver in ("rheo", "rrsw"):
+        cfg = rheo.TreeConfig(K=n, m=0, depth=1, verifier=ver)
+        fac = lambda: rheo.rheo_step(cfg, 1.0, n, lambda a, b: nd, lambda i: list(p))
+        res[ver] = _first_token_stats(enumerate_all(fac))
+    assert res["rheo"] == res["rrsw"]
+    assert _rrsw(q, p, n, 0) == _thm2(q, p, n, 0)[0]
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_pure_topk_tree_acceptance(seed):
+    # the pure top-K tree (Sec. 2.1, no sampled slot) verified by the same
+    # sequential tests accepts sum_{Top_n} p and is lossless
+    rng = np.random.default_rng(500 + seed)
+    V = int(rng.integers(4, 8))
+    n = int(rng.integers(1, V))
+    q = _rand_weights(rng, V)
+    p = _rand_weights(rng, V)
+    nd = rheo.node_dist_from_weights(list(range(V)), q, m=1)
+    cfg = rheo.TreeConfig(K=n, m=1, depth=1, mode="topk")
+    fac = lambda: rheo.rheo_step(cfg, 1.0, n, lambda a, b: nd, lambda i: list(p))
+    out, acc = _first_token_stats(enumerate_all(fac))
+    ps = F(sum(p))
+    assert acc == sum(F(p[v]) for v in nd.support[:n]) / ps
+    assert out == {v: F(p[v]) / ps for v in range(V)}
+
+
 # --------------------------------------------------------------------------
 # Thm. 1: losslessness by exact enumeration over several steps
 # --------------------------------------------------------------------------
@@ -298,7 +375,7 @@ def _one_step(cfg, T, R, pre, lf, model, cache):
     nodes = yield from rheo.build_tree(cfg, T, dd)
     pt = rheo.prune(nodes, R)
     holder["nodes"], holder["pt"] = nodes, pt
-    acc, u = yield from rheo.verify(nodes, pt, tp)
+    acc, u = yield from rheo.verify(nodes, pt, tp, cfg.verifier)
     return tuple(acc) + (u,)
 
 
@@ -361,12 +438,26 @@ LOSSLESS_CASES += [
 ]
 
 
+# the leads-first baseline (App. D.2) and the pure top-K tree are lossless too
+LOSSLESS_CASES += [
+    (5, 3, 1, 2, 4, 1.0, 0, False, "canonical", 2, "rrsw"),
+    (5, 3, 2, 2, 5, 0.6, 0, False, "canonical", 2, "rrsw"),
+    (6, 4, 2, 2, 6, 1.0, 5, False, "canonical", 2, "rrsw"),
+    (4, 3, 1, 2, 3, 1.0, 0, False, "canonical", 2, "rrsw"),
+    (5, 3, 1, 2, 5, 1.0, 0, False, "canonical", 2, "topk"),
+    (5, 2, 1, 2, 2, 0.5, 0, False, "canonical", 2, "topk"),
+]
+
+
 @pytest.mark.parametrize("case", LOSSLESS_CASES)
 def test_thm1_lossless_by_enumeration(case):
-    V, K, m, D, R, T, S, tempered, model, L = case
-    lf = _logits_fn(hash(case) & 0xFFFF, V)
+    V, K, m, D, R, T, S, tempered, model, L = case[:10]
+    method = case[10] if len(case) > 10 else "rheo"
+    lf = _logits_fn(hash(case[:10]) & 0xFFFF, V)
     cfg = rheo.TreeConfig(K=K, m=m, depth=D, n_expand=min(K, 2), support=S,
-                          construct_tempered=tempered, model=model)
+                          construct_tempered=tempered, model=model,
+                          mode="topk" if method == "topk" else "rheo",
+                          verifier="rrsw" if method == "rrsw" else "rheo")
     dist = _multi_step_dist(cfg, T, R, L, lf, model)
     assert sum(dist.values()) == 1
     for seq, prob in dist.items():
