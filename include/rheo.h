@@ -66,6 +66,8 @@ enum {
 
 enum { RHEO_F32 = 0, RHEO_BF16 = 1 };
 
+enum { RHEO_METHOD_RHEO = 0, RHEO_METHOD_RRSW = 1, RHEO_METHOD_TOPK = 2 };
+
 typedef struct rheo_config {
     int32_t batch;               /* B >= 1 independent sequences                      */
     int32_t vocab;               /* V, 2 <= V <= 262143                               */
@@ -84,7 +86,14 @@ typedef struct rheo_config {
     int32_t construct_tempered;  /* 0: tree built on untempered q (Sec. 5.4);
                                     1: on the tempered q_T                              */
     int32_t dtype;               /* RHEO_F32 or RHEO_BF16                               */
-    int32_t reserved;            /* must be 0                                           */
+    int32_t method;              /* RHEO_METHOD_RHEO: the pools of Sec. 3.2 verified by
+                                    Algorithm 1 (the sampled child first);
+                                    RHEO_METHOD_RRSW: the same pools verified leads
+                                    first -- the leads under p, then the sampled child
+                                    under what remains, then the fills under
+                                    norm(max(0, r - q~)) (App. D.2);
+                                    RHEO_METHOD_TOPK: pure top-K pools, no sampled
+                                    slot (Sec. 2.1), sequential tests under p        */
     int64_t row_stride;          /* elements between consecutive logit rows (>= V)     */
     double eps_m0;               /* epsilon of the m = 0 proxy q(x_1) + eps (Sec. 3.2);
                                     0 selects 2^-40                                     */

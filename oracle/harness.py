@@ -67,7 +67,7 @@ def oracle_step(w, b, step, T=None, trace=None, model="canonical", cfg=None,
         nodes = yield from rheo.build_tree(cfg, T, draft_dist, b)
         pt = rheo.prune(nodes, w.R)
         holder["nodes"], holder["pt"] = nodes, pt
-        acc, u = yield from rheo.verify(nodes, pt, target_P)
+        acc, u = yield from rheo.verify(nodes, pt, target_P, cfg.verifier)
         return nodes, pt, acc, u
 
     return run_philox(process(), synth.step_rng_key(w, step), b, trace)

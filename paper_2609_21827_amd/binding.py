@@ -16,6 +16,8 @@ LIB_PATH = os.path.join(HERE, "librheo.so")
 
 RHEO_OK, RHEO_EINVAL, RHEO_ENOMEM, RHEO_EHIP, RHEO_ESTATE = 0, -1, -2, -3, -4
 RHEO_F32, RHEO_BF16 = 0, 1
+RHEO_METHOD_RHEO, RHEO_METHOD_RRSW, RHEO_METHOD_TOPK = 0, 1, 2
+METHODS = {"rheo": RHEO_METHOD_RHEO, "rrsw": RHEO_METHOD_RRSW, "topk": RHEO_METHOD_TOPK}
 ERROR_NAMES = {RHEO_EINVAL: "EINVAL", RHEO_ENOMEM: "ENOMEM", RHEO_EHIP: "EHIP",
                RHEO_ESTATE: "ESTATE"}
 
@@ -31,7 +33,7 @@ class RheoConfig(ctypes.Structure):
                 ("pool", ctypes.c_int32), ("leads", ctypes.c_int32),
                 ("depth", ctypes.c_int32), ("n_expand", ctypes.c_int32),
                 ("support", ctypes.c_int32), ("construct_tempered", ctypes.c_int32),
-                ("dtype", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("method", ctypes.c_int32),
                 ("row_stride", ctypes.c_int64), ("eps_m0", ctypes.c_double)]
 
 
@@ -110,7 +112,7 @@ class Tree:
 
     def __init__(self, batch, vocab, pool, leads, depth, support, dtype,
                  n_expand=0, construct_tempered=False, row_stride=None,
-                 eps_m0=0.0, device="cuda"):
+                 eps_m0=0.0, method="rheo", device="cuda"):
         lib = load_library()
         self.device = torch.device(device)
         self.B, self.V, self.K, self.m, self.D = batch, vocab, pool, leads, depth
@@ -119,7 +121,8 @@ class Tree:
         self.row_stride = row_stride or vocab
         cfg = RheoConfig(batch, vocab, pool, leads, depth, n_expand, support,
                          int(construct_tempered),
-                         RHEO_BF16 if dtype == torch.bfloat16 else RHEO_F32, 0,
+                         RHEO_BF16 if dtype == torch.bfloat16 else RHEO_F32,
+                         METHODS[method] if isinstance(method, str) else int(method),
                          self.row_stride, eps_m0)
         h = ctypes.c_void_p()
         _check(lib.rheo_create(ctypes.byref(cfg), ctypes.byref(h)))

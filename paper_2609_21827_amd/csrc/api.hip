@@ -116,7 +116,8 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
     if (c.depth < 1 || c.depth > 15) return fail(RHEO_EINVAL, "depth must be in [1, 15]");
     if (c.n_expand < 1 || c.n_expand > c.pool) return fail(RHEO_EINVAL, "n_expand must be in [1, K]");
     if (c.dtype != RHEO_F32 && c.dtype != RHEO_BF16) return fail(RHEO_EINVAL, "unknown dtype");
-    if (c.reserved != 0) return fail(RHEO_EINVAL, "reserved field must be 0");
+    if (c.method < RHEO_METHOD_RHEO || c.method > RHEO_METHOD_TOPK)
+        return fail(RHEO_EINVAL, "unknown method %d", c.method);
     // support <= 0: dense mode, the support is the whole vocabulary
     const bool dense = c.support <= 0;
     const int S = dense ? c.vocab : (c.support < c.vocab ? c.support : c.vocab);
@@ -137,6 +138,8 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
     TreeDev& d = t->dev;
     d.B = c.batch; d.V = c.vocab; d.K = c.pool; d.m = c.leads; d.D = c.depth;
     d.NE = c.n_expand; d.S = S; d.dtype = c.dtype; d.stride = c.row_stride;
+    d.rrsw = c.method == RHEO_METHOD_RRSW;
+    d.topk = c.method == RHEO_METHOD_TOPK;
     d.dense = dense ? 1 : 0;
     d.NCH = (c.vocab + WAVE_TOKENS(c.dtype) - 1) / WAVE_TOKENS(c.dtype);
     d.eps = c.eps_m0;

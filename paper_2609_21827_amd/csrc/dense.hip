@@ -391,7 +391,7 @@ __global__ __launch_bounds__(NTD) void k_dpool(TreeDev t, LevelArgs a) {
         int kind, tok;
         double proxy;
         const double dS1 = (double)S1;
-        if (s < m) {
+        if (s < m || t.topk) {                   // a lead (pure top-K pools: every slot)
             kind = LEAD;
             tok = key_id(s_x[s]);
             proxy = __ddiv_rn((double)s_xw[s], dS1);

@@ -210,12 +210,16 @@ __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, 
         t.exp_of[nb + pu] = e_idx;
         if (level == 0) emit_root(t, nb);
     }
-    // the K children: top-m leads, Y, fills (App. C.1)
+    // the K children: top-m leads, Y, fills (App. C.1); pure top-K pools:
+    // the K best by (w1 desc, id asc)
     if (tid < K) {
         const int s = tid;
         const int yr = wr(yi);
         int item, kind;
-        if (s < m) {
+        if (t.topk) {
+            item = xs(s);
+            kind = LEAD;
+        } else if (s < m) {
             item = xs(s);
             kind = LEAD;
         } else if (s == m) {

@@ -62,6 +62,8 @@ struct TreeDev {
     uint32_t* row_cnt;             // [B * NE] chunk blocks arrived (0 between launches)
     uint32_t* seq_cnt;             // [B] rows whose pool is written (0 between launches)
     int C, Sc;
+    int rrsw;                      // verification leads first (App. D.2)
+    int topk;                      // pure top-K pools, no sampled slot
 };
 
 struct LevelArgs {

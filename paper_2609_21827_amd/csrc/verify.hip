@@ -21,6 +21,10 @@
 //        none accepted (or no candidates): u* ~ r by inverse CDF over token
 //        ids, t = floor(U64 Z_rem / 2^64): the chunk holding t from the chunk
 //        totals corrected at the special tokens, then a scan of that chunk.
+//      The RRSw baseline (App. D.2) tests the leads -- the candidates before
+//      the sampled child -- first, under p; then the sampled child against
+//      what remains (mass Z_l = S_p less the rejected leads) in place of S_p
+//      above, and the fills under the residual with Z_l for S_p.
 // Team exchanges use agent-scope atomic stores and loads only (they are
 // coherent across the XCDs without cache write-back or invalidation), with
 // arrival epochs in per-block flags and bounded waits.
@@ -206,7 +210,7 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
     __shared__ int s_nc, s_spos, s_mode, s_next, s_token, s_cstar;
     __shared__ int s_cur, s_curp, s_fc, s_e;     // the node this layer verifies
     __shared__ int s_resid;                      // the sampled child was rejected
-    __shared__ uint64_t s_Sp;
+    __shared__ uint64_t s_Sp, s_Zl;
     __shared__ uint64_t s_U[16], s_Ufin;         // the layer's uniforms
     __shared__ u128 s_F, s_Zrem, s_tt;
     __shared__ float s_M;
@@ -428,14 +432,15 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
         //         and the decisions of lane 0) ---------------------------------
         uint64_t Sp = 0;
         // The remaining candidates' tests in slot order (Algorithm 1), one
-        // lane per candidate: lane ci holds N_ci (0 for the sampled child);
+        // lane per candidate in [lo, nc_): lane ci holds N_ci (0 for the
+        // sampled child);
         // the residual mass before candidate ci is Zrem less the N of the
         // candidates before it (all rejected if ci is reached), so the
         // first lane whose test passes is the accepted candidate.  Returns
         // its index, or -1 with *zrem reduced by every candidate's N; marks
         // the rejected candidates.  Wave 0 only.
-        auto cand_tests = [&](int nc_, int spos_, u128 Nu, u128* zrem) -> int {
-            const bool cand = lane < nc_ && lane != spos_;
+        auto cand_tests = [&](int lo, int nc_, int spos_, u128 Nu, u128* zrem) -> int {
+            const bool cand = lane >= lo && lane < nc_ && lane != spos_;
             if (!cand) Nu = 0;
             const u128 before = wave_incl_scan_u128(Nu) - Nu;
             const u128 zr = *zrem - before;
@@ -487,33 +492,47 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
             wave_sync();
             if (lane < nc) s_c_tail[lane] = DN ? -1 : find_sorted(s_tid, nt, s_c_tok[lane]);
             wave_sync();
-            // the sampled child first (every lane takes the same decision)
+            // RRSw (App. D.2): the leads -- the candidates before the sampled
+            // child -- are tested first, under p; the sampled child is then
+            // tested under what remains, of mass Z_l.  Algorithm 1 tests the
+            // sampled child first (Z_l = S_p).  Every lane takes the same
+            // decisions.
             int mode = (nc == 0) ? 2 : 0;      // 0: candidate tests follow, 1: accepted, 2: final sample
-            int next = -1;
-            if (spos >= 0) {
+            int next = -1, clo = 0;
+            uint64_t Zl = Sp;
+            if (t.rrsw && spos > 0) {
+                u128 zr = Sp;
+                const u128 Np = (lane < spos) ? (u128)s_tp[nt + lane] : (u128)0;
+                next = cand_tests(0, spos, -1, Np, &zr);
+                if (next >= 0) mode = 1;
+                Zl = (uint64_t)zr;
+                clo = spos + 1;
+            }
+            if (mode == 0 && spos >= 0) {
                 const int yi = s_c_tail[spos];
                 if (!DN && yi < 0 && lane == 0) atomicOr(t.err, 4);
                 const uint64_t QY = DN ? (uint64_t)s_c_q[spos] : ((yi >= 0) ? s_tq[yi] : 0);
                 const uint64_t PY = s_tp[nt + spos];
                 const uint64_t U = s_U[0];
-                if ((u128)(U + 1) * QY * Sp <= (((u128)PY * Zq) << 32)) {
+                if ((u128)(U + 1) * QY * Zl <= (((u128)PY * Zq) << 32)) {
                     mode = 1;
                     next = spos;
                 }
             }
             const bool resid = spos >= 0 && mode == 0;
             const u128 F = resid ? (u128)Zq : (u128)1;
-            // no rejected Y: r = p, mass S_p.  Sparse rejection: Z_r = Zq Sp
-            // less the sum over the tail of min(P_v Zq, Q_v Sp).  Dense
-            // rejection: the residual totals come from a third pass.
-            u128 Zrem = Sp;
+            // no rejected Y: r = p less rejected leads, mass Z_l.  Sparse
+            // rejection: Z_r = Zq Z_l less the sum over the tail of
+            // min(P_v Zq, Q_v Z_l).  Dense rejection: the residual totals
+            // come from a third pass.
+            u128 Zrem = Zl;
             if (resid && !DN) {
                 u128 d = 0;
                 for (int i = lane; i < nt; i += WAVE) {
-                    const u128 pz = (u128)s_tp[i] * Zq, qs = (u128)s_tq[i] * Sp;
+                    const u128 pz = (u128)s_tp[i] * Zq, qs = (u128)s_tq[i] * Zl;
                     d += pz < qs ? pz : qs;
                 }
-                Zrem = (u128)Zq * Sp - wave_sum_u128(d);
+                Zrem = (u128)Zq * Zl - wave_sum_u128(d);
             }
             if (mode == 0 && !(DN && resid)) {
                 u128 Nu = 0;
@@ -522,15 +541,16 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
                     const int ti = s_c_tail[lane];
                     Nu = F * (u128)P;
                     if (resid && ti >= 0) {
-                        const u128 pz = (u128)P * Zq, qs = (u128)s_tq[ti] * Sp;
+                        const u128 pz = (u128)P * Zq, qs = (u128)s_tq[ti] * Zl;
                         Nu = pz > qs ? pz - qs : (u128)0;
                     }
                 }
-                next = cand_tests(nc, spos, Nu, &Zrem);
+                next = cand_tests(clo, nc, spos, Nu, &Zrem);
                 mode = next >= 0 ? 1 : 2;
             }
             if (lane == 0) {
                 s_Sp = Sp;
+                s_Zl = Zl;
                 s_mode = mode;
                 s_resid = resid ? 1 : 0;
                 s_F = F;
@@ -548,10 +568,13 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
         }
         __syncthreads();
         Sp = s_Sp;
+        const uint64_t Zl = s_Zl;
         const bool residual = s_resid != 0;
+        const int nrej = (t.rrsw && residual) ? spos : 0;    // leads rejected before Y
         if (DN && s_mode == 0) {
-            // N_v = max(0, P_v Zq - Q_v Sp) over all of V (Q_v from the draft
-            // row, 0 at the leads): chunk totals over the segment, exchanged
+            // N_v = max(0, P_v Zq - Q_v Z_l) over all of V (Q_v from the draft
+            // row, 0 at the leads; P_v = 0 at leads rejected before Y):
+            // chunk totals over the segment, exchanged
             for (int c = c0 + wid; c < c1; c += NWV) {
                 const uint4 xv = load_vec<DT>(row, c * WAVE + lane, V);
                 const uint4 dv = load_vec<DT>(drow, c * WAVE + lane, V);
@@ -560,11 +583,12 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
                 for (int k = 0; k < VEC; ++k) {
                     const int v = (c * WAVE + lane) * VEC + k;
                     if (v < V) {
-                        bool lead = false;
+                        bool lead = false, rej = false;
                         for (int q = 0; q < nlead; ++q) lead |= s_lead[q] == v;
-                        const uint64_t P = cweight(velem<DT>(xv, k), M, a.kT);
+                        for (int q = 0; q < nrej; ++q) rej |= s_c_tok[q] == v;
+                        const uint64_t P = rej ? 0u : cweight(velem<DT>(xv, k), M, a.kT);
                         const uint64_t Q = lead ? 0u : cweight(velem<DT>(dv, k), dref, a.kT);
-                        const u128 pz = (u128)P * Zq, qs = (u128)Q * Sp;
+                        const u128 pz = (u128)P * Zq, qs = (u128)Q * Zl;
                         sum += pz > qs ? pz - qs : (u128)0;
                     }
                 }
@@ -585,10 +609,10 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
                 u128 Nu = 0;
                 if (lane < nc) {
                     const uint64_t P = s_tp[nt + lane];
-                    const u128 pz = (u128)P * Zq, qs = (u128)s_c_q[lane] * Sp;
+                    const u128 pz = (u128)P * Zq, qs = (u128)s_c_q[lane] * Zl;
                     Nu = pz > qs ? pz - qs : (u128)0;
                 }
-                const int next = cand_tests(nc, spos, Nu, &Zrem);
+                const int next = cand_tests(t.rrsw ? spos + 1 : 0, nc, spos, Nu, &Zrem);
                 if (lane == 0) {
                     s_mode = next >= 0 ? 1 : 2;
                     s_Zrem = Zrem;
@@ -626,7 +650,7 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
                 int lb;
                 find_sorted(s_tid, nt, cidx * CH, &lb);
                 for (int i = lb; i < nt && s_tid[i] < (cidx + 1) * CH; ++i) {
-                    const u128 pz = (u128)s_tp[i] * Zq, qs = (u128)s_tq[i] * Sp;
+                    const u128 pz = (u128)s_tp[i] * Zq, qs = (u128)s_tq[i] * Zl;
                     d += pz < qs ? pz : qs;       // F P - N for a live tail token
                 }
             }
@@ -637,7 +661,7 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
                 const u128 fp = F * (u128)s_tp[nt + ci];
                 if (residual && s_c_tail[ci] >= 0) {
                     // zeroed tail token: its live deficit was counted above
-                    const u128 pz = (u128)s_tp[nt + ci] * Zq, qs = (u128)s_tq[s_c_tail[ci]] * Sp;
+                    const u128 pz = (u128)s_tp[nt + ci] * Zq, qs = (u128)s_tq[s_c_tail[ci]] * Zl;
                     d += fp - (pz < qs ? pz : qs);
                 } else {
                     d += fp;
@@ -651,8 +675,9 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
             if (DN && residual) {
                 u128 w = nchunk_at(c);
                 for (int ci = 0; ci < nc; ++ci) {
-                    if (!s_c_zero[ci] || s_c_tok[ci] / CH != c) continue;
-                    const u128 pz = (u128)s_tp[nt + ci] * Zq, qs = (u128)s_c_q[ci] * Sp;
+                    // (rejected leads were left out of the third pass)
+                    if (!s_c_zero[ci] || ci < nrej || s_c_tok[ci] / CH != c) continue;
+                    const u128 pz = (u128)s_tp[nt + ci] * Zq, qs = (u128)s_c_q[ci] * Zl;
                     w -= pz > qs ? pz - qs : (u128)0;
                 }
                 return w;
@@ -698,7 +723,7 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
                     bool lead = false;
                     for (int q = 0; q < nlead; ++q) lead |= s_lead[q] == v;
                     const uint64_t Q = lead ? 0u : cweight(load_logit<DT>(drow, v), dref, a.kT);
-                    const u128 pz = (u128)P * Zq, qs = (u128)Q * Sp;
+                    const u128 pz = (u128)P * Zq, qs = (u128)Q * Zl;
                     w = pz > qs ? pz - qs : (u128)0;
                 } else {
                     w = F * (u128)P;
@@ -711,7 +736,7 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
             for (int i = tid; i < nt; i += NTV) {
                 const int v = s_tid[i];
                 if (v / CH == cs) {
-                    const u128 pz = (u128)s_tp[i] * Zq, qs = (u128)s_tq[i] * Sp;
+                    const u128 pz = (u128)s_tp[i] * Zq, qs = (u128)s_tq[i] * Zl;
                     s_cn[v - cs * CH] = pz > qs ? pz - qs : (u128)0;
                 }
             }

@@ -18,7 +18,7 @@ from .binding import Tree
 def make_tree(w, device="cuda", **over):
     kw = dict(batch=w.B, vocab=w.V, pool=w.K, leads=w.m, depth=w.depth,
               support=w.support, n_expand=w.n_expand,
-              construct_tempered=w.construct_tempered, eps_m0=w.eps_m0,
+              construct_tempered=w.construct_tempered, eps_m0=w.eps_m0, method=w.method,
               dtype=torch.bfloat16 if w.dtype == "bf16" else torch.float32,
               device=device)
     kw.update(over)

@@ -336,3 +336,37 @@ def test_dense_batched(dev):
 def test_headline_dense(dev):
     """The dense bench workload at its full size, sampled sequences."""
     run_parity(W["headline_dense"], [0], [0, 63], dev=dev)
+
+
+# ---- the comparison methods: RRSw verification, pure top-K trees ----------
+
+METHOD_OVERS = [dict(), dict(m=2, K=4, R=10), dict(m=0, eps_m0=2.0 ** -20),
+                dict(T=0.6, construct_tempered=True), dict(B=3)]
+
+
+@pytest.mark.parametrize("method", ["rrsw", "topk"])
+@pytest.mark.parametrize("over", METHOD_OVERS)
+def test_methods_tiny(dev, method, over):
+    w = W["tiny"].with_(name="tiny_" + method, method=method, **over)
+    run_parity(w, range(30), list(range(w.B)), dev=dev)
+
+
+@pytest.mark.parametrize("method", ["rrsw", "topk"])
+def test_methods_dense_tiny(dev, method):
+    w = W["tiny"].with_(name="tiny_dense_" + method, support=0, method=method, m=2, K=4, R=10)
+    run_parity(w, range(20), [0], dev=dev)
+
+
+@pytest.mark.parametrize("method", ["rrsw", "topk"])
+def test_methods_llama2_both_modes(dev, method):
+    for support in (128, 0):
+        w = W["llama2"].with_(name="llama2_" + method, method=method, support=support,
+                              m=2, depth=3, R=20)
+        run_parity(w, range(2), [0], dev=dev)
+
+
+@pytest.mark.parametrize("method", ["rrsw", "topk"])
+def test_methods_headline(dev, method):
+    """The batched bench shape (one block per row at every level)."""
+    run_parity(W["headline"].with_(name="headline_" + method, method=method), [0], [0, 63],
+               dev=dev)

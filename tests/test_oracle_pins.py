@@ -636,3 +636,22 @@ def test_philox_sampler_frequencies():
     tot = sum(wts)
     chi2 = sum((counts[i] - n * w / tot) ** 2 / (n * w / tot) for i, w in zip(ids, wts))
     assert chi2 < 16.3   # 3 d.o.f., p = 0.001
+
+
+def test_harness_applies_the_method():
+    # the workload's method reaches the oracle step: under RRSw a lead's test
+    # (draw index 32 * level + its slot) comes before the sampled child's
+    # (index 32 * level) at some layer; under Algorithm 1 never
+    import synth
+    from oracle.harness import oracle_step
+    w = synth.WORKLOADS["tiny"]
+    seen = {"rheo": False, "rrsw": False}
+    for method in seen:
+        for step in range(12):
+            tr = []
+            oracle_step(w.with_(method=method), 0, step, trace=tr)
+            tests = [t[2] for t in tr if t[0] == "Bern"]
+            for i, idx in enumerate(tests):
+                if idx % 32 == 0 and any(j // 32 == idx // 32 for j in tests[:i]):
+                    seen[method] = True
+    assert seen == {"rheo": False, "rrsw": True}
