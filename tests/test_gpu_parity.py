@@ -140,6 +140,14 @@ def test_headline(dev):
     run_parity(W["headline"], [0, 1], [0, 31, 63], dev=dev)
 
 
+@pytest.mark.parametrize("support", [256, 1024])
+def test_headline_supports(dev, support):
+    # the larger sparse supports (Sec. 5.5) at the batched shape, where
+    # every level runs one block per row
+    w = W["headline"].with_(name=f"headline_s{support}", support=support, depth=4, R=30)
+    run_parity(w, [0], [0, 63], dev=dev)
+
+
 SHAPES = (
     {},
     {"RHEO_EXPAND_VARIANT": "0", "RHEO_VERIFY_BLOCKS": "4"},
