@@ -120,6 +120,10 @@ def main():
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB five times "
                          "(counter calibration under rocprofv3 --pmc)")
+    ap.add_argument("--sweep", choices=["table4", "methods", "rheostat", "support"],
+                    default=None,
+                    help="instead of the throughput line, print one JSON line per "
+                         "configuration of a sweep (see run_sweep)")
     ap.add_argument("--traffic-from", nargs=4, default=None,
                     metavar=("EXP_FETCH", "EXP_WRITE", "COPY_FETCH", "COPY_WRITE"),
                     help="write the traffic file from four rocprofv3 --pmc "
@@ -151,6 +155,10 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes": n, "copies": 5}), flush=True)
+        return
+
+    if args.sweep:
+        run_sweep(args)
         return
 
     import synth
@@ -339,6 +347,99 @@ def main():
     }
     print(json.dumps(res), flush=True)
     tree.close()
+
+
+def run_sweep(args):
+    """Sweeps on the batched shape (B = 64, V = 128256 bf16, synthetic rows),
+    one JSON line per configuration:
+      table4    single-layer acceptance (depth 1, K = 3: top-1, the sampled
+                token, the best remaining token) of the three methods
+                (App. A, Table 4: Top-K <= RRSw <= Rheo);
+      methods   tau = mean tokens emitted per sequence and step, full tree,
+                per method (App. A, Table 3);
+      rheostat  tau over the leads m and the temperature T (Sec. 5.4);
+      support   sparse support S (and the dense tree): top-S coverage of the
+                untempered draft distribution, expand-level time, tau
+                (Sec. 5.5, Table 5).
+    Acceptance and tau come from the GPU path itself on seeded steps."""
+    import torch
+    import synth
+    from paper_2609_21827_amd.driver import make_tree, run_step, replay_step
+
+    dev = "cuda"
+    base = synth.WORKLOADS["headline"]
+
+    def steps_stats(w, nsteps, first=0):
+        tree = make_tree(w, device=dev)
+        try:
+            lens = []
+            for s in range(first, first + nsteps):
+                _, alen, _ = run_step(tree, w, s, device=dev)
+                lens.append(alen)
+            assert tree.device_error() == 0
+        finally:
+            tree.close()
+        alen = torch.cat(lens).double()
+        return {"tau": round(float((alen + 1).mean()), 4),
+                "accept_rate": round(float((alen >= 1).double().mean()), 4),
+                "samples": int(alen.numel())}
+
+    def emit(name, cfg, res):
+        print(json.dumps({"sweep": name, "config": cfg, **res}), flush=True)
+
+    if args.sweep == "table4":
+        for method in ("topk", "rrsw", "rheo"):
+            w = base.with_(name="table4_" + method, method=method, K=3, m=1, depth=1, R=3,
+                            n_expand=1)
+            emit("table4", {"method": method, "K": 3, "m": 1, "depth": 1},
+                 steps_stats(w, 60))
+    elif args.sweep == "methods":
+        for method in ("topk", "rrsw", "rheo"):
+            w = base.with_(name="methods_" + method, method=method)
+            emit("methods", {"method": method, "K": w.K, "m": w.m, "depth": w.depth,
+                             "budget": w.R}, steps_stats(w, 12))
+    elif args.sweep == "rheostat":
+        for m in (0, 1, 2, 3):
+            for T in (0.2, 0.6, 1.0, 1.5):
+                w = base.with_(name="rheostat", m=m, T=T)
+                emit("rheostat", {"m": m, "T": T, "K": w.K, "depth": w.depth},
+                     steps_stats(w, 4))
+    else:
+        for S in (128, 256, 512, 1024, 0):
+            w = base.with_(name="support", support=S)
+            res = steps_stats(w, 6)
+            # coverage of the top-S entries under the untempered draft
+            # softmax, over the root rows and one level of frontier rows
+            tree = make_tree(w, device=dev)
+            rec = {}
+            run_step(tree, w, 100, device=dev, record=rec)
+            rows = torch.cat([r.reshape(-1, r.shape[-1])[:, :w.V] for r in rec["draft"][:2]]).float()
+            lse = torch.logsumexp(rows, dim=1)
+            if S > 0:
+                top = torch.topk(rows, S, dim=1).values
+                cov = torch.exp(torch.logsumexp(top, dim=1) - lse).mean().item()
+            else:
+                cov = 1.0
+            # expand-level time, replayed with the rows resident in HBM
+            for _ in range(3):
+                replay_step(tree, rec, w.R)
+            torch.cuda.synchronize()
+            ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                  for _ in range(10 * w.depth)]
+            for it in range(10):
+                tree.begin_step()
+                for d, r in enumerate(rec["draft"]):
+                    ev[it * w.depth + d][0].record()
+                    tree.expand_level(r, rec["T"], rec["rng_key"])
+                    ev[it * w.depth + d][1].record()
+                tree.prune(w.R)
+                tree.verify(rec["target"], rec["T"], rec["rng_key"])
+            torch.cuda.synchronize()
+            lvl = sum(a.elapsed_time(b) for a, b in ev) * 1e3 / len(ev)
+            assert tree.device_error() == 0
+            tree.close()
+            emit("support", {"support": S if S > 0 else "full", "K": w.K, "depth": w.depth},
+                 {**res, "coverage": round(cov, 4), "expand_level_us": round(lvl, 2)})
 
 
 if __name__ == "__main__":

@@ -39,6 +39,7 @@ constexpr int SMAX = 1024;    // largest support
 constexpr int MERGE_MAX = 2048;  // chunk-list keys one row merges (C * Sc)
 constexpr int NTE = 512;      // threads per k_expand_row block
 constexpr int EBATCH = 8;     // 16-byte vectors per thread and batch of k_expand_row
+constexpr int kCountTailMax = 256;  // largest support whose tail is ordered by counting
 
 template <int DT>
 __device__ __forceinline__ float elem(const uint4& v, int k) {
@@ -81,18 +82,29 @@ __device__ __forceinline__ uint4 load_row_vec(const char* base, int vi, int V) {
 // LDS layout of the pool kernel's dynamic buffer: the chunk lists and one
 // empty list after them, the support, ranking keys and per-entry
 // arrays; the level's priority keys (<= 225 of them) reuse the regions of
-// the support and the ranking keys.
+// the support and the ranking keys.  The ranking-key region holds a power
+// of two >= S keys (sorted in place for large supports).  top_min and
+// k2_min (entries, bytes) enlarge the first two regions for callers that
+// use them as scratch before the pool.
 struct PoolLds {
     int m, top, k2, w1, q, tq, wr, xs, ir, tx, bytes;
 };
 __host__ __device__ inline int pad16(int x) { return (x + 15) & ~15; }
-__host__ __device__ inline PoolLds pool_lds(int S, int C) {
+__host__ __device__ inline int pow2_at_least(int x) {
+    int p = 1;
+    while (p < x) p <<= 1;
+    return p;
+}
+__host__ __device__ inline PoolLds pool_lds(int S, int C, int top_min = 0, int k2_min = 0) {
     PoolLds L;
-    const int S2 = S > 256 ? S : 256;
+    int S2 = S > 256 ? S : 256;
+    if (S2 < top_min) S2 = top_min;
+    int k2b = 8 * pow2_at_least(S > 256 ? S : 256);
+    if (k2b < k2_min) k2b = k2_min;
     L.m = 0;
     L.top = L.m + pad16(8 * (C + 1) * S);
     L.k2 = L.top + pad16(8 * S2);
-    L.w1 = L.k2 + pad16(8 * S2);
+    L.w1 = L.k2 + pad16(k2b);
     L.q = L.w1 + pad16(4 * S);
     L.tq = L.q + pad16(4 * S);
     L.wr = L.tq + pad16(4 * S);
@@ -106,7 +118,9 @@ __host__ __device__ inline PoolLds pool_lds(int S, int C) {
 // The pool of one row from its support s_top (App. C.1), formed by NT
 // threads (tid < NT).  Children fields the frontier selection reads in other
 // blocks (token, score, path) are published with agent-scope atomics.
-template <int NT>
+// SORT_TAIL: order the tail by sorting (supports above kCountTailMax)
+// rather than by counting; both give the same order.
+template <int NT, bool SORT_TAIL>
 __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, int row,
                                           uint8_t* lds, const PoolLds& L, int pu,
                                           const ParentRec& pr, uint64_t u, uint64_t* s_red,
@@ -186,17 +200,52 @@ __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, 
     // ids and the q~ mass of the entries before it.  The tail is written to
     // the tree in that order (q~ for verification), and Y ~ q~_T is the
     // entry whose interval [mass before, mass before + q) holds
-    // t = floor(U64 Zq / 2^64): the inverse CDF over token ids.
+    // t = floor(U64 Zq / 2^64): the inverse CDF over token ids.  Small
+    // supports count, for every entry, the smaller ids and their mass;
+    // large ones sort the tail by id and take a prefix sum.
     const uint64_t tt = __umul64hi(u, Zq);
     const int64_t tail_base = ((int64_t)b * t.E + e_idx) * S;
-    rank_prefix<NT>(s_k2, s_q, S, [&](int i, int ir, uint64_t pre) {
-        if (s_k2[i] != 0ull) {
-            const uint32_t q = s_q[i];
-            t.tail_id[tail_base + ir] = key_id(s_top[i]);
-            t.tail_q[tail_base + ir] = q;
-            if (pre <= tt && tt - pre < (uint64_t)q) *s_yi = i;
+    if constexpr (!SORT_TAIL) {
+        rank_prefix<NT>(s_k2, s_q, S, [&](int i, int ir, uint64_t pre) {
+            if (s_k2[i] != 0ull) {
+                const uint32_t q = s_q[i];
+                t.tail_id[tail_base + ir] = key_id(s_top[i]);
+                t.tail_q[tail_base + ir] = q;
+                if (pre <= tt && tt - pre < (uint64_t)q) *s_yi = i;
+            }
+        });
+    } else {
+        // sort keys: the complement of (id, position) for the tail, so that
+        // the descending sort puts ids in ascending order; 0 (last) for the
+        // leads and the padding
+        const int n2 = pow2_at_least(S);
+        psync<NT>();
+        for (int i = tid; i < n2; i += NT) {
+            const bool tail = i < S && s_k2[i] != 0ull;
+            s_k2[i] = tail ? ~(((uint64_t)(uint32_t)key_id(s_top[i]) << 32) | (uint32_t)i) : 0ull;
         }
-    });
+        psync<NT>();
+        bitonic_sort_desc<NT>(s_k2, n2);
+        const int ntail = S - m;
+        const int per = n2 > NT ? n2 / NT : 1;       // sorted entries per thread
+        const int r0 = tid * per;
+        uint64_t mine = 0;
+        for (int r = r0; r < r0 + per; ++r)
+            if (r < ntail) mine += s_q[(uint32_t)~s_k2[r]];
+        uint64_t tot;
+        uint64_t pre = block_excl_scan_u64<NT>(mine, s_red, &tot);
+        for (int r = r0; r < r0 + per; ++r) {
+            if (r < ntail) {
+                const uint64_t kk = ~s_k2[r];
+                const int i = (int)(uint32_t)kk;
+                const uint32_t q = s_q[i];
+                t.tail_id[tail_base + r] = (int)(kk >> 32);
+                t.tail_q[tail_base + r] = q;
+                if (pre <= tt && tt - pre < (uint64_t)q) *s_yi = i;
+                pre += q;
+            }
+        }
+    }
     psync<NT>();
     int yi = *s_yi;
     if (yi < 0) {
@@ -276,6 +325,7 @@ __device__ __forceinline__ void row_parent(const TreeDev& t, const LevelArgs& a,
 // k_pool: one block per row: parent, support (merge of the chunk lists),
 // pool, and, by the last row of each sequence, the next frontier
 // ---------------------------------------------------------------------------
+template <bool SORT_TAIL>
 __global__ __launch_bounds__(NTP) void k_pool(TreeDev t, LevelArgs a) {
     extern __shared__ __align__(16) uint8_t s_pdyn[];
     __shared__ uint64_t s_red[2 * NTP / WAVE];
@@ -364,7 +414,7 @@ __global__ __launch_bounds__(NTP) void k_pool(TreeDev t, LevelArgs a) {
     __syncthreads();
 
     // the pool, formed by the whole block
-    pool_form<NTP>(t, a, row, s_pdyn, L, s_pu, pr, s_u, s_red, &s_yi);
+    pool_form<NTP, SORT_TAIL>(t, a, row, s_pdyn, L, s_pu, pr, s_u, s_red, &s_yi);
     if (level + 1 >= t.D) return;
 
     // the next frontier: the last row of the sequence to finish selects it
@@ -448,14 +498,16 @@ __device__ void rank_keys32(const uint32_t* keys, int n, int16_t* rank) {
     }
 }
 
-// h = the largest 16-bit code that at least nsel of the 2 * NT offered codes
-// (c1 and c2 of every thread) reach, four bits per round: each wave counts
-// its offers >= h | d << sh for d = 1..15 with ballots, lane d of the wave
-// stores that count, the waves' counts are added, and d is the largest one
-// whose count still reaches nsel.  s_cnt holds 2 * (NT / WAVE) * 16 ints.
-// Needs nsel <= 2 * NT; all threads of the block call it.
+// h = the largest 16-bit code that at least nsel of the offered codes reach
+// (c1 and c2 of every thread, and c3 and c4 too if `four`, a block-uniform
+// flag), four bits per round: each wave counts its offers >= h | d << sh
+// for d = 1..15 with ballots, lane d of the wave stores that count, the
+// waves' counts are added, and d is the largest one whose count still
+// reaches nsel.  s_cnt holds 2 * (NT / WAVE) * 16 ints.  Needs nsel <= the
+// number of offers; all threads of the block call it.
 template <int NT>
-__device__ __forceinline__ uint32_t offer_threshold(uint32_t c1, uint32_t c2, int nsel,
+__device__ __forceinline__ uint32_t offer_threshold(uint32_t c1, uint32_t c2, uint32_t c3,
+                                                    uint32_t c4, bool four, int nsel,
                                                     int* s_cnt) {
     constexpr int NW = NT / WAVE;
     const int lane = threadIdx.x % WAVE, wid = threadIdx.x / WAVE;
@@ -465,12 +517,24 @@ __device__ __forceinline__ uint32_t offer_threshold(uint32_t c1, uint32_t c2, in
         const int sh = 12 - 4 * r;
         int* buf = s_cnt + (r & 1) * NW * 16;
         uint32_t mine = 0;
+        if (four) {
 #pragma unroll
-        for (int d = 1; d < 16; ++d) {
-            const uint32_t cand = h | ((uint32_t)d << sh);
-            const uint32_t n = (uint32_t)(__popcll(__ballot(c1 >= cand)) +
-                                          __popcll(__ballot(c2 >= cand)));
-            mine = (lane == d) ? n : mine;
+            for (int d = 1; d < 16; ++d) {
+                const uint32_t cand = h | ((uint32_t)d << sh);
+                const uint32_t n = (uint32_t)(__popcll(__ballot(c1 >= cand)) +
+                                              __popcll(__ballot(c2 >= cand)) +
+                                              __popcll(__ballot(c3 >= cand)) +
+                                              __popcll(__ballot(c4 >= cand)));
+                mine = (lane == d) ? n : mine;
+            }
+        } else {
+#pragma unroll
+            for (int d = 1; d < 16; ++d) {
+                const uint32_t cand = h | ((uint32_t)d << sh);
+                const uint32_t n = (uint32_t)(__popcll(__ballot(c1 >= cand)) +
+                                              __popcll(__ballot(c2 >= cand)));
+                mine = (lane == d) ? n : mine;
+            }
         }
         if (lane < 16) buf[wid * 16 + lane] = (int)mine;
         __syncthreads();
@@ -484,6 +548,39 @@ __device__ __forceinline__ uint32_t offer_threshold(uint32_t c1, uint32_t c2, in
         h |= d << sh;
     }
     return h;
+}
+template <int NT>
+__device__ __forceinline__ uint32_t offer_threshold(uint32_t c1, uint32_t c2, int nsel,
+                                                    int* s_cnt) {
+    return offer_threshold<NT>(c1, c2, 0u, 0u, false, nsel, s_cnt);
+}
+
+// The largest bin b of a 256-bin histogram in LDS whose suffix count (bins
+// >= b) reaches need, and the count of the bins above it (.y); (-1, 0) if
+// none does.  Threads 0..255 hold one bin each; s_w holds 9 ints.  All
+// threads of the block call it; it ends with a barrier.
+template <int NT>
+__device__ __forceinline__ int2 suffix_pick256(const int* hist, int need, int* s_w) {
+    static_assert(NT >= 256, "one bin per thread");
+    const int t = threadIdx.x, lane = t % WAVE, w = t / WAVE;
+    const int v = (t < 256) ? hist[t] : 0;
+    const int ex = wave_excl_scan(v);
+    const int wt = (int)lane_u32((uint32_t)(ex + v), WAVE - 1);
+    if (t < 256 && lane == 0) s_w[w] = wt;
+    __syncthreads();
+    int higher = 0;
+    if (t < 256) {
+        for (int x = w + 1; x < 256 / WAVE; ++x) higher += s_w[x];
+    }
+    const int suf = wt - ex + higher;               // sum of bins >= t
+    const uint64_t ok = __ballot(t < 256 && suf >= need);
+    const int top = ok ? w * WAVE + 63 - __builtin_clzll(ok) : -1;
+    if (t < 256 && lane == 0) s_w[4 + w] = top;
+    __syncthreads();
+    const int bin = max(max(s_w[4], s_w[5]), max(s_w[6], s_w[7]));
+    if (t == bin) s_w[8] = suf - v;
+    __syncthreads();
+    return make_int2(bin, bin >= 0 ? s_w[8] : 0);
 }
 
 // Exact selection for a degenerate range: more candidates than LDS holds
@@ -642,6 +739,14 @@ __device__ void exact_select_fallback(const char* base, int V, int vfirst, uint3
         }
     }
     __syncthreads();
+}
+
+// The candidate count after exact_select_fallback (which ends with a
+// barrier): an atomic load behind a compiler barrier, since the call is not
+// inlined and a plain load of the counter may be scheduled before it.
+__device__ __forceinline__ int fallback_count(int* cnt) {
+    asm volatile("" ::: "memory");
+    return __hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
 template <int DT, int NVC>
@@ -869,7 +974,7 @@ __device__ __forceinline__ void select_block(const TreeDev& t, const LevelArgs& 
                 }
             },
             s_redi, s_tie);
-        cnt = min(s_cnt, CAPC);
+        cnt = min(fallback_count(&s_cnt), CAPC);
     }
 
     // exact top-nsel of the candidates, written sorted; unused slots are 0
@@ -889,25 +994,44 @@ __device__ __forceinline__ void select_block(const TreeDev& t, const LevelArgs& 
 // k_expand_row: the whole level for one row per block.  The row is streamed
 // once (double-buffered batches of 16-byte vectors; only each vector's
 // exact maximum is kept, as a 16-bit order code in registers); the
-// threshold comes from every thread's two largest vector maxima as in
-// k_select; only the candidate vectors are read again; their elements above
-// the threshold are ranked into the support, then the pool (App. C.1) and,
-// by the last row of each sequence, the next frontier -- with no chunk
-// lists, no merge and no second launch.  Used when the row fits NQ vectors
-// per thread and the level has enough rows to fill the chip.
+// threshold comes from the largest vector maxima every thread offers (two,
+// or four for supports above 128), and for supports above kCountTailMax
+// (LS) is raised to the exact S-th largest vector maximum by two rounds of
+// a 256-bin histogram; only the candidate vectors are read again; their
+// elements at or above the threshold are ranked (LS: sorted) into the
+// support, then the pool (App. C.1) and, by the last row of each sequence,
+// the next frontier -- with no chunk lists, no merge and no second launch.
+// Used when the row fits NQ vectors per thread and the level has enough
+// rows to fill the chip.
 // ---------------------------------------------------------------------------
-template <int DT, int NQ>
+constexpr int CAPV_L = 2048;  // candidate vectors of a large-support row
+constexpr int CAPC_L = 2048;  // candidates of a large-support row (sorted in place)
+
+// Dynamic LDS of k_expand_row: the pool layout; large supports sort their
+// candidates in the support region and list candidate vectors in the
+// ranking-key region, both free until the pool is formed.
+__host__ __device__ inline PoolLds row_lds(int S, bool ls) {
+    return ls ? pool_lds(S, 0, CAPC_L, 4 * CAPV_L) : pool_lds(S, 0);
+}
+
+// SC: the support class -- 0: S <= 128 (two offers per thread), 1: S <= 256
+// (four offers), 2: larger supports (LS).
+template <int DT, int NQ, int SC>
 __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
+    constexpr bool LS = SC == 2;
+    constexpr bool four = SC >= 1;
     constexpr int VEC = DT ? 8 : 4;
     constexpr int NW = NTE / WAVE;
     constexpr int NB = NQ / EBATCH;
     constexpr int NM = DT ? NQ / 2 : NQ;
+    constexpr int CV = LS ? CAPV_L : CAPV;      // candidate vectors held
+    constexpr int CC = LS ? CAPC_L : CAPC;      // candidates held
     static_assert(NQ % (2 * EBATCH) == 0 && NQ <= 32, "batches come in pairs");
-    static_assert(CAPV <= NTE, "one candidate vector per thread");
     extern __shared__ __align__(16) uint8_t s_pdyn[];
-    __shared__ __align__(16) uint64_t s_keys[CAPC];
-    __shared__ int16_t s_rank[CAPC];
-    __shared__ int s_cvi[CAPV];
+    __shared__ __align__(16) uint64_t s_keys_st[LS ? 2 : CAPC];
+    __shared__ int16_t s_rank[LS ? 2 : CAPC];
+    __shared__ int s_cvi_st[LS ? 1 : CAPV];
+    __shared__ int s_hist[LS ? 256 : 1];
     __shared__ int s_thr[2 * NW * 16];
     __shared__ int s_wn[NW];
     __shared__ int s_cnt;
@@ -916,9 +1040,11 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
     __shared__ int s_tie[32][NW];
     __shared__ int s_pu, s_yi;
     __shared__ uint64_t s_u;
-    const PoolLds L = pool_lds(t.S, 0);
+    const PoolLds L = row_lds(t.S, LS);
     uint64_t* s_top = (uint64_t*)(s_pdyn + L.top);
     uint64_t* s_k2 = (uint64_t*)(s_pdyn + L.k2);
+    uint64_t* s_keys = LS ? s_top : s_keys_st;
+    int* s_cvi = LS ? (int*)s_k2 : s_cvi_st;
 
     const int tid = threadIdx.x, lane = tid % WAVE, wid = tid / WAVE;
     const int row = blockIdx.x;
@@ -935,11 +1061,12 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
         row_parent(t, a, b, j, &s_pu, &s_u);
         s_cnt = 0;
     }
-    for (int i = tid; i < S; i += NTE) s_top[i] = 0ull;   // id -1 until ranked
+    if (!LS)
+        for (int i = tid; i < S; i += NTE) s_top[i] = 0ull;   // id -1 until ranked
 
     // ---- the row, streamed: vector q of this thread is tid + NTE * q ------
     uint32_t vm[NM];
-    uint32_t c1 = 0, c2 = 0;
+    uint32_t c1 = 0, c2 = 0, c3 = 0, c4 = 0;
     rs_ushort2 p1 = {0, 0}, p2 = {0, 0};
     const int wfirst = __builtin_amdgcn_readfirstlane(wid) * WAVE;
     auto load_batch = [&](uint4 (&r)[EBATCH], int bt) {
@@ -973,6 +1100,8 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
                                        fmaxf(elem<DT>(r[e], 2), elem<DT>(r[e], 3)));
                 vm[bt * EBATCH + e] = __float_as_uint(mx);
                 const uint32_t cv = ord32(mx) >> 16;
+                c4 = max(c4, min(c3, cv));
+                c3 = max(c3, min(c2, cv));
                 c2 = max(c2, min(c1, cv));
                 c1 = max(c1, cv);
             }
@@ -989,13 +1118,55 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
             proc_batch(rb, bt + 1);
         }
     }
+    // bf16: the two largest of each half (four distinct vectors)
     if (DT) {
-        c1 = max((uint32_t)p1.x, (uint32_t)p1.y);
-        c2 = max(min((uint32_t)p1.x, (uint32_t)p1.y), max((uint32_t)p2.x, (uint32_t)p2.y));
+        if constexpr (four) {
+            c1 = p1.x;
+            c2 = p1.y;
+            c3 = p2.x;
+            c4 = p2.y;
+        } else {
+            c1 = max((uint32_t)p1.x, (uint32_t)p1.y);
+            c2 = max(min((uint32_t)p1.x, (uint32_t)p1.y), max((uint32_t)p2.x, (uint32_t)p2.y));
+        }
     }
 
-    // ---- threshold: h = the nsel-th largest of the 2 * NTE offered codes
-    const uint32_t h = offer_threshold<NTE>(c1, c2, nsel, s_thr);
+    // ---- threshold: h = the nsel-th largest of the offered codes (a lower
+    //      bound of the nsel-th largest vector maximum)
+    uint32_t h = offer_threshold<NTE>(c1, c2, c3, c4, four, nsel, s_thr);
+    if constexpr (LS) {
+        // raised to the nsel-th largest vector maximum: the high byte of its
+        // code, then the low byte, from histograms of the codes >= h
+        auto code_of = [&](int q) -> uint32_t {
+            if (DT) {
+                const rs_ushort2 c = bf16x2_codes(vm[q / 2]);
+                return (q & 1) ? (uint32_t)c.y : (uint32_t)c.x;
+            }
+            return ord32(__uint_as_float(vm[q])) >> 16;
+        };
+        for (int i = tid; i < 256; i += NTE) s_hist[i] = 0;
+        __syncthreads();
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+            const uint32_t c = code_of(q);
+            if (c >= h && tid + NTE * q < NVR) atomicAdd(&s_hist[c >> 8], 1);
+        }
+        __syncthreads();
+        const int2 hi8 = suffix_pick256<NTE>(s_hist, nsel, s_thr);
+        if (hi8.x >= 0) {
+            for (int i = tid; i < 256; i += NTE) s_hist[i] = 0;
+            __syncthreads();
+#pragma unroll
+            for (int q = 0; q < NQ; ++q) {
+                const uint32_t c = code_of(q);
+                if (c >= h && (int)(c >> 8) == hi8.x && tid + NTE * q < NVR)
+                    atomicAdd(&s_hist[c & 0xFFu], 1);
+            }
+            __syncthreads();
+            const int2 lo8 = suffix_pick256<NTE>(s_hist, nsel - hi8.y, s_thr);
+            if (lo8.x >= 0) h = max(h, ((uint32_t)hi8.x << 8) | (uint32_t)lo8.x);
+        }
+    }
     // the parent record, for the children written at the end
     const ParentRec pr = (tid < K) ? parent_rec(t, level, nb, s_pu) : ParentRec{1.0, 0ull};
     const float tau = (h << 16) > ord32(-INFINITY) ? unord32(h << 16) : -INFINITY;
@@ -1004,7 +1175,7 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
     //      of its own to its region of s_cvi; if a wave has more than its
     //      region holds, but all fit, they are written again into one list
     //      with slots reserved per wave
-    constexpr int WCAPR = CAPV / NW;
+    constexpr int WCAPR = CV / NW;
     auto vmax_of = [&](int q) -> float {
         return DT ? ((q & 1) ? bf_hi(vm[q / 2]) : bf_lo(vm[q / 2])) : __uint_as_float(vm[q]);
     };
@@ -1034,7 +1205,7 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
         wbefore += (w < wid) ? wn[w] : 0;
         nv += wn[w];
     }
-    const bool contig = ovf && nv <= CAPV;
+    const bool contig = ovf && nv <= CV;
     if (contig) {
         int wpos = wbefore;
 #pragma unroll
@@ -1051,13 +1222,14 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
         }
         __syncthreads();
     }
-    // ---- their elements >= tau (one candidate vector per thread, read again)
-    if (!ovf || contig) {
+    // ---- their elements >= tau (candidate vectors read again, one per
+    //      thread and round; small supports have a single round)
+    auto gather = [&](int e) {
         uint4 x = make_uint4(0, 0, 0, 0);
         int e0 = V;
-        if (tid < nv) {
-            // entry tid of the concatenated regions (or of the one list)
-            int w = 0, off = tid;
+        if (e < nv) {
+            // entry e of the concatenated regions (or of the one list)
+            int w = 0, off = e;
             if (!contig) {
 #pragma unroll
                 for (int q = 0; q < NW - 1; ++q) {
@@ -1081,36 +1253,51 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
         for (int k = 0; k < VEC; ++k) {
             const float v = elem<DT>(x, k);
             if (v >= tau && e0 + k < V) {
-                if (pos < CAPC) s_keys[pos] = logit_key(v, (uint32_t)(e0 + k));
+                if (pos < CC) s_keys[pos] = logit_key(v, (uint32_t)(e0 + k));
                 ++pos;
             }
         }
+    };
+    if (!ovf || contig) {
+        if constexpr (LS) {
+            for (int e = tid; e - tid < nv; e += NTE) gather(e);
+        } else {
+            gather(tid);                          // nv <= CAPV <= NTE
+        }
     } else if (tid == 0) {
-        s_cnt = CAPC + 1;                        // too many: exact fallback below
+        s_cnt = CC + 1;                          // too many: exact fallback below
     }
     __syncthreads();
     int cnt = s_cnt;
-    if (cnt > CAPC) {
+    if (cnt > CC) {
         __syncthreads();
         if (tid == 0) s_cnt = 0;
         exact_select_fallback<DT, NTE, NQ>(
-            base, V, 0, h, nsel, CAPC,
-            [&](float v, int id) {
+            base, V, 0, h, nsel, CC,
+            [=](float v, int id) {
                 const int pos = atomicAdd(&s_cnt, 1);
-                if (pos < CAPC) s_keys[pos] = logit_key(v, (uint32_t)id);
+                if (pos < CC) s_keys[pos] = logit_key(v, (uint32_t)id);
             },
             s_redi, s_tie);
-        cnt = min(s_cnt, CAPC);
+        cnt = min(fallback_count(&s_cnt), CC);
     }
 
     // ---- the support: the top nsel candidates in (logit desc, id asc) order
-    rank_keys<NTE>(s_keys, cnt, s_rank);
-    __syncthreads();
-    for (int i = tid; i < cnt; i += NTE) {
-        const int rk = s_rank[i];
-        if (rk < nsel) s_top[rk] = s_keys[i];
+    if constexpr (LS) {
+        // sorted in place (padding 0 sorts last; at least nsel entries)
+        const int n2 = pow2_at_least(max(cnt, nsel));
+        for (int i = cnt + tid; i < n2; i += NTE) s_keys[i] = 0ull;
+        __syncthreads();
+        bitonic_sort_desc<NTE>(s_keys, n2);
+    } else {
+        rank_keys<NTE>(s_keys, cnt, s_rank);
+        __syncthreads();
+        for (int i = tid; i < cnt; i += NTE) {
+            const int rk = s_rank[i];
+            if (rk < nsel) s_top[rk] = s_keys[i];
+        }
+        __syncthreads();
     }
-    __syncthreads();
     for (int i = tid; i < S; i += NTE) {
         if ((uint32_t)key_id(s_top[i]) >= (uint32_t)V) {   // a support slot left empty
             atomicOr(t.err, 256);
@@ -1119,7 +1306,7 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
     }
     __syncthreads();
 
-    pool_form<NTE>(t, a, row, s_pdyn, L, s_pu, pr, s_u, s_red, &s_yi);
+    pool_form<NTE, LS>(t, a, row, s_pdyn, L, s_pu, pr, s_u, s_red, &s_yi);
     if (level + 1 >= t.D) return;
     select_frontier(t, a, b, s_top, s_k2);
 }
@@ -1173,7 +1360,9 @@ hipError_t launch_select(const TreeDev& t, const LevelArgs& a, int variant, hipS
 hipError_t launch_expand(const TreeDev& t, const LevelArgs& a, int variant, hipStream_t s) {
     hipError_t e = launch_select(t, a, variant, s);
     if (e != hipSuccess) return e;
-    k_pool<<<t.B * a.P, NTP, (size_t)pool_lds(t.S, t.C).bytes, s>>>(t, a);
+    const size_t shm = (size_t)pool_lds(t.S, t.C).bytes;
+    if (t.S > kCountTailMax) k_pool<true><<<t.B * a.P, NTP, shm, s>>>(t, a);
+    else k_pool<false><<<t.B * a.P, NTP, shm, s>>>(t, a);
     return hipGetLastError();
 }
 
@@ -1188,20 +1377,26 @@ int expand_row_nq(int dtype, int V) {
     return 0;
 }
 
+template <int DT, int SC>
+static hipError_t launch_row(const TreeDev& t, const LevelArgs& a, int nq, hipStream_t s) {
+    const dim3 grid(t.B * a.P);
+    const size_t shm = (size_t)row_lds(t.S, SC == 2).bytes;
+    if (nq == 16) k_expand_row<DT, 16, SC><<<grid, NTE, shm, s>>>(t, a);
+    else if (nq == 32) k_expand_row<DT, 32, SC><<<grid, NTE, shm, s>>>(t, a);
+    else return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
+template <int DT>
+static hipError_t launch_row_dt(const TreeDev& t, const LevelArgs& a, int nq, hipStream_t s) {
+    if (t.S > kCountTailMax) return launch_row<DT, 2>(t, a, nq, s);
+    if (t.S > NTE / 4) return launch_row<DT, 1>(t, a, nq, s);
+    return launch_row<DT, 0>(t, a, nq, s);
+}
+
 hipError_t launch_expand_row(const TreeDev& t, const LevelArgs& a, hipStream_t s) {
     const int nq = expand_row_nq(t.dtype, t.V);
-    const dim3 grid(t.B * a.P);
-    const size_t shm = (size_t)pool_lds(t.S, 0).bytes;
-    if (t.dtype) {
-        if (nq == 16) k_expand_row<1, 16><<<grid, NTE, shm, s>>>(t, a);
-        else if (nq == 32) k_expand_row<1, 32><<<grid, NTE, shm, s>>>(t, a);
-        else return hipErrorInvalidValue;
-    } else {
-        if (nq == 16) k_expand_row<0, 16><<<grid, NTE, shm, s>>>(t, a);
-        else if (nq == 32) k_expand_row<0, 32><<<grid, NTE, shm, s>>>(t, a);
-        else return hipErrorInvalidValue;
-    }
-    return hipGetLastError();
+    return t.dtype ? launch_row_dt<1>(t, a, nq, s) : launch_row_dt<0>(t, a, nq, s);
 }
 
 }  // namespace rheo

@@ -106,6 +106,37 @@ __device__ __forceinline__ void psync() {
     if (NT == WAVE) wave_sync();
     else __syncthreads();
 }
+
+// Descending bitonic sort of n 64-bit keys in LDS (n a power of two) by NT
+// threads; the caller has synchronised after writing the keys, and the sort
+// ends with a barrier.  Compare-exchange pair i of a stage with distance j
+// joins positions lo = ((i & ~(j - 1)) << 1) | (i & (j - 1)) and lo + j;
+// for j <= WAVE every position a wave touches lies in the 2 * WAVE-wide
+// window of its own pair indices, so consecutive such stages only need the
+// wave's own accesses ordered.
+template <int NT>
+__device__ __forceinline__ void bitonic_sort_desc(uint64_t* k, int n) {
+    const int tid = threadIdx.x % NT;
+    const int half = n >> 1;
+    for (int kk = 2; kk <= n; kk <<= 1) {
+        for (int j = kk >> 1; j > 0; j >>= 1) {
+            for (int i = tid; i < half; i += NT) {
+                const int lo = ((i & ~(j - 1)) << 1) | (i & (j - 1));
+                const int hi = lo + j;
+                const uint64_t x = k[lo], y = k[hi];
+                const bool desc = (lo & kk) == 0;
+                if ((x < y) == desc) {
+                    k[lo] = y;
+                    k[hi] = x;
+                }
+            }
+            const int jn = (j > 1) ? (j >> 1) : kk;      // the next stage's distance
+            if (j > WAVE || jn > WAVE) psync<NT>();
+            else wave_sync();
+        }
+    }
+    psync<NT>();
+}
 template <int NT>
 __device__ __forceinline__ uint64_t psum(uint64_t v, uint64_t* sh) {
     if (NT == WAVE) return wave_sum_u64(v);

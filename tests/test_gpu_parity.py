@@ -107,6 +107,11 @@ def test_tiny_variants(dev, over):
     dict(V=4099, dtype="f32", recipe="zipf_t3", support=64, K=6, depth=5, R=40, B=2),
     dict(V=128256, dtype="bf16", recipe="zipf", support=512, K=8, depth=2, R=10),
     dict(V=70001, dtype="bf16", recipe="zipf", quantum=2.0, support=128, K=4, depth=2, R=6),
+    # supports above 256: the whole row as the support, a support that is
+    # no power of two, and massive ties at the threshold
+    dict(V=1003, dtype="bf16", recipe="zipf", support=1024, K=5, depth=3, R=12),
+    dict(V=300, dtype="f32", recipe="zipf", support=300, K=4, depth=3, R=12),
+    dict(V=32000, dtype="bf16", recipe="zipf", quantum=0.5, support=700, K=6, depth=3, R=20),
 ])
 @pytest.mark.parametrize("row", ["auto", "1"])
 def test_edge_shapes(dev, over, row):
@@ -140,12 +145,20 @@ def test_headline(dev):
     run_parity(W["headline"], [0, 1], [0, 31, 63], dev=dev)
 
 
-@pytest.mark.parametrize("support", [256, 1024])
+@pytest.mark.parametrize("support", [256, 512, 1024])
 def test_headline_supports(dev, support):
     # the larger sparse supports (Sec. 5.5) at the batched shape, where
     # every level runs one block per row
     w = W["headline"].with_(name=f"headline_s{support}", support=support, depth=4, R=30)
     run_parity(w, [0], [0, 63], dev=dev)
+
+
+def test_support_fallback_rows(dev):
+    # sequences 30 and 40 of step 2 at support 256 each hold a row whose
+    # candidates overflow LDS (exact re-selection from the row), once
+    # miscounted after the out-of-line fallback
+    w = W["headline"].with_(name="headline_s256", support=256)
+    run_parity(w, [2], [30, 40], dev=dev)
 
 
 SHAPES = (
