@@ -15,6 +15,7 @@ from .drivers import run_philox
 def tree_config(w, **over):
     kw = dict(K=w.K, m=w.m, depth=w.depth, n_expand=w.n_expand,
               support=w.support, construct_tempered=w.construct_tempered,
+              construct_full=w.construct_full,
               eps=w.eps_m0, mode="topk" if w.method == "topk" else "rheo",
               verifier="rrsw" if w.method == "rrsw" else "rheo")
     kw.update(over)
@@ -51,7 +52,8 @@ def oracle_step(w, b, step, T=None, trace=None, model="canonical", cfg=None,
             cache[("d", key)] = synth.as_fp32_numpy(synth.draft_rows(w, [key]))[0]
         row = cache[("d", key)]
         return rheo.node_dist_from_logits(row, cfg.m, T, cfg.support,
-                                          cfg.construct_tempered, model)
+                                          cfg.construct_tempered, model,
+                                          cfg.construct_full)
 
     holder = {}
 

@@ -177,7 +177,8 @@ class NodeDist:
     support  token ids of the draft support, in rank order x_1, x_2, ...
              (construction probability descending, token id ascending)
     w1       construction weights (untempered q) in the same order
-    s1       sum of w1: q(x_i) = w1[i] / s1
+    s1       total construction weight, q(x_i) = w1[i] / s1: the sum of w1
+             (or of every token's weight, for the whole-vocabulary reading)
     tail     q~ restricted to the support minus the top-m tokens, as an
              ExplicitDist of tempered weights; q~(v) = weight / total
     """
@@ -194,7 +195,7 @@ def rank_order(ids, weights):
 
 
 def node_dist_from_logits(logits, m, T, support_size=0, construct_tempered=False,
-                          model="canonical"):
+                          model="canonical", construct_full=False):
     """Build the node's distributions from one row of draft logits.
 
     support_size S > 0 truncates the logits to the S largest entries (ties by
@@ -202,7 +203,13 @@ def node_dist_from_logits(logits, m, T, support_size=0, construct_tempered=False
     The construction distribution q is untempered unless
     ``construct_tempered`` (Sec. 5.4).  The tail q~ = q_T / z on the support
     minus x_1..x_m (App. C.1) is evaluated relative to the logit of x_{m+1},
-    so its largest weight is 2**30 and its total never vanishes."""
+    so its largest weight is 2**30 and its total never vanishes.
+
+    ``construct_full``: the other reading of the sparse mode, where the
+    truncation touches only the sampled token (Sec. 5.5, discussion of
+    Table 5): the construction softmax runs over the whole vocabulary (its
+    total s1 sums every token's weight; the support's weights and order are
+    the same), while the tail q~ stays on the support."""
     l = np.asarray(logits, dtype=np.float32)
     V = l.shape[0]
     ids = np.arange(V, dtype=np.int64)
@@ -219,13 +226,19 @@ def node_dist_from_logits(logits, m, T, support_size=0, construct_tempered=False
     r = rank_order(list(sup), w)
     support = [int(sup[i]) for i in r]
     w1 = [w[i] for i in r]
+    s1 = sum(w1)
+    if construct_full and len(sup) < V:
+        if model == "canonical":
+            s1 = sum(int(x) for x in numerics.canonical_weights(l, ref, Tc))
+        else:
+            s1 = sum(numerics.fp64_weights(l, ref, Tc))
     tail_ids = support[m:]
     ref_t = l[tail_ids[0]]
     if model == "canonical":
         q = [int(x) for x in numerics.canonical_weights(l[tail_ids], ref_t, T)]
     else:
         q = numerics.fp64_weights(l[tail_ids], ref_t, T)
-    return NodeDist(support, w1, sum(w1), ExplicitDist(tail_ids, q))
+    return NodeDist(support, w1, s1, ExplicitDist(tail_ids, q))
 
 
 def node_dist_from_weights(ids, w1, q_tail=None, m=1):
@@ -338,6 +351,7 @@ class TreeConfig:
     n_expand: int = None
     support: int = 0
     construct_tempered: bool = False
+    construct_full: bool = False  # construction over the whole vocabulary, sparse tail
     eps: float = 2.0 ** -40
     mode: str = "rheo"           # "rheo" or "topk" (pure top-K baseline)
     verifier: str = "rheo"       # "rheo" (Algorithm 1) or "rrsw" (App. D.2 baseline)

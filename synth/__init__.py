@@ -78,6 +78,7 @@ class Workload:
     seed: int = 0x5EED0000
     n_expand: int = None
     construct_tempered: bool = False
+    construct_full: bool = False
     method: str = "rheo"        # "rheo" (Algorithm 1), "rrsw" (leads-first
                                 # baseline, App. D.2) or "topk" (no sampled slot)
     eps_m0: float = 2.0 ** -40

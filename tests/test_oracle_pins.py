@@ -360,7 +360,8 @@ def _one_step(cfg, T, R, pre, lf, model, cache):
         k = ("d", pre + _path(nodes, node.uid))
         if k not in cache:
             cache[k] = rheo.node_dist_from_logits(
-                lf(*k), cfg.m, T, cfg.support, cfg.construct_tempered, model)
+                lf(*k), cfg.m, T, cfg.support, cfg.construct_tempered, model,
+                cfg.construct_full)
         return cache[k]
     holder = {}
 
@@ -448,14 +449,23 @@ LOSSLESS_CASES += [
     (5, 2, 1, 2, 2, 0.5, 0, False, "canonical", 2, "topk"),
 ]
 
+# the whole-vocabulary construction reading of the sparse mode (Sec. 5.5):
+# only the proxies change, so the output stays the target's
+LOSSLESS_CASES += [
+    (6, 3, 1, 2, 4, 1.0, 4, False, "canonical", 2, "rheo", True),
+    (6, 3, 0, 2, 5, 0.6, 3, True, "canonical", 2, "rheo", True),
+    (5, 3, 1, 2, 4, 1.0, 3, False, "canonical", 2, "rrsw", True),
+]
+
 
 @pytest.mark.parametrize("case", LOSSLESS_CASES)
 def test_thm1_lossless_by_enumeration(case):
     V, K, m, D, R, T, S, tempered, model, L = case[:10]
     method = case[10] if len(case) > 10 else "rheo"
+    full = case[11] if len(case) > 11 else False
     lf = _logits_fn(hash(case[:10]) & 0xFFFF, V)
     cfg = rheo.TreeConfig(K=K, m=m, depth=D, n_expand=min(K, 2), support=S,
-                          construct_tempered=tempered, model=model,
+                          construct_tempered=tempered, construct_full=full, model=model,
                           mode="topk" if method == "topk" else "rheo",
                           verifier="rrsw" if method == "rrsw" else "rheo")
     dist = _multi_step_dist(cfg, T, R, L, lf, model)
@@ -655,3 +665,28 @@ def test_harness_applies_the_method():
                 if idx % 32 == 0 and any(j // 32 == idx // 32 for j in tests[:i]):
                     seen[method] = True
     assert seen == {"rheo": False, "rrsw": True}
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_whole_vocabulary_construction(seed):
+    # Sec. 5.5 reading: construction over all of V, sampling on the top S.
+    rng = np.random.default_rng(700 + seed)
+    V, S, m, T = 40, 8, 1, 0.8
+    l = (rng.normal(0, 2.0, V)).astype(np.float32)
+    sparse = rheo.node_dist_from_logits(l, m, T, S)
+    full = rheo.node_dist_from_logits(l, m, T, S, construct_full=True)
+    dense = rheo.node_dist_from_logits(l, m, T, 0)
+    # the support, its weights, order and tail are those of the sparse node
+    assert full.support == sparse.support and full.w1 == sparse.w1
+    assert full.tail.ids == sparse.tail.ids and full.tail.weights == sparse.tail.weights
+    # the total is the dense node's, so q(x_i) are whole-vocabulary probabilities
+    assert full.s1 == dense.s1 and full.support == dense.support[:S]
+    assert full.w1 == dense.w1[:S]
+    ex = np.exp(l.astype(np.float64) - l.max())
+    for i, v in enumerate(full.support):
+        q = full.w1[i] / full.s1
+        assert abs(q - ex[v] / ex.sum()) <= 1e-6
+    # at S = V the two readings coincide
+    a = rheo.node_dist_from_logits(l, m, T, V, construct_full=True)
+    b = rheo.node_dist_from_logits(l, m, T, V)
+    assert a.s1 == b.s1 and a.w1 == b.w1
