@@ -12,6 +12,8 @@ import json
 import os
 from fractions import Fraction
 
+import zlib
+
 import numpy as np
 import pytest
 
@@ -463,7 +465,8 @@ def test_thm1_lossless_by_enumeration(case):
     V, K, m, D, R, T, S, tempered, model, L = case[:10]
     method = case[10] if len(case) > 10 else "rheo"
     full = case[11] if len(case) > 11 else False
-    lf = _logits_fn(hash(case[:10]) & 0xFFFF, V)
+    # a seed that does not depend on the interpreter's string hashing
+    lf = _logits_fn(zlib.crc32(repr(case[:10]).encode()) & 0xFFFF, V)
     cfg = rheo.TreeConfig(K=K, m=m, depth=D, n_expand=min(K, 2), support=S,
                           construct_tempered=tempered, construct_full=full, model=model,
                           mode="topk" if method == "topk" else "rheo",
