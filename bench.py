@@ -360,7 +360,8 @@ def run_sweep(args):
       rheostat  tau over the leads m and the temperature T (Sec. 5.4);
       support   sparse support S (and the dense tree): top-S coverage of the
                 untempered draft distribution, expand-level time, tau
-                (Sec. 5.5, Table 5).
+                (Sec. 5.5, Table 5); also two supports with the construction
+                over the whole vocabulary (the tail still sparse).
     Acceptance and tau come from the GPU path itself on seeded steps."""
     import torch
     import synth
@@ -405,8 +406,9 @@ def run_sweep(args):
                 emit("rheostat", {"m": m, "T": T, "K": w.K, "depth": w.depth},
                      steps_stats(w, 4))
     else:
-        for S in (128, 256, 512, 1024, 0):
-            w = base.with_(name="support", support=S)
+        for S, full in ((128, False), (256, False), (512, False), (1024, False), (0, False),
+                        (128, True), (1024, True)):
+            w = base.with_(name="support", support=S, construct_full=full)
             res = steps_stats(w, 6)
             # coverage of the top-S entries under the untempered draft
             # softmax, over the root rows and one level of frontier rows
@@ -438,7 +440,8 @@ def run_sweep(args):
             lvl = sum(a.elapsed_time(b) for a, b in ev) * 1e3 / len(ev)
             assert tree.device_error() == 0
             tree.close()
-            emit("support", {"support": S if S > 0 else "full", "K": w.K, "depth": w.depth},
+            emit("support", {"support": S if S > 0 else "full", "construct_full": full,
+                             "K": w.K, "depth": w.depth},
                  {**res, "coverage": round(cov, 4), "expand_level_us": round(lvl, 2)})
 
 

@@ -94,6 +94,13 @@ typedef struct rheo_config {
                                     norm(max(0, r - q~)) (App. D.2);
                                     RHEO_METHOD_TOPK: pure top-K pools, no sampled
                                     slot (Sec. 2.1), sequential tests under p        */
+    int32_t construct_full;      /* sparse mode: 0 builds the tree on q truncated to
+                                    the support (Sec. 3.2); 1 on q over the whole
+                                    vocabulary, the support then limiting only the
+                                    sampled token's tail q~ and verification (the
+                                    reading of Sec. 5.5 that truncation touches only
+                                    the sampled token).  Costs one extra read of each
+                                    draft row.  0 or 1; no effect in dense mode     */
     int64_t row_stride;          /* elements between consecutive logit rows (>= V)     */
     double eps_m0;               /* epsilon of the m = 0 proxy q(x_1) + eps (Sec. 3.2);
                                     0 selects 2^-40                                     */

@@ -34,6 +34,7 @@ class RheoConfig(ctypes.Structure):
                 ("depth", ctypes.c_int32), ("n_expand", ctypes.c_int32),
                 ("support", ctypes.c_int32), ("construct_tempered", ctypes.c_int32),
                 ("dtype", ctypes.c_int32), ("method", ctypes.c_int32),
+                ("construct_full", ctypes.c_int32),
                 ("row_stride", ctypes.c_int64), ("eps_m0", ctypes.c_double)]
 
 
@@ -112,7 +113,7 @@ class Tree:
 
     def __init__(self, batch, vocab, pool, leads, depth, support, dtype,
                  n_expand=0, construct_tempered=False, row_stride=None,
-                 eps_m0=0.0, method="rheo", device="cuda"):
+                 eps_m0=0.0, method="rheo", construct_full=False, device="cuda"):
         lib = load_library()
         self.device = torch.device(device)
         self.B, self.V, self.K, self.m, self.D = batch, vocab, pool, leads, depth
@@ -123,7 +124,7 @@ class Tree:
                          int(construct_tempered),
                          RHEO_BF16 if dtype == torch.bfloat16 else RHEO_F32,
                          METHODS[method] if isinstance(method, str) else int(method),
-                         self.row_stride, eps_m0)
+                         int(construct_full), self.row_stride, eps_m0)
         h = ctypes.c_void_p()
         _check(lib.rheo_create(ctypes.byref(cfg), ctypes.byref(h)))
         self._h = h

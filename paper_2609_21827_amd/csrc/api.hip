@@ -118,6 +118,8 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
     if (c.dtype != RHEO_F32 && c.dtype != RHEO_BF16) return fail(RHEO_EINVAL, "unknown dtype");
     if (c.method < RHEO_METHOD_RHEO || c.method > RHEO_METHOD_TOPK)
         return fail(RHEO_EINVAL, "unknown method %d", c.method);
+    if (c.construct_full != 0 && c.construct_full != 1)
+        return fail(RHEO_EINVAL, "construct_full must be 0 or 1");
     // support <= 0: dense mode, the support is the whole vocabulary
     const bool dense = c.support <= 0;
     const int S = dense ? c.vocab : (c.support < c.vocab ? c.support : c.vocab);
@@ -141,6 +143,8 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
     d.rrsw = c.method == RHEO_METHOD_RRSW;
     d.topk = c.method == RHEO_METHOD_TOPK;
     d.dense = dense ? 1 : 0;
+    // a support of the whole vocabulary already constructs over all of it
+    d.cfull = (!dense && c.construct_full && S < c.vocab) ? 1 : 0;
     d.NCH = (c.vocab + WAVE_TOKENS(c.dtype) - 1) / WAVE_TOKENS(c.dtype);
     d.eps = c.eps_m0;
     d.NN = 1 + c.pool + (c.depth - 1) * c.n_expand * c.pool;
@@ -208,6 +212,7 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
     rc = rc ? rc : dalloc(t, &d.dref, DN ? B * E : 1);
     rc = rc ? rc : dalloc(t, &d.dleads, DN ? B * E * 16 : 1);
     rc = rc ? rc : dalloc(t, &d.zq, B * E);
+    rc = rc ? rc : dalloc(t, &d.s1row, d.cfull ? B * d.NE : 1);
     rc = rc ? rc : dalloc(t, &d.frontier, B * d.NE);
     rc = rc ? rc : dalloc(t, &d.fr_u, B * d.NE);
     rc = rc ? rc : dalloc(t, &d.fr_parent, B * d.NE);
@@ -285,7 +290,12 @@ int rheo_expand_level(rheo_tree* t, const void* logits, float T, uint64_t key, v
     a.k1 = k_of_T(t->cfg.construct_tempered ? T : 1.0f);
     a.kT = k_of_T(T);
     a.rng_key = key;
-    hipError_t e;
+    hipError_t e = hipSuccess;
+    if (t->dev.cfull) {
+        // the construction totals over the whole rows, read by the pools
+        e = launch_row_wsum(t->dev, a, (hipStream_t)stream);
+        if (e != hipSuccess) return hip_fail(e, "row total launch");
+    }
     if (t->dev.dense) {
         e = launch_select(t->dev, a, t->variant, (hipStream_t)stream);
         if (e == hipSuccess)

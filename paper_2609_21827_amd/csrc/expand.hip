@@ -166,6 +166,7 @@ __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, 
     }
     uint64_t S1, Zq;
     psum2<NT>(part1, partq, s_red, &S1, &Zq);
+    if (t.cfull) S1 = t.s1row[row];          // construction over the whole vocabulary
     if (NT == WAVE) wave_sync();             // (a block sum has synchronised)
     bool tie = false;
     for (int i = tid + 1; i < S; i += NT)
@@ -1367,6 +1368,50 @@ hipError_t launch_expand(const TreeDev& t, const LevelArgs& a, int variant, hipS
 }
 
 int expand_variant_nvc(int v) { return kNVC[v]; }
+
+// ---------------------------------------------------------------------------
+// k_row_wsum: for the whole-vocabulary construction of a sparse tree, the
+// total construction weight of every row of the level, sum over all V of
+// w(l; M, k1) with M the row maximum (the same weights the pool computes
+// on its support).  One block per row, two passes over the row: the
+// maximum, then the weights.
+// ---------------------------------------------------------------------------
+constexpr int NTW = 256;
+
+template <int DT>
+__global__ __launch_bounds__(NTW) void k_row_wsum(TreeDev t, LevelArgs a) {
+    constexpr int VEC = DT ? 8 : 4;
+    __shared__ float s_max[NTW / WAVE];
+    __shared__ uint64_t s_sum[NTW / WAVE];
+    const int row = blockIdx.x;
+    const int V = t.V;
+    const int NVR = (V + VEC - 1) / VEC;
+    const char* base = (const char*)a.logits + (int64_t)row * t.stride * (DT ? 2 : 4);
+    float mx = -INFINITY;
+    for (int vi = threadIdx.x; vi < NVR; vi += NTW) {
+        const uint4 x = load_row_vec<DT>(base, vi, V);
+#pragma unroll
+        for (int k = 0; k < VEC; ++k)
+            if (vi * VEC + k < V) mx = fmaxf(mx, elem<DT>(x, k));
+    }
+    const float M = block_max<NTW>(mx, s_max);
+    uint64_t sum = 0;
+    for (int vi = threadIdx.x; vi < NVR; vi += NTW) {
+        const uint4 x = load_row_vec<DT>(base, vi, V);
+#pragma unroll
+        for (int k = 0; k < VEC; ++k)
+            if (vi * VEC + k < V) sum += cweight(elem<DT>(x, k), M, a.k1);
+    }
+    sum = block_sum_u64<NTW>(sum, s_sum);
+    if (threadIdx.x == 0) t.s1row[row] = sum;
+}
+
+hipError_t launch_row_wsum(const TreeDev& t, const LevelArgs& a, hipStream_t s) {
+    const dim3 grid(t.B * a.P);
+    if (t.dtype) k_row_wsum<1><<<grid, NTW, 0, s>>>(t, a);
+    else k_row_wsum<0><<<grid, NTW, 0, s>>>(t, a);
+    return hipGetLastError();
+}
 
 // Vectors per thread k_expand_row needs for a row of V elements (16 or 32),
 // or 0 if the row is too long for it.

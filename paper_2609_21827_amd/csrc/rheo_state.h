@@ -64,6 +64,8 @@ struct TreeDev {
     int C, Sc;
     int rrsw;                      // verification leads first (App. D.2)
     int topk;                      // pure top-K pools, no sampled slot
+    int cfull;                     // construction over the whole vocabulary (sparse)
+    uint64_t* s1row;               // [B * NE]: its total per row of the level
 };
 
 struct LevelArgs {
@@ -105,6 +107,7 @@ struct ExpandVariant {
     bool ok;                       // the row's C * Sc keys fit the merge
 };
 hipError_t launch_expand_row(const TreeDev& t, const LevelArgs& a, hipStream_t s);
+hipError_t launch_row_wsum(const TreeDev& t, const LevelArgs& a, hipStream_t s);
 int expand_row_nq(int dtype, int V);
 int expand_variant_count(int dtype);
 int expand_variant_nvc(int v);

@@ -19,6 +19,7 @@ def make_tree(w, device="cuda", **over):
     kw = dict(batch=w.B, vocab=w.V, pool=w.K, leads=w.m, depth=w.depth,
               support=w.support, n_expand=w.n_expand,
               construct_tempered=w.construct_tempered, eps_m0=w.eps_m0, method=w.method,
+              construct_full=w.construct_full,
               dtype=torch.bfloat16 if w.dtype == "bf16" else torch.float32,
               device=device)
     kw.update(over)

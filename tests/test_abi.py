@@ -37,7 +37,7 @@ def _cfg(**kw):
     from paper_2609_21827_amd.binding import RheoConfig
     base = dict(batch=2, vocab=1000, pool=4, leads=1, depth=3, n_expand=0,
                 support=128, construct_tempered=0, dtype=1, method=0,
-                row_stride=1000, eps_m0=0.0)
+                construct_full=0, row_stride=1000, eps_m0=0.0)
     base.update(kw)
     return RheoConfig(**base)
 
@@ -46,6 +46,7 @@ BAD = [
     dict(batch=0), dict(vocab=1), dict(vocab=262144), dict(pool=0), dict(pool=16),
     dict(leads=4), dict(leads=-1), dict(depth=0), dict(depth=16),
     dict(n_expand=5), dict(dtype=7), dict(method=3), dict(method=-1), dict(support=0, vocab=3, row_stride=8),
+    dict(construct_full=2), dict(construct_full=-1),
     dict(support=3), dict(vocab=5000, row_stride=5000, support=2000), dict(row_stride=999),
     dict(row_stride=1001), dict(eps_m0=-1.0),
     dict(vocab=3, support=3, pool=4),

@@ -161,6 +161,26 @@ def test_support_fallback_rows(dev):
     run_parity(w, [2], [30, 40], dev=dev)
 
 
+# ---- whole-vocabulary construction with a sparse tail (Sec. 5.5 reading)
+@pytest.mark.parametrize("over", [dict(support=16), dict(support=16, construct_tempered=True, T=0.6),
+                                  dict(support=8, m=0, K=4, R=10)])
+def test_construct_full_tiny(dev, over):
+    w = W["tiny"].with_(name="tiny_full", construct_full=True, **over)
+    run_parity(w, range(30), [0], dev=dev)
+
+
+def test_construct_full_llama2(dev):
+    run_parity(W["llama2"].with_(name="llama2_full", construct_full=True), range(2), [0], dev=dev)
+
+
+@pytest.mark.parametrize("support,row", [(128, "auto"), (128, "0"), (512, "auto")])
+def test_construct_full_headline(dev, support, row):
+    w = W["headline"].with_(name="headline_full", construct_full=True, support=support,
+                            depth=3, R=20)
+    env = {"RHEO_EXPAND_ROW": row} if row != "auto" else None
+    run_parity(w, [0], [0, 63], dev=dev, env=env)
+
+
 SHAPES = (
     {},
     {"RHEO_EXPAND_VARIANT": "0", "RHEO_VERIFY_BLOCKS": "4"},
