@@ -413,6 +413,26 @@ class PrunedTree:
     sampled: list        # pruned index -> position of the sampled child or -1
 
 
+def tree_mask(nodes, pt):
+    """What the target model needs to score the pruned tree in one forward
+    pass (Sec. 1; Sec. 2.1: the drafted paths are verified in parallel):
+    mask[i][j] = 1 iff pruned node j lies on the path from the root to
+    pruned node i (i itself included), and the depth of every pruned node
+    (the root 0), i.e. its position after the prefix."""
+    n = len(pt.order)
+    mask = [[0] * n for _ in range(n)]
+    depth = [0] * n
+    for i in range(n):
+        j, d = i, 0
+        while j != -1:
+            mask[i][j] = 1
+            j = pt.parent[j]
+            d += 1
+        depth[i] = d - 1
+        assert depth[i] == nodes[pt.order[i]].depth
+    return mask, depth
+
+
 def prune(nodes, R):
     """Keep the R best non-root nodes under ``priority`` (App. C.1).  The
     root is not counted in R (App. C.3, base case: T_1 is one depth-1

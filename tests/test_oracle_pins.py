@@ -693,3 +693,36 @@ def test_whole_vocabulary_construction(seed):
     a = rheo.node_dist_from_logits(l, m, T, V, construct_full=True)
     b = rheo.node_dist_from_logits(l, m, T, V)
     assert a.s1 == b.s1 and a.w1 == b.w1
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_tree_mask(seed):
+    # the mask the target forward needs (Sec. 2.1): ancestors by the node
+    # records' own parent links, rows nested along the tree, lower triangular
+    rng = np.random.default_rng(900 + seed)
+    V, K, m, D, R = 12, 4, 1, 3, 14
+    cfg = rheo.TreeConfig(K=K, m=m, depth=D, n_expand=2)
+    dists = {}
+
+    def dd(node, nodes):
+        if node.uid not in dists:
+            l = rng.normal(0, 2.0, V).astype(np.float32)
+            dists[node.uid] = rheo.node_dist_from_logits(l, m, 1.0)
+        return dists[node.uid]
+    nodes = run_philox(rheo.build_tree(cfg, 1.0, dd), 0x1234 + seed, 0)
+    pt = rheo.prune(nodes, R)
+    mask, depth = rheo.tree_mask(nodes, pt)
+    n = len(pt.order)
+    pos = {u: i for i, u in enumerate(pt.order)}
+    for i in range(n):
+        anc = set()
+        u = pt.order[i]
+        while u != -1:
+            anc.add(pos[u])
+            u = nodes[u].parent
+        assert {j for j in range(n) if mask[i][j]} == anc
+        assert sum(mask[i]) == depth[i] + 1
+        assert all(mask[i][j] == 0 for j in range(i + 1, n))
+        if i:
+            p = pt.parent[i]
+            assert [mask[i][j] - mask[p][j] for j in range(n)] == [int(j == i) for j in range(n)]
