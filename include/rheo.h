@@ -166,6 +166,18 @@ int rheo_prune(rheo_tree* tree, int32_t budget, void* stream);
 int rheo_pruned_view(rheo_tree* tree, int32_t* parent, int32_t* token,
                      void* stream);
 
+/* What the target model needs to score the pruned tree in one forward
+ * pass, all drafted paths at once (Sec. 1; Sec. 2.1), in pruned order.
+ * Valid after rheo_prune.  Either pointer may be NULL.
+ *   mask   [B][R+1][R+1] uint8: mask[b][i][j] = 1 iff pruned node j is on
+ *          the path from the root to pruned node i (i included), else 0.
+ *          Parents precede their children in pruned order, so the mask is
+ *          lower triangular.
+ *   depth  [B][R+1] int32: depth of each pruned node (root 0), its
+ *          position after the prefix.
+ * Buffers are the caller's, written completely. */
+int rheo_tree_mask(rheo_tree* tree, uint8_t* mask, int32_t* depth, void* stream);
+
 /* RheoVerification (Algorithm 1) applied layer by layer from the root
  * (Thm. 1), with p = softmax(target / T) over the whole vocabulary.
  *   target_logits [B][R+1][row_stride] of cfg.dtype (pruned-node order)

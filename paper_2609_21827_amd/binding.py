@@ -23,7 +23,8 @@ ERROR_NAMES = {RHEO_EINVAL: "EINVAL", RHEO_ENOMEM: "ENOMEM", RHEO_EHIP: "EHIP",
 
 # every symbol the header declares
 EXPORTS = ["rheo_create", "rheo_destroy", "rheo_begin_step", "rheo_expand_level",
-           "rheo_frontier", "rheo_frontier_view", "rheo_prune", "rheo_pruned_view", "rheo_verify",
+           "rheo_frontier", "rheo_frontier_view", "rheo_prune", "rheo_pruned_view",
+           "rheo_tree_mask", "rheo_verify",
            "rheo_read_nodes", "rheo_device_error", "rheo_node_count",
            "rheo_last_error"]
 
@@ -66,6 +67,7 @@ def load_library(path=LIB_PATH):
         "rheo_frontier_view": ([vp, ctypes.POINTER(vp), ctypes.POINTER(vp)], ctypes.c_int),
         "rheo_prune": ([vp, i32, vp], ctypes.c_int),
         "rheo_pruned_view": ([vp, vp, vp, vp], ctypes.c_int),
+        "rheo_tree_mask": ([vp, vp, vp, vp], ctypes.c_int),
         "rheo_verify": ([vp, vp, f32, u64, vp, vp, vp, vp], ctypes.c_int),
         "rheo_read_nodes": ([vp] * 10, ctypes.c_int),
         "rheo_device_error": ([vp, ctypes.POINTER(ctypes.c_int32)], ctypes.c_int),
@@ -177,6 +179,16 @@ class Tree:
         par, tok = out
         _check(_LIB.rheo_pruned_view(self._h, _ptr(par), _ptr(tok), _stream(stream)))
         return par, tok
+
+    def tree_mask(self, out=None, stream=None):
+        """(mask [B][R+1][R+1] uint8, depth [B][R+1] int32) of the pruned tree."""
+        n = self.R + 1
+        if out is None:
+            out = (torch.empty((self.B, n, n), dtype=torch.uint8, device=self.device),
+                   torch.empty((self.B, n), dtype=torch.int32, device=self.device))
+        mask, depth = out
+        _check(_LIB.rheo_tree_mask(self._h, _ptr(mask), _ptr(depth), _stream(stream)))
+        return mask, depth
 
     def verify(self, target_logits, T, rng_key, out=None, stream=None):
         if out is None:

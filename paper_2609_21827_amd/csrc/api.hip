@@ -352,6 +352,13 @@ int rheo_pruned_view(rheo_tree* t, int32_t* parent, int32_t* token, void* stream
     return e == hipSuccess ? RHEO_OK : hip_fail(e, "pruned view launch");
 }
 
+int rheo_tree_mask(rheo_tree* t, uint8_t* mask, int32_t* depth, void* stream) {
+    if (!t) return fail(RHEO_EINVAL, "NULL tree");
+    if (t->state != PRUNED && t->state != VERIFIED) return fail(RHEO_ESTATE, "no pruned tree");
+    const hipError_t e = launch_tree_mask(t->dev, t->R, mask, depth, (hipStream_t)stream);
+    return e == hipSuccess ? RHEO_OK : hip_fail(e, "tree mask launch");
+}
+
 int rheo_verify(rheo_tree* t, const void* logits, float T, uint64_t key, int32_t* accepted,
                 int32_t* accept_len, int32_t* final_token, void* stream) {
     if (!t) return fail(RHEO_EINVAL, "NULL tree");

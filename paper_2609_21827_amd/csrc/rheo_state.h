@@ -108,6 +108,8 @@ struct ExpandVariant {
 };
 hipError_t launch_expand_row(const TreeDev& t, const LevelArgs& a, hipStream_t s);
 hipError_t launch_row_wsum(const TreeDev& t, const LevelArgs& a, hipStream_t s);
+hipError_t launch_tree_mask(const TreeDev& t, int R, uint8_t* mask, int32_t* depth,
+                            hipStream_t s);
 int expand_row_nq(int dtype, int V);
 int expand_variant_count(int dtype);
 int expand_variant_nvc(int v);

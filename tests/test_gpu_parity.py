@@ -16,6 +16,7 @@ import pytest
 import torch
 
 import synth
+from oracle import rheo
 from oracle.harness import node_table, oracle_step
 
 pytestmark = pytest.mark.gpu
@@ -32,7 +33,7 @@ def dev():
     return "cuda"
 
 
-def _check_seq(w, tree_nodes, ppar, ptok, acc, alen, fin, b, step, T):
+def _check_seq(w, tree_nodes, ppar, ptok, acc, alen, fin, b, step, T, mask=None, depth=None):
     print(f"  oracle {w.name} b={b} step={step} T={T}", flush=True)
     nodes, pt, oacc, ou = oracle_step(w, b, step, T=T)
     tab = node_table(nodes)
@@ -48,6 +49,10 @@ def _check_seq(w, tree_nodes, ppar, ptok, acc, alen, fin, b, step, T):
     R = len(pt.order) - 1
     assert list(ptok[b][:R + 1]) == [-1] + [nodes[u].token for u in pt.order[1:]]
     assert list(ppar[b][:R + 1]) == list(pt.parent)
+    if mask is not None:
+        om, od = rheo.tree_mask(nodes, pt)
+        assert np.array_equal(mask[b], np.array(om, dtype=np.uint8)), b
+        assert list(depth[b]) == od
     n = int(alen[b])
     assert list(acc[b][:n]) == list(oacc), (b, list(acc[b][:n]), oacc)
     assert all(x == -1 for x in acc[b][n:])
@@ -69,11 +74,12 @@ def run_parity(w, steps, seqs, T=None, dev="cuda", tree_kw=None, env=None):
             acc, alen, fin = run_step(tree, w, step, T=T, device=dev)
             nodes = {k: v.cpu().numpy() for k, v in tree.read_nodes().items()}
             ppar, ptok = (x.cpu().numpy() for x in tree.pruned_view())
+            mask, depth = (x.cpu().numpy() for x in tree.tree_mask())
             torch.cuda.synchronize()
             assert tree.device_error() == 0
             for b in seqs:
                 _check_seq(w, nodes, ppar, ptok, acc.numpy(), alen.numpy(), fin.numpy(),
-                           b, step, T)
+                           b, step, T, mask, depth)
     finally:
         tree.close()
 
