@@ -185,7 +185,15 @@ int rheo_tree_mask(rheo_tree* tree, uint8_t* mask, int32_t* depth, void* stream)
  *   accept_len    [B] int32: number of accepted draft tokens
  *   final_token   [B] int32: the token emitted after them (residual sample,
  *                 or a sample of p below an accepted leaf)
- * The output of a step is accepted[0..accept_len) followed by final_token. */
+ * The output of a step is accepted[0..accept_len) followed by final_token.
+ * The kernel's blocks wait for each other (teams of blocks per sequence);
+ * its grid never exceeds what the device holds at once, so on a device that
+ * runs nothing else at the same time every wait completes.  Work running
+ * concurrently on the same device can delay some blocks: a wait longer
+ * than about a second then ends the walk and sets device error bit 128.
+ * The environment variable RHEO_VERIFY_COOP=1 (read at rheo_create) makes
+ * the launch cooperative, which guarantees co-residency at the cost of
+ * about 11 us of dispatch delay per call. */
 int rheo_verify(rheo_tree* tree, const void* target_logits, float T,
                 uint64_t rng_key, int32_t* accepted, int32_t* accept_len,
                 int32_t* final_token, void* stream);

@@ -62,6 +62,7 @@ struct rheo_tree {
     int row_mode = 0;                     // sparse levels: 1 one block per row, 0 chunks,
                                           // -1 by the number of rows
     int vG = 1, v_segch = 1, v_grid = 1;  // verification team shape
+    int v_coop = 0;                       // cooperative launch of the verify kernel
     float T_expand = 1.0f;
     void* blocks[48] = {};
     const void* draft[16] = {};           // dense: each level's draft rows (borrowed)
@@ -250,6 +251,8 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
         return hip_fail(e, "initialising tree state");
     }
     e = verify_shape(d, &t->vG, &t->v_segch, &t->v_grid);
+    // RHEO_VERIFY_COOP=1: launch the verify teams cooperatively
+    if (const char* vc = getenv("RHEO_VERIFY_COOP")) t->v_coop = vc[0] == '1';
     if (e != hipSuccess) {
         free_all(t);
         delete t;
@@ -377,7 +380,8 @@ int rheo_verify(rheo_tree* t, const void* logits, float T, uint64_t key, int32_t
     a.final_token = final_token;
     a.G = t->vG;
     for (int i = 0; i < 16; ++i) a.draft[i] = t->draft[i];
-    const hipError_t e = launch_verify(t->dev, a, t->v_segch, t->v_grid, (hipStream_t)stream);
+    const hipError_t e = launch_verify(t->dev, a, t->v_segch, t->v_grid, t->v_coop,
+                                       (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "verify launch");
     t->state = VERIFIED;
     return RHEO_OK;

@@ -96,7 +96,7 @@ hipError_t launch_select(const TreeDev& t, const LevelArgs& a, int variant, hipS
 hipError_t launch_dense(const TreeDev& t, const LevelArgs& a, int nvc, hipStream_t s);
 hipError_t launch_prune(const TreeDev& t, int R, hipStream_t s);
 hipError_t verify_shape(const TreeDev& t, int* G, int* segch, int* grid);
-hipError_t launch_verify(const TreeDev& t, const VerifyArgs& a, int segch, int grid,
+hipError_t launch_verify(const TreeDev& t, const VerifyArgs& a, int segch, int grid, int coop,
                          hipStream_t s);
 
 // expand kernel variants: the chunk each selection block holds in registers

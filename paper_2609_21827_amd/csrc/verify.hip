@@ -808,14 +808,22 @@ hipError_t verify_shape(const TreeDev& t, int* G_out, int* segch, int* grid) {
     return hipSuccess;
 }
 
-hipError_t launch_verify(const TreeDev& t, const VerifyArgs& a, int segch, int grid,
+// The grid never exceeds what the device holds at once (verify_shape), so
+// on a device that runs nothing else every block is resident from the
+// start and the team barriers complete.  coop = 1 asks the runtime to
+// guarantee that (a cooperative launch, which on this platform adds about
+// 11 us of dispatch delay); otherwise a barrier that waits past its spin
+// limit, because other work held part of the device, ends the walk with
+// device error 128 rather than hanging.
+hipError_t launch_verify(const TreeDev& t, const VerifyArgs& a, int segch, int grid, int coop,
                          hipStream_t s) {
     const void* fn = verify_fn(t);
     TreeDev tt = t;
     VerifyArgs aa = a;
     aa.NV = segch;
     void* args[] = {&tt, &aa};
-    return hipLaunchCooperativeKernel(fn, dim3(grid), dim3(NTV), args, 0, s);
+    if (coop) return hipLaunchCooperativeKernel(fn, dim3(grid), dim3(NTV), args, 0, s);
+    return hipLaunchKernel(fn, dim3(grid), dim3(NTV), args, 0, s);
 }
 
 }  // namespace rheo

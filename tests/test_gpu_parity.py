@@ -194,6 +194,7 @@ SHAPES = (
     {"RHEO_EXPAND_VARIANT": "1", "RHEO_VERIFY_BLOCKS": "1024"},
     {"RHEO_EXPAND_ROW": "1"},
     {"RHEO_EXPAND_ROW": "0", "RHEO_VERIFY_BLOCKS": "256"},
+    {"RHEO_VERIFY_COOP": "1"},
 )
 
 
