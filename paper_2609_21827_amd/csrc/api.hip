@@ -62,6 +62,7 @@ struct rheo_tree {
     int row_mode = 0;                     // sparse levels: 1 one block per row, 0 chunks,
                                           // -1 by the number of rows
     int vG = 1, v_segch = 1, v_grid = 1;  // verification team shape
+    int row_min = kRowMin;                // fewest rows for the per-row kernel
     int v_coop = 0;                       // cooperative launch of the verify kernel
     float T_expand = 1.0f;
     void* blocks[48] = {};
@@ -176,6 +177,7 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
         if (er[0] == '0') t->row_mode = 0;
         else if (er[0] == '1' && t->row_mode != 0) t->row_mode = 1;
     }
+    if (const char* rm = getenv("RHEO_ROW_MIN")) t->row_min = atoi(rm);
     const char* env = getenv("RHEO_EXPAND_VARIANT");
     if (env) {
         const int v = atoi(env);
@@ -303,7 +305,7 @@ int rheo_expand_level(rheo_tree* t, const void* logits, float T, uint64_t key, v
         e = launch_select(t->dev, a, t->variant, (hipStream_t)stream);
         if (e == hipSuccess)
             e = launch_dense(t->dev, a, expand_variant_nvc(t->variant), (hipStream_t)stream);
-    } else if (t->row_mode == 1 || (t->row_mode < 0 && t->dev.B * a.P >= kRowMin)) {
+    } else if (t->row_mode == 1 || (t->row_mode < 0 && t->dev.B * a.P >= t->row_min)) {
         e = launch_expand_row(t->dev, a, (hipStream_t)stream);
     } else {
         e = launch_expand(t->dev, a, t->variant, (hipStream_t)stream);

@@ -119,7 +119,8 @@ __host__ __device__ inline PoolLds pool_lds(int S, int C, int top_min = 0, int k
 // threads (tid < NT).  Children fields the frontier selection reads in other
 // blocks (token, score, path) are published with agent-scope atomics.
 // SORT_TAIL: order the tail by sorting (supports above kCountTailMax)
-// rather than by counting; both give the same order.
+// rather than by counting; both give the same order.  A support slot left
+// empty (no candidate reached it) is flagged and filled with a -inf key.
 template <int NT, bool SORT_TAIL>
 __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, int row,
                                           uint8_t* lds, const PoolLds& L, int pu,
@@ -149,11 +150,19 @@ __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, 
     // is in (logit desc, id asc) order and the weight never grows along it,
     // so the rank differs from the position only where two different logits
     // share a weight: then the ranks and the tail are computed again.
-    const float M = key_value(s_top[0]);
-    const float ref0 = key_value(s_top[m]);
+    auto filled = [&](uint64_t k) {
+        return (uint32_t)key_id(k) >= (uint32_t)t.V ? logit_key(-INFINITY, 0u) : k;
+    };
+    const float M = key_value(filled(s_top[0]));
+    const float ref0 = key_value(filled(s_top[m]));
     uint64_t part1 = 0, partq = 0;
     for (int i = tid; i < S; i += NT) {
-        const uint64_t tk = s_top[i];
+        uint64_t tk = s_top[i];
+        if ((uint32_t)key_id(tk) >= (uint32_t)t.V) {   // a support slot left empty
+            atomicOr(t.err, 256);
+            tk = logit_key(-INFINITY, 0u);
+            s_top[i] = tk;
+        }
         const float v = key_value(tk);
         const uint32_t w = cweight(v, M, a.k1);
         s_w1[i] = w;
@@ -234,7 +243,7 @@ __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, 
         for (int r = r0; r < r0 + per; ++r)
             if (r < ntail) mine += s_q[(uint32_t)~s_k2[r]];
         uint64_t tot;
-        uint64_t pre = block_excl_scan_u64<NT>(mine, s_red, &tot);
+        uint64_t pre = pscan_excl<NT>(mine, s_red, &tot);
         for (int r = r0; r < r0 + per; ++r) {
             if (r < ntail) {
                 const uint64_t kk = ~s_k2[r];
@@ -304,11 +313,26 @@ __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, 
 
 // The parent of row j of sequence b: frontier node j of the previous level
 // (the n_expand children with the highest priority, chosen by the previous
-// launch), with the Philox draw of its sampled slot.  One thread.
+// launch), with the Philox draw of its sampled slot.  One thread.  The
+// loads are issued by row_parent_load and checked by row_parent, so a
+// kernel can let them complete while it streams its row.
+struct RowParentRaw {
+    int pu;
+    uint64_t u;
+};
+__device__ __forceinline__ RowParentRaw row_parent_load(const TreeDev& t, const LevelArgs& a,
+                                                        int b, int j) {
+    RowParentRaw r{0, 0ull};
+    if (a.level > 0) {
+        r.pu = t.frontier[(int64_t)b * t.NE + j];
+        r.u = t.fr_u[(int64_t)b * t.NE + j];
+    }
+    return r;
+}
 __device__ __forceinline__ void row_parent(const TreeDev& t, const LevelArgs& a, int b, int j,
-                                           int* s_pu, uint64_t* s_u) {
+                                           const RowParentRaw& raw, int* s_pu, uint64_t* s_u) {
     const int level = a.level, K = t.K, NE = t.NE;
-    int pu = (level == 0) ? 0 : t.frontier[(int64_t)b * NE + j];
+    int pu = raw.pu;
     const int lo_uid = (level == 0) ? 0 : ((level == 1) ? 1 : 1 + K + (level - 2) * NE * K);
     const int hi_uid = (level == 0) ? 1 : lo_uid + ((level == 1) ? 1 : NE) * K;
     if (pu < lo_uid || pu >= hi_uid) {
@@ -316,8 +340,7 @@ __device__ __forceinline__ void row_parent(const TreeDev& t, const LevelArgs& a,
         pu = 0;
     }
     *s_pu = pu;
-    uint64_t u = (level == 0) ? philox_draw(a.rng_key, P_DRAFT, (uint64_t)b, 0ull)
-                              : t.fr_u[(int64_t)b * NE + j];
+    uint64_t u = (level == 0) ? philox_draw(a.rng_key, P_DRAFT, (uint64_t)b, 0ull) : raw.u;
     if (pu == 0 && level > 0) u = philox_draw(a.rng_key, P_DRAFT, (uint64_t)b, 0ull);
     *s_u = u;
 }
@@ -352,7 +375,7 @@ __global__ __launch_bounds__(NTP) void k_pool(TreeDev t, LevelArgs a) {
     // with the Philox draw of its sampled slot; and the chunk lists, with
     // an empty list after them
     const int C4 = (C + 3) & ~3;
-    if (tid == 0) row_parent(t, a, b, j, &s_pu, &s_u);
+    if (tid == 0) row_parent(t, a, b, j, row_parent_load(t, a, b, j), &s_pu, &s_u);
     const uint64_t* src = t.sel + (int64_t)row * C * S;
     for (int i = tid; i < C * S; i += NTP) s_m[i] = src[i];
     for (int i = C * S + tid; i < (C + 1) * S; i += NTP) s_m[i] = 0ull;
@@ -403,13 +426,6 @@ __global__ __launch_bounds__(NTP) void k_pool(TreeDev t, LevelArgs a) {
             }
             if (kA != 0ull && rA < S) s_top[rA] = kA;
             if (kB != 0ull && rB < S) s_top[rB] = kB;
-        }
-    }
-    __syncthreads();
-    for (int i = tid; i < S; i += NTP) {
-        if ((uint32_t)key_id(s_top[i]) >= (uint32_t)t.V) {   // a support slot left empty
-            atomicOr(t.err, 256);
-            s_top[i] = logit_key(-INFINITY, 0u);
         }
     }
     __syncthreads();
@@ -1058,8 +1074,11 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
     const int nsel = S;                            // S <= V
     const char* base = (const char*)a.logits + (int64_t)row * t.stride * (DT ? 2 : 4);
 
+    // the parent's frontier entry is loaded now and checked after the
+    // row is streamed, so wave 0 does not wait for it
+    RowParentRaw rp{0, 0ull};
     if (tid == 0) {
-        row_parent(t, a, b, j, &s_pu, &s_u);
+        rp = row_parent_load(t, a, b, j);
         s_cnt = 0;
     }
     if (!LS)
@@ -1119,6 +1138,7 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
             proc_batch(rb, bt + 1);
         }
     }
+    if (tid == 0) row_parent(t, a, b, j, rp, &s_pu, &s_u);
     // bf16: the two largest of each half (four distinct vectors)
     if (DT) {
         if constexpr (four) {
@@ -1296,13 +1316,6 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
         for (int i = tid; i < cnt; i += NTE) {
             const int rk = s_rank[i];
             if (rk < nsel) s_top[rk] = s_keys[i];
-        }
-        __syncthreads();
-    }
-    for (int i = tid; i < S; i += NTE) {
-        if ((uint32_t)key_id(s_top[i]) >= (uint32_t)V) {   // a support slot left empty
-            atomicOr(t.err, 256);
-            s_top[i] = logit_key(-INFINITY, 0u);
         }
     }
     __syncthreads();

@@ -152,6 +152,17 @@ __device__ __forceinline__ void psum2(uint64_t a, uint64_t b, uint64_t* sh, uint
         block_sum2_u64<NT>(a, b, sh, ra, rb);
     }
 }
+// Exclusive prefix sum of one 64-bit value per thread over the pool's NT
+// threads (sh: NT / WAVE words for a block); *total receives the sum.
+template <int NT>
+__device__ __forceinline__ uint64_t pscan_excl(uint64_t v, uint64_t* sh, uint64_t* total) {
+    if (NT == WAVE) {
+        const uint64_t inc = wave_incl_scan_u64(v);
+        *total = lane_u64(inc, WAVE - 1);
+        return inc - v;
+    }
+    return block_excl_scan_u64<NT>(v, sh, total);
+}
 template <int NT>
 __device__ __forceinline__ bool pany(bool p) {
     if (NT == WAVE) return __ballot(p) != 0ull;
