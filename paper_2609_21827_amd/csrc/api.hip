@@ -240,6 +240,7 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
     hipError_t e = hipMemset(d.err, 0, sizeof(int32_t));
     if (e == hipSuccess) e = hipMemset(d.team_flag, 0, B * 64 * sizeof(uint64_t));
     if (e == hipSuccess) e = hipMemset(d.team_epoch, 0, B * sizeof(uint64_t));
+    if (e == hipSuccess) e = hipMemset(d.team_max, 0, B * 64 * sizeof(uint64_t));
     if (e == hipSuccess) e = hipMemset(d.row_cnt, 0, B * d.NE * sizeof(uint32_t));
     if (e == hipSuccess) e = hipMemset(d.seq_cnt, 0, B * sizeof(uint32_t));
     if (e == hipSuccess && dense) e = hipMemset(d.dflag, 0, B * d.NE * sizeof(int32_t));

@@ -155,6 +155,47 @@ __device__ u128 block_sum_u128(u128 v, u128* sh) {
 // every team member has arrived.  Prior team-visible stores must be agent
 // atomic stores; each thread waits for its own before the block barrier.
 // Returns false (and raises the error flag) if the wait timed out.
+// The team's row maximum: every block publishes its segment maximum in one
+// word with the (low 32 bits of the) epoch, and waits until all G words of
+// the team carry that epoch; the words then hold every segment's maximum,
+// so no separate barrier or read follows.  *s_M receives the maximum.
+// Bounded like team_barrier.
+__device__ bool team_max_exchange(uint64_t* words, int g, int G, uint64_t epoch, float mx,
+                                  int32_t* err, int* s_ok, float* s_M) {
+    const uint32_t e32 = (uint32_t)epoch;
+    if (threadIdx.x < WAVE) {
+        if (threadIdx.x == 0) {
+            *s_ok = 1;
+            __hip_atomic_store(&words[g], ((uint64_t)e32 << 32) | ord32(mx), __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+        }
+        float v = -INFINITY;
+        long spins = 0;
+        for (;;) {
+            bool ok = true;
+            if ((int)threadIdx.x < G) {
+                const uint64_t w = __hip_atomic_load(&words[threadIdx.x], __ATOMIC_RELAXED,
+                                                     __HIP_MEMORY_SCOPE_AGENT);
+                ok = (uint32_t)(w >> 32) == e32;
+                v = unord32((uint32_t)w);
+            }
+            if (__all(ok)) break;
+            if (++spins > kSpinLimit) {
+                if (threadIdx.x == 0) {
+                    atomicOr(err, 128);
+                    *s_ok = 0;
+                }
+                break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+        }
+        v = wave_max(v);
+        if (threadIdx.x == 0) *s_M = v;
+    }
+    __syncthreads();
+    return *s_ok != 0;
+}
+
 __device__ bool team_barrier(uint64_t* flags, int g, int G, uint64_t epoch, int32_t* err,
                              int* s_ok) {
     __builtin_amdgcn_s_waitcnt(0);
@@ -236,7 +277,7 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
     // barrier epochs of this call: the team's base, read before any block
     // of the team can pass its first barrier; the leader advances it on exit
     const uint64_t epoch = t.team_epoch[b];
-    uint32_t* tmax_x = t.team_max + (int64_t)b * GMAX;
+    uint64_t* tmax_x = t.team_max + (int64_t)b * GMAX;
     uint64_t* chunk_x = t.team_chunk + (int64_t)b * NCMAX;
     uint32_t* sp_x = t.team_sp + (int64_t)b * SPMAX;
     uint64_t* nchunk_x = t.team_nchunk + (int64_t)b * NCMAX * 2;   // dense residual totals
@@ -370,20 +411,9 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
             for (int k = 0; k < VEC; ++k) mx = fmaxf(mx, velem<DT>(xv, k));
         }
         mx = block_max<NTV>(mx, s_redf);
-        if (tid == 0)
-            __hip_atomic_store(&tmax_x[g], __float_as_uint(mx), __ATOMIC_RELAXED,
-                               __HIP_MEMORY_SCOPE_AGENT);
-        if (!team_barrier(flags, g, G, epoch + 3 * level + 1, t.err, &s_ok)) break;
+        if (!team_max_exchange(tmax_x, g, G, epoch + 3 * level + 1, mx, t.err, &s_ok, &s_M))
+            break;
         const int nc = s_nc, spos = s_spos;
-        if (tid < WAVE) {
-            float v = -INFINITY;
-            if (tid < G)
-                v = __uint_as_float(__hip_atomic_load(&tmax_x[tid], __ATOMIC_RELAXED,
-                                                      __HIP_MEMORY_SCOPE_AGENT));
-            v = wave_max(v);
-            if (tid == 0) s_M = v;
-        }
-        __syncthreads();
         const float M = s_M;
         // ---- 2. weights of the segment, chunk totals, and p's weights at
         //         the special tokens this block owns ---------------------------
