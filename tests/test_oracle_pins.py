@@ -10,9 +10,8 @@ Philox) and brute force.
 
 import json
 import os
-from fractions import Fraction
-
 import zlib
+from fractions import Fraction
 
 import numpy as np
 import pytest
