@@ -1,7 +1,8 @@
 // RheoVerification (Algorithm 1) applied layer by layer from the root of the
 // pruned tree (Thm. 1).
 //
-// A team of G co-resident blocks walks one sequence (cooperative launch).
+// A team of G co-resident blocks walks one sequence (the grid never exceeds
+// what the device holds at once; see launch_verify).
 // At each layer the current node's target row is split into G segments of
 // whole 64*VEC-token chunks; every block holds its segment in registers:
 //   1. segment maximum -> team exchange -> row maximum M
@@ -811,8 +812,8 @@ static const void* verify_fn(const TreeDev& t) {
 }
 
 // Team shape for a tree: about `target` blocks in all (1024 by default),
-// segments of whole chunks, G <= GMAX, every block co-resident (cooperative
-// launch).
+// segments of whole chunks, G <= GMAX, and no more blocks than the device
+// holds at once, so every block can be resident together.
 hipError_t verify_shape(const TreeDev& t, int* G_out, int* segch, int* grid) {
     const int VEC = t.dtype ? 8 : 4;
     const int NC = (t.V + WAVE * VEC - 1) / (WAVE * VEC);
