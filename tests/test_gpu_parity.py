@@ -418,3 +418,16 @@ def test_methods_headline(dev, method):
     """The batched bench shape (one block per row at every level)."""
     run_parity(W["headline"].with_(name="headline_" + method, method=method), [0], [0, 63],
                dev=dev)
+
+
+@pytest.mark.parametrize("method,over", [
+    ("rrsw", dict(support=512, depth=3, R=20)),                  # large-support pools
+    ("topk", dict(support=1024, depth=3, R=20)),
+    ("rrsw", dict(construct_full=True, depth=3, R=20)),          # whole-vocabulary q
+    ("topk", dict(construct_full=True, support=256, depth=3, R=20)),
+    ("rrsw", dict(support=0, B=8, depth=3, R=20)),               # dense, batched shape
+    ("topk", dict(support=0, B=8, depth=3, R=20)),
+])
+def test_method_combinations(dev, method, over):
+    w = W["headline"].with_(name=f"headline_{method}_combo", method=method, **over)
+    run_parity(w, [0], [0, w.B - 1], dev=dev)
