@@ -180,8 +180,14 @@ __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, 
     bool tie = false;
     for (int i = tid + 1; i < S; i += NT)
         tie |= s_w1[i] == s_w1[i - 1] && (s_top[i] >> 32) != (s_top[i - 1] >> 32);
-    const bool ident = !pany<NT>(tie);
-    if (!ident) {
+    // Counting (small supports) goes ahead with the rank by weight taken to
+    // be the support order and learns at the barrier that ends the tail
+    // whether two different logits share a weight; only then (rarely) are
+    // the ranks, the tail weights and the tail computed again.  Sorting
+    // (large supports) checks first.
+    bool ident = true;
+    if constexpr (SORT_TAIL) ident = !pany<NT>(tie);
+    auto reorder = [&]() {
         for (int i = tid; i < S; i += NT)
             s_k2[i] = ((uint64_t)s_w1[i] << 32) |
                       (uint64_t)(0xFFFFFFFFu - (uint32_t)key_id(s_top[i]));
@@ -201,7 +207,8 @@ __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, 
             s_k2[i] = tail ? (uint64_t)(0xFFFFFFFFu - (uint32_t)key_id(tk)) + 1 : 0ull;
         }
         Zq = psum<NT>(partq, s_red);
-    }
+    };
+    if (!ident) reorder();
     // position in the support of rank r, and rank of position i
     auto xs = [&](int r) -> int { return ident ? r : (int)s_xs[r]; };
     auto wr = [&](int i) -> int { return ident ? i : (int)s_wr[i]; };
@@ -213,18 +220,31 @@ __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, 
     // t = floor(U64 Zq / 2^64): the inverse CDF over token ids.  Small
     // supports count, for every entry, the smaller ids and their mass;
     // large ones sort the tail by id and take a prefix sum.
-    const uint64_t tt = __umul64hi(u, Zq);
     const int64_t tail_base = ((int64_t)b * t.E + e_idx) * S;
     if constexpr (!SORT_TAIL) {
-        rank_prefix<NT>(s_k2, s_q, S, [&](int i, int ir, uint64_t pre) {
-            if (s_k2[i] != 0ull) {
-                const uint32_t q = s_q[i];
-                t.tail_id[tail_base + ir] = key_id(s_top[i]);
-                t.tail_q[tail_base + ir] = q;
-                if (pre <= tt && tt - pre < (uint64_t)q) *s_yi = i;
-            }
-        });
+        auto tail_count = [&]() {
+            const uint64_t tt = __umul64hi(u, Zq);
+            rank_prefix<NT>(s_k2, s_q, S, [&](int i, int ir, uint64_t pre) {
+                if (s_k2[i] != 0ull) {
+                    const uint32_t q = s_q[i];
+                    t.tail_id[tail_base + ir] = key_id(s_top[i]);
+                    t.tail_q[tail_base + ir] = q;
+                    if (pre <= tt && tt - pre < (uint64_t)q) *s_yi = i;
+                }
+            });
+        };
+        tail_count();
+        const bool anytie = pany<NT>(tie);      // also the barrier after the tail
+        if (NT == WAVE) wave_sync();
+        if (anytie) {
+            ident = false;
+            if (tid == 0) *s_yi = -1;
+            reorder();                           // (synchronises before the new tail)
+            tail_count();
+            psync<NT>();
+        }
     } else {
+        const uint64_t tt = __umul64hi(u, Zq);
         // sort keys: the complement of (id, position) for the tail, so that
         // the descending sort puts ids in ascending order; 0 (last) for the
         // leads and the padding
@@ -255,8 +275,8 @@ __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, 
                 pre += q;
             }
         }
+        psync<NT>();
     }
-    psync<NT>();
     int yi = *s_yi;
     if (yi < 0) {
         if (tid == 0) atomicOr(t.err, 1);
@@ -1311,12 +1331,7 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
         __syncthreads();
         bitonic_sort_desc<NTE>(s_keys, n2);
     } else {
-        rank_keys<NTE>(s_keys, cnt, s_rank);
-        __syncthreads();
-        for (int i = tid; i < cnt; i += NTE) {
-            const int rk = s_rank[i];
-            if (rk < nsel) s_top[rk] = s_keys[i];
-        }
+        rank_keys<NTE>(s_keys, cnt, s_rank, s_top, nsel);     // placed as ranked
     }
     __syncthreads();
 

@@ -294,9 +294,13 @@ __device__ __forceinline__ float wave_sort_desc(float v) {
 }
 
 // rank[i] = number of keys strictly greater than keys[i], for unique keys
-// in LDS; each key is compared by a group of F consecutive lanes.
+// in LDS; each key is compared by a group of F consecutive lanes.  With
+// `out`, the lane that finishes key i writes it to out[rank] instead when
+// the rank is below nsel (and writes no rank), so no barrier is needed
+// between ranking and placing.
 template <int NT>
-__device__ void rank_keys(const uint64_t* keys, int n, int16_t* rank) {
+__device__ void rank_keys(const uint64_t* keys, int n, int16_t* rank, uint64_t* out = nullptr,
+                          int nsel = 0) {
     int npad = 1;
     while (npad < n) npad <<= 1;
     int F = NT / npad;
@@ -318,7 +322,13 @@ __device__ void rank_keys(const uint64_t* keys, int n, int16_t* rank) {
             for (; j < n; j += F) cnt += keys[j] > k;
         }
         for (int o = 1; o < F; o <<= 1) cnt += __shfl_xor(cnt, o);
-        if (i < n && sub == 0) rank[i] = (int16_t)cnt;
+        if (i < n && sub == 0) {
+            if (out) {
+                if (cnt < nsel) out[cnt] = keys[i];
+            } else {
+                rank[i] = (int16_t)cnt;
+            }
+        }
     }
 }
 
