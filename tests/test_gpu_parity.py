@@ -431,3 +431,32 @@ def test_methods_headline(dev, method):
 def test_method_combinations(dev, method, over):
     w = W["headline"].with_(name=f"headline_{method}_combo", method=method, **over)
     run_parity(w, [0], [0, w.B - 1], dev=dev)
+
+
+def _many_steps(w, steps, dev):
+    """Steps in a row on one handle, the device error flag after each, and
+    one sequence of each step against the oracle."""
+    from paper_2609_21827_amd.driver import make_tree, run_step
+    tree = make_tree(w, device=dev)
+    try:
+        for step in steps:
+            print(f"gpu step {w.name} step={step}", flush=True)
+            acc, alen, fin = run_step(tree, w, step, device=dev)
+            nodes = {k: v.cpu().numpy() for k, v in tree.read_nodes().items()}
+            ppar, ptok = (x.cpu().numpy() for x in tree.pruned_view())
+            torch.cuda.synchronize()
+            assert tree.device_error() == 0, step
+            b = (13 * step + 5) % w.B
+            _check_seq(w, nodes, ppar, ptok, acc.numpy(), alen.numpy(), fin.numpy(), b, step, w.T)
+    finally:
+        tree.close()
+
+
+def test_headline_many_steps(dev):
+    _many_steps(W["headline"], range(2, 12), dev)
+
+
+@pytest.mark.parametrize("support", [256, 1024])
+def test_large_supports_many_steps(dev, support):
+    w = W["headline"].with_(name=f"headline_s{support}", support=support)
+    _many_steps(w, range(3, 9), dev)
