@@ -226,6 +226,7 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
     rc = rc ? rc : dalloc(t, &d.team_flag, B * 64);
     rc = rc ? rc : dalloc(t, &d.team_epoch, B);
     rc = rc ? rc : dalloc(t, &d.team_max, B * 64);
+    rc = rc ? rc : dalloc(t, &d.team_sum, B * 64);
     rc = rc ? rc : dalloc(t, &d.team_chunk, B * 1024);
     rc = rc ? rc : dalloc(t, &d.team_sp, B * (1024 + 16));
     rc = rc ? rc : dalloc(t, &d.team_nchunk, dense ? B * 1024 * 2 : 1);
@@ -241,6 +242,7 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
     if (e == hipSuccess) e = hipMemset(d.team_flag, 0, B * 64 * sizeof(uint64_t));
     if (e == hipSuccess) e = hipMemset(d.team_epoch, 0, B * sizeof(uint64_t));
     if (e == hipSuccess) e = hipMemset(d.team_max, 0, B * 64 * sizeof(uint64_t));
+    if (e == hipSuccess) e = hipMemset(d.team_sum, 0, B * 64 * sizeof(uint64_t));
     if (e == hipSuccess) e = hipMemset(d.row_cnt, 0, B * d.NE * sizeof(uint32_t));
     if (e == hipSuccess) e = hipMemset(d.seq_cnt, 0, B * sizeof(uint32_t));
     if (e == hipSuccess && dense) e = hipMemset(d.dflag, 0, B * d.NE * sizeof(int32_t));

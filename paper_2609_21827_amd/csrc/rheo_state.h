@@ -44,6 +44,7 @@ struct TreeDev {
     uint64_t* team_flag;           // [B][GMAX] arrival epochs
     uint64_t* team_epoch;          // [B] first barrier epoch of the next call
     uint64_t* team_max;            // [B][GMAX] segment maxima: epoch << 32 | order code
+    uint64_t* team_sum;            // [B][GMAX] segment weight sums: epoch << 48 | sum
     uint64_t* team_chunk;          // [B][NCMAX] chunk totals of p's weights
     uint32_t* team_sp;             // [B][SPMAX] p's weights at the special tokens
     uint64_t* team_nchunk;         // dense: [B][NCMAX][2] residual chunk totals (u128)

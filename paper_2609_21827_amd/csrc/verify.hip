@@ -197,6 +197,55 @@ __device__ bool team_max_exchange(uint64_t* words, int g, int G, uint64_t epoch,
     return *s_ok != 0;
 }
 
+// The team's total of p's weights (sparse mode): every block publishes the
+// sum over its segment (< 2^48: at most 2^18 tokens of weight <= 2^30) in
+// one word with the low 16 bits of the epoch, after its chunk totals; the
+// words then carry every segment's sum, so the total needs no further read.
+// A word left from an earlier barrier is fewer than 2^16 epochs old, so
+// the 16-bit comparison cannot mistake it for the current one.  wsum holds
+// the block's per-wave sums.  Bounded like team_barrier.
+__device__ bool team_sum_exchange(uint64_t* words, int g, int G, uint64_t epoch,
+                                  const uint64_t* wsum, int nw, int32_t* err, int* s_ok,
+                                  uint64_t* s_total) {
+    constexpr uint64_t M48 = (1ull << 48) - 1;
+    const uint64_t e16 = epoch & 0xFFFFull;
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (threadIdx.x < WAVE) {
+        if (threadIdx.x == 0) {
+            *s_ok = 1;
+            uint64_t sum = 0;
+            for (int w = 0; w < nw; ++w) sum += wsum[w];
+            __hip_atomic_store(&words[g], (e16 << 48) | (sum & M48), __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+        }
+        uint64_t v = 0;
+        long spins = 0;
+        for (;;) {
+            bool ok = true;
+            if ((int)threadIdx.x < G) {
+                const uint64_t w = __hip_atomic_load(&words[threadIdx.x], __ATOMIC_RELAXED,
+                                                     __HIP_MEMORY_SCOPE_AGENT);
+                ok = (w >> 48) == e16;
+                v = w & M48;
+            }
+            if (__all(ok)) break;
+            if (++spins > kSpinLimit) {
+                if (threadIdx.x == 0) {
+                    atomicOr(err, 128);
+                    *s_ok = 0;
+                }
+                break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+        }
+        v = wave_sum_u64(v);
+        if (threadIdx.x == 0) *s_total = v;
+    }
+    __syncthreads();
+    return *s_ok != 0;
+}
+
 __device__ bool team_barrier(uint64_t* flags, int g, int G, uint64_t epoch, int32_t* err,
                              int* s_ok) {
     __builtin_amdgcn_s_waitcnt(0);
@@ -281,6 +330,7 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
     uint64_t* tmax_x = t.team_max + (int64_t)b * GMAX;
     uint64_t* chunk_x = t.team_chunk + (int64_t)b * NCMAX;
     uint32_t* sp_x = t.team_sp + (int64_t)b * SPMAX;
+    uint64_t* tsum_x = t.team_sum + (int64_t)b * GMAX;
     uint64_t* nchunk_x = t.team_nchunk + (int64_t)b * NCMAX * 2;   // dense residual totals
     auto nchunk_at = [&](int c) -> u128 {
         const uint64_t lo = __hip_atomic_load(&nchunk_x[2 * c], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -336,10 +386,13 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
             const int c = c0 + wid + NWV * j;
             xr[j] = (c < c1) ? load_vec<DT>(row, c * WAVE + lane, V) : make_uint4(0, 0, 0, 0);
         }
-        float sp_l = 0.0f;                   // logit of this thread's tail token, if owned
-        if (sp_id >= lo_tok && sp_id < hi_tok) sp_l = load_logit<DT>(row, sp_id);
-        float c_l = 0.0f;                    // logit of this lane's candidate, if owned
-        if (keep && ctok >= lo_tok && ctok < hi_tok) c_l = load_logit<DT>(row, ctok);
+        // the logits of the special tokens: sparse mode, every block reads
+        // all of them (each block then has p's weights at them without an
+        // exchange); dense mode, the block that owns the token
+        float sp_l = 0.0f;                   // logit of this thread's tail token
+        if (sp_id >= 0) sp_l = load_logit<DT>(row, sp_id);
+        float c_l = 0.0f;                    // logit of this lane's candidate
+        if (keep && (!DN || (ctok >= lo_tok && ctok < hi_tok))) c_l = load_logit<DT>(row, ctok);
         // dense mode: q~ at this node comes from its draft row (borrowed),
         // the logit of its x_{m+1} and its leads
         const char* drow = nullptr;
@@ -417,7 +470,8 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
         const int nc = s_nc, spos = s_spos;
         const float M = s_M;
         // ---- 2. weights of the segment, chunk totals, and p's weights at
-        //         the special tokens this block owns ---------------------------
+        //         the special tokens ------------------------------------------
+        uint64_t wpart = 0;                  // this wave's sum over its chunks
 #pragma unroll
         for (int j = 0; j < JREG; ++j) {
             const int c = c0 + wid + NWV * j;
@@ -429,6 +483,7 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
                     if (v < V) sum += cweight(velem<DT>(xr[j], k), M, a.kT);
                 }
                 sum = wave_sum_u64(sum);
+                wpart += sum;
                 if (lane == 0)
                     __hip_atomic_store(&chunk_x[c], sum, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
@@ -442,22 +497,27 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
                 if (v < V) sum += cweight(velem<DT>(xv, k), M, a.kT);
             }
             sum = wave_sum_u64(sum);
+            wpart += sum;
             if (lane == 0)
                 __hip_atomic_store(&chunk_x[c], sum, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
-        if (sp_id >= lo_tok && sp_id < hi_tok)
-            __hip_atomic_store(&sp_x[tid], cweight(sp_l, M, a.kT), __ATOMIC_RELAXED,
-                               __HIP_MEMORY_SCOPE_AGENT);
-        for (int i = tid + NTV; i < nt; i += NTV) {
-            const int v = s_tid[i];
-            if (v >= lo_tok && v < hi_tok)
-                __hip_atomic_store(&sp_x[i], cweight(load_logit<DT>(row, v), M, a.kT),
-                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if constexpr (!DN) {
+            // p's weights at every special token, from the logits read with
+            // the segment; the team's total arrives with the exchange
+            if (tid < nt) s_tp[tid] = cweight(sp_l, M, a.kT);
+            for (int i = tid + NTV; i < nt; i += NTV)
+                s_tp[i] = cweight(load_logit<DT>(row, s_tid[i]), M, a.kT);
+            if (cpos >= 0) s_tp[nt + cpos] = cweight(c_l, M, a.kT);
+            if (lane == 0) s_red[wid] = wpart;
+            if (!team_sum_exchange(tsum_x, g, G, epoch + 3 * level + 2, s_red, NWV, t.err, &s_ok,
+                                   &s_Sp))
+                break;
+        } else {
+            if (cpos >= 0 && ctok >= lo_tok && ctok < hi_tok)
+                __hip_atomic_store(&sp_x[nt + cpos], cweight(c_l, M, a.kT), __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+            if (!team_barrier(flags, g, G, epoch + 3 * level + 2, t.err, &s_ok)) break;
         }
-        if (cpos >= 0 && ctok >= lo_tok && ctok < hi_tok)
-            __hip_atomic_store(&sp_x[nt + cpos], cweight(c_l, M, a.kT), __ATOMIC_RELAXED,
-                               __HIP_MEMORY_SCOPE_AGENT);
-        if (!team_barrier(flags, g, G, epoch + 3 * level + 2, t.err, &s_ok)) break;
         // ---- 3. Algorithm 1 at this layer, by wave 0 (the chunk totals and
         //         the special weights from the team, S_p, the tail deficit,
         //         and the decisions of lane 0) ---------------------------------
@@ -489,6 +549,7 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
             // weight passes of other blocks on this compute unit
             __builtin_amdgcn_s_setprio(3);
             uint64_t part = 0;
+            if constexpr (DN) {
             for (int cb = 0; cb < NC; cb += 4 * WAVE) {
                 uint64_t cv[4];
 #pragma unroll
@@ -519,7 +580,8 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
                     if (i < nsp) s_tp[i] = pv[q];
                 }
             }
-            Sp = wave_sum_u64(part);
+            }
+            Sp = DN ? wave_sum_u64(part) : s_Sp;
             wave_sync();
             if (lane < nc) s_c_tail[lane] = DN ? -1 : find_sorted(s_tid, nt, s_c_tok[lane]);
             wave_sync();
@@ -669,6 +731,13 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
         }
         // ---- final sample u* ~ r (one block of the team) --------------------
         if (g != 0) break;
+        if constexpr (!DN) {
+            // the chunk totals, published before the second exchange
+            for (int c = tid; c < NC; c += NTV)
+                s_chunk[c] = __hip_atomic_load(&chunk_x[c], __ATOMIC_RELAXED,
+                                               __HIP_MEMORY_SCOPE_AGENT);
+            __syncthreads();
+        }
         const u128 F = s_F;
         const u128 tt = s_tt;
         // corrected chunk totals, contiguous chunk ranges per thread
