@@ -535,6 +535,12 @@ __device__ void rank_keys32(const uint32_t* keys, int n, int16_t* rank) {
     }
 }
 
+// Lane l (a constant) of v replaced by the wave-uniform s.
+__device__ __forceinline__ int writelane_i32(int v, int s, int l) {
+    asm volatile("v_writelane_b32 %0, %1, %2" : "+v"(v) : "s"(s), "n"(l));
+    return v;
+}
+
 // h = the largest 16-bit code that at least nsel of the offered codes reach
 // (c1 and c2 of every thread, and c3 and c4 too if `four`, a block-uniform
 // flag), four bits per round: each wave counts its offers >= h | d << sh
@@ -553,27 +559,30 @@ __device__ __forceinline__ uint32_t offer_threshold(uint32_t c1, uint32_t c2, ui
     for (int r = 0; r < 4; ++r) {
         const int sh = 12 - 4 * r;
         int* buf = s_cnt + (r & 1) * NW * 16;
-        uint32_t mine = 0;
+        // h has no bits at or below this digit, so c >= h | d << sh is
+        // ((c - h, saturated at 0) >> sh) >= d: a compare with a small constant
+        const uint32_t e1 = __builtin_elementwise_sub_sat(c1, h) >> sh;
+        const uint32_t e2 = __builtin_elementwise_sub_sat(c2, h) >> sh;
+        const uint32_t e3 = __builtin_elementwise_sub_sat(c3, h) >> sh;
+        const uint32_t e4 = __builtin_elementwise_sub_sat(c4, h) >> sh;
+        int mine = 0;
         if (four) {
 #pragma unroll
             for (int d = 1; d < 16; ++d) {
-                const uint32_t cand = h | ((uint32_t)d << sh);
-                const uint32_t n = (uint32_t)(__popcll(__ballot(c1 >= cand)) +
-                                              __popcll(__ballot(c2 >= cand)) +
-                                              __popcll(__ballot(c3 >= cand)) +
-                                              __popcll(__ballot(c4 >= cand)));
-                mine = (lane == d) ? n : mine;
+                const uint32_t cd = (uint32_t)d;
+                const int n = __popcll(__ballot(e1 >= cd)) + __popcll(__ballot(e2 >= cd)) +
+                              __popcll(__ballot(e3 >= cd)) + __popcll(__ballot(e4 >= cd));
+                mine = writelane_i32(mine, n, d);
             }
         } else {
 #pragma unroll
             for (int d = 1; d < 16; ++d) {
-                const uint32_t cand = h | ((uint32_t)d << sh);
-                const uint32_t n = (uint32_t)(__popcll(__ballot(c1 >= cand)) +
-                                              __popcll(__ballot(c2 >= cand)));
-                mine = (lane == d) ? n : mine;
+                const uint32_t cd = (uint32_t)d;
+                const int n = __popcll(__ballot(e1 >= cd)) + __popcll(__ballot(e2 >= cd));
+                mine = writelane_i32(mine, n, d);
             }
         }
-        if (lane < 16) buf[wid * 16 + lane] = (int)mine;
+        if (lane < 16) buf[wid * 16 + lane] = mine;
         __syncthreads();
         int tot = 0;
         if (lane < 16) {
@@ -1105,6 +1114,8 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
         for (int i = tid; i < S; i += NTE) s_top[i] = 0ull;   // id -1 until ranked
 
     // ---- the row, streamed: vector q of this thread is tid + NTE * q ------
+    // vm: each vector's maximum -- bf16: the 16-bit order codes of vectors
+    // 2 qi (low half) and 2 qi + 1 (high half) in vm[qi]; fp32: its bits
     uint32_t vm[NM];
     uint32_t c1 = 0, c2 = 0, c3 = 0, c4 = 0;
     rs_ushort2 p1 = {0, 0}, p2 = {0, 0};
@@ -1128,8 +1139,8 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
                 const uint32_t lo = bf16x8_max_raw(r[e]);
                 const uint32_t hi = bf16x8_max_raw(r[e + 1]);
                 const int qi = (bt * EBATCH + e) / 2;
-                vm[qi] = __builtin_amdgcn_perm(hi, lo, 0x07060302u);
-                const rs_ushort2 cq = bf16x2_codes(vm[qi]);
+                const rs_ushort2 cq = bf16x2_codes(__builtin_amdgcn_perm(hi, lo, 0x07060302u));
+                vm[qi] = __builtin_bit_cast(uint32_t, cq);
                 p2 = __builtin_elementwise_max(p2, __builtin_elementwise_min(p1, cq));
                 p1 = __builtin_elementwise_max(p1, cq);
             }
@@ -1180,7 +1191,7 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
         // code, then the low byte, from histograms of the codes >= h
         auto code_of = [&](int q) -> uint32_t {
             if (DT) {
-                const rs_ushort2 c = bf16x2_codes(vm[q / 2]);
+                const rs_ushort2 c = __builtin_bit_cast(rs_ushort2, vm[q / 2]);
                 return (q & 1) ? (uint32_t)c.y : (uint32_t)c.x;
             }
             return ord32(__uint_as_float(vm[q])) >> 16;
@@ -1212,30 +1223,51 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
     const ParentRec pr = (tid < K) ? parent_rec(t, level, nb, s_pu) : ParentRec{1.0, 0ull};
     const float tau = (h << 16) > ord32(-INFINITY) ? unord32(h << 16) : -INFINITY;
 
-    // ---- candidate vectors (maximum >= tau): every wave appends the indices
-    //      of its own to its region of s_cvi; if a wave has more than its
-    //      region holds, but all fit, they are written again into one list
-    //      with slots reserved per wave
+    // ---- candidate vectors (maximum >= tau): every thread marks its own in
+    //      a bit mask (bf16: bit qi is vector 2 qi, bit 16 + qi vector
+    //      2 qi + 1; fp32: bit q is vector q), the wave's offsets come from
+    //      one prefix sum, and every wave appends them to its region of
+    //      s_cvi; if a wave has more than its region holds, but all fit, they
+    //      are written again into one list with slots reserved per wave
     constexpr int WCAPR = CV / NW;
-    auto vmax_of = [&](int q) -> float {
-        return DT ? ((q & 1) ? bf_hi(vm[q / 2]) : bf_lo(vm[q / 2])) : __uint_as_float(vm[q]);
-    };
+    uint32_t take = 0;
     {
-        int wpos = 0;
+        // vectors of this thread inside the row: q < nqv
+        const int nqv = min(NQ, max(0, (NVR - tid + NTE - 1) / NTE));
+        if (DT) {
+            // code >= h is maximum >= tau, except that a -0 maximum passes
+            // tau = +0 as a logit (code of -0: 0x7FFF)
+            const uint32_t hc = (h == 0x8000u) ? 0x7FFFu : h;
+            const rs_ushort2 h2 = {(unsigned short)hc, (unsigned short)hc};
+            const rs_ushort2 one = {1, 1};
+            uint32_t below = 0;
 #pragma unroll
-        for (int q = 0; q < NQ; ++q) {
-            const int vi = tid + NTE * q;
-            const bool take = vmax_of(q) >= tau && vi < NVR;
-            const uint64_t msk = __ballot(take);
-            if (take) {
-                const int pos = wpos + (int)__builtin_amdgcn_mbcnt_hi(
-                    (uint32_t)(msk >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)msk, 0u));
-                if (pos < WCAPR) s_cvi[wid * WCAPR + pos] = vi;
+            for (int qi = 0; qi < NM; ++qi) {
+                const rs_ushort2 c = __builtin_bit_cast(rs_ushort2, vm[qi]);
+                const rs_ushort2 d = __builtin_elementwise_min(__builtin_elementwise_sub_sat(h2, c), one);
+                below |= __builtin_bit_cast(uint32_t, d) << qi;
             }
-            wpos += __popcll(msk);
+            const uint32_t vlo = (1u << ((nqv + 1) >> 1)) - 1u;
+            const uint32_t vhi = ((1u << (nqv >> 1)) - 1u) << 16;
+            take = ~below & (vlo | vhi);
+        } else {
+#pragma unroll
+            for (int q = 0; q < NQ; ++q) take |= (uint32_t)(__uint_as_float(vm[q]) >= tau) << q;
+            take &= nqv >= 32 ? 0xFFFFFFFFu : (1u << nqv) - 1u;
         }
-        if (lane == 0) s_wn[wid] = wpos;
     }
+    const int tn = __popc(take);
+    const int texcl = wave_excl_scan(tn);
+    auto push_vectors = [&](int pos, int* dst, int cap) {
+        for (uint32_t mk = take; mk != 0u; mk &= mk - 1u) {
+            const int bb = __builtin_ctz(mk);
+            const int q = DT ? ((bb < 16) ? 2 * bb : 2 * (bb - 16) + 1) : bb;
+            if (pos < cap) dst[pos] = tid + NTE * q;
+            ++pos;
+        }
+    };
+    push_vectors(texcl, s_cvi + wid * WCAPR, WCAPR);
+    if (lane == WAVE - 1) s_wn[wid] = texcl + tn;
     __syncthreads();
     int wn[NW], nv = 0, wbefore = 0;
     bool ovf = false;
@@ -1248,19 +1280,7 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
     }
     const bool contig = ovf && nv <= CV;
     if (contig) {
-        int wpos = wbefore;
-#pragma unroll
-        for (int q = 0; q < NQ; ++q) {
-            const int vi = tid + NTE * q;
-            const bool take = vmax_of(q) >= tau && vi < NVR;
-            const uint64_t msk = __ballot(take);
-            if (take) {
-                const int pos = wpos + (int)__builtin_amdgcn_mbcnt_hi(
-                    (uint32_t)(msk >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)msk, 0u));
-                s_cvi[pos] = vi;
-            }
-            wpos += __popcll(msk);
-        }
+        push_vectors(wbefore + texcl, s_cvi, CV);
         __syncthreads();
     }
     // ---- their elements >= tau (candidate vectors read again, one per
