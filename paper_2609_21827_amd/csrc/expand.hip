@@ -1103,13 +1103,10 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
     const int nsel = S;                            // S <= V
     const char* base = (const char*)a.logits + (int64_t)row * t.stride * (DT ? 2 : 4);
 
-    // the parent's frontier entry is loaded now and checked after the
-    // row is streamed, so wave 0 does not wait for it
+    // the parent's frontier entry is loaded while the row streams (after
+    // its first loads are issued) and checked after the row is streamed
     RowParentRaw rp{0, 0ull};
-    if (tid == 0) {
-        rp = row_parent_load(t, a, b, j);
-        s_cnt = 0;
-    }
+    if (tid == 0) s_cnt = 0;
     if (!LS)
         for (int i = tid; i < S; i += NTE) s_top[i] = 0ull;   // id -1 until ranked
 
@@ -1166,6 +1163,7 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
             load_batch(rb, bt + 1);
             proc_batch(ra, bt);
             if (bt + 2 < NB) load_batch(ra, bt + 2);
+            if (bt == 0 && tid == 0) rp = row_parent_load(t, a, b, j);
             proc_batch(rb, bt + 1);
         }
     }

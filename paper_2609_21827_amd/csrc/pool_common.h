@@ -75,19 +75,30 @@ __device__ __forceinline__ void rank_prefix(const uint64_t* keys, const uint32_t
     int F = 1;
     while (F < 16 && 2 * F * n <= NT) F *= 2;
     const int sub = t % F;
+    // lane `sub` of an entry's F lanes takes entries [j0, j1), a run whose
+    // length and start are multiples of 4: keys read two and weights four
+    // at a time (both arrays 16-byte aligned)
+    const int L = ((n + F - 1) / F + 3) & ~3;
+    const int j0 = min(sub * L, n), j1 = min(j0 + L, n);
+    const ulonglong2* kp = (const ulonglong2*)keys;
+    const uint4* wp = (const uint4*)w;
     for (int base = 0; base < n; base += NT / F) {
         const int i = base + t / F;
         const uint64_t k = keys[i < n ? i : 0];
         int c = 0;
         uint64_t pre = 0;
-        // branch-free, so that the loads of several keys are in flight
-#pragma unroll 4
-        for (int j = sub; j < n; j += F) {
-            const uint64_t x = keys[j];
-            const uint64_t wj = w[j];
-            const uint64_t gt = x > k ? 1ull : 0ull;
+        int j = j0;
+        for (; j + 3 < j1; j += 4) {
+            const ulonglong2 ka = kp[j / 2], kb = kp[j / 2 + 1];
+            const uint4 ww = wp[j / 4];
+            c += (int)(ka.x > k) + (int)(ka.y > k) + (int)(kb.x > k) + (int)(kb.y > k);
+            pre += (uint64_t)(ka.x > k ? ww.x : 0u) + (uint64_t)(ka.y > k ? ww.y : 0u) +
+                   (uint64_t)(kb.x > k ? ww.z : 0u) + (uint64_t)(kb.y > k ? ww.w : 0u);
+        }
+        for (; j < j1; ++j) {
+            const bool gt = keys[j] > k;
             c += (int)gt;
-            pre += wj & (0ull - gt);
+            pre += gt ? (uint64_t)w[j] : 0ull;
         }
         for (int o = 1; o < F; o <<= 1) {
             c += __shfl_xor(c, o);

@@ -308,18 +308,28 @@ __device__ void rank_keys(const uint64_t* keys, int n, int16_t* rank, uint64_t* 
     if (F > WAVE) F = WAVE;
     const int sub = threadIdx.x % F;
     const int per = NT / F;
+    // lane `sub` of a key's F lanes compares it with keys [j0, j1), a run of
+    // even length and start, read two at a time (keys are 16-byte aligned)
+    const int L = ((n + F - 1) / F + 1) & ~1;
+    const int j0 = min(sub * L, n), j1 = min(j0 + L, n);
+    const ulonglong2* kp = (const ulonglong2*)keys;
     for (int base = 0; base < n; base += per) {
         const int i = base + threadIdx.x / F;
         int cnt = 0;
         if (i < n) {
             const uint64_t k = keys[i];
-            int j = sub;
-            for (; j + 3 * F < n; j += 4 * F) {
-                const uint64_t a = keys[j], b = keys[j + F], c = keys[j + 2 * F],
-                               d = keys[j + 3 * F];
-                cnt += (a > k) + (b > k) + (c > k) + (d > k);
+            int j = j0;
+            for (; j + 7 < j1; j += 8) {
+                const ulonglong2 a = kp[j / 2], b = kp[j / 2 + 1], c = kp[j / 2 + 2],
+                                 d = kp[j / 2 + 3];
+                cnt += (a.x > k) + (a.y > k) + (b.x > k) + (b.y > k) + (c.x > k) + (c.y > k) +
+                       (d.x > k) + (d.y > k);
             }
-            for (; j < n; j += F) cnt += keys[j] > k;
+            for (; j + 1 < j1; j += 2) {
+                const ulonglong2 a = kp[j / 2];
+                cnt += (a.x > k) + (a.y > k);
+            }
+            if (j < j1) cnt += keys[j] > k;
         }
         for (int o = 1; o < F; o <<= 1) cnt += __shfl_xor(cnt, o);
         if (i < n && sub == 0) {
