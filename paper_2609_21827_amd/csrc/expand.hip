@@ -1110,23 +1110,29 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
     if (!LS)
         for (int i = tid; i < S; i += NTE) s_top[i] = 0ull;   // id -1 until ranked
 
-    // ---- the row, streamed: vector q of this thread is tid + NTE * q ------
+    // ---- the row, streamed: vector q of this thread is vidx(q) ------------
     // vm: each vector's maximum -- bf16: the 16-bit order codes of vectors
     // 2 qi (low half) and 2 qi + 1 (high half) in vm[qi]; fp32: its bits
     uint32_t vm[NM];
     uint32_t c1 = 0, c2 = 0, c3 = 0, c4 = 0;
     rs_ushort2 p1 = {0, 0}, p2 = {0, 0};
-    const int wfirst = __builtin_amdgcn_readfirstlane(wid) * WAVE;
+    // vector q of this thread: lane `lane` of the 64-vector slot (wid + q)
+    // mod NW of block stride q.  Rotating the slot spreads every wave's
+    // reads over all offsets (mod one block stride, 8 KB) in the row; with
+    // a fixed slot per wave its reads kept to one offset, and the waves of
+    // a block finished streaming up to several µs apart.
+    const int wsu = __builtin_amdgcn_readfirstlane(wid);
+    auto vidx = [&](int q) -> int { return (((wsu + q) & (NW - 1)) * WAVE + lane) + NTE * q; };
     auto load_batch = [&](uint4 (&r)[EBATCH], int bt) {
-        // plain loads when every lane of the wave reads whole vectors
-        if (wfirst + WAVE - 1 + NTE * (bt * EBATCH + EBATCH - 1) < NVF) {
+        // plain loads when every lane of the block reads whole vectors
+        if (NTE - 1 + NTE * (bt * EBATCH + EBATCH - 1) < NVF) {
 #pragma unroll
             for (int e = 0; e < EBATCH; ++e)
-                r[e] = load_stream16(base + (int64_t)(tid + NTE * (bt * EBATCH + e)) * 16);
+                r[e] = load_stream16(base + (int64_t)vidx(bt * EBATCH + e) * 16);
         } else {
 #pragma unroll
             for (int e = 0; e < EBATCH; ++e)
-                r[e] = load_row_vec<DT>(base, tid + NTE * (bt * EBATCH + e), V);
+                r[e] = load_row_vec<DT>(base, vidx(bt * EBATCH + e), V);
         }
     };
     auto proc_batch = [&](const uint4 (&r)[EBATCH], int bt) {
@@ -1199,7 +1205,7 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
 #pragma unroll
         for (int q = 0; q < NQ; ++q) {
             const uint32_t c = code_of(q);
-            if (c >= h && tid + NTE * q < NVR) atomicAdd(&s_hist[c >> 8], 1);
+            if (c >= h && vidx(q) < NVR) atomicAdd(&s_hist[c >> 8], 1);
         }
         __syncthreads();
         const int2 hi8 = suffix_pick256<NTE>(s_hist, nsel, s_thr);
@@ -1209,7 +1215,7 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
 #pragma unroll
             for (int q = 0; q < NQ; ++q) {
                 const uint32_t c = code_of(q);
-                if (c >= h && (int)(c >> 8) == hi8.x && tid + NTE * q < NVR)
+                if (c >= h && (int)(c >> 8) == hi8.x && vidx(q) < NVR)
                     atomicAdd(&s_hist[c & 0xFFu], 1);
             }
             __syncthreads();
@@ -1231,7 +1237,8 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
     uint32_t take = 0;
     {
         // vectors of this thread inside the row: q < nqv
-        const int nqv = min(NQ, max(0, (NVR - tid + NTE - 1) / NTE));
+        int nqv = min(NQ, max(0, (NVR - lane - (NTE - WAVE) + NTE - 1) / NTE));
+        while (nqv < NQ && vidx(nqv) < NVR) ++nqv;      // at most twice
         if (DT) {
             // code >= h is maximum >= tau, except that a -0 maximum passes
             // tau = +0 as a logit (code of -0: 0x7FFF)
@@ -1260,7 +1267,7 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
         for (uint32_t mk = take; mk != 0u; mk &= mk - 1u) {
             const int bb = __builtin_ctz(mk);
             const int q = DT ? ((bb < 16) ? 2 * bb : 2 * (bb - 16) + 1) : bb;
-            if (pos < cap) dst[pos] = tid + NTE * q;
+            if (pos < cap) dst[pos] = vidx(q);
             ++pos;
         }
     };
