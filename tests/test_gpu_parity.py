@@ -118,6 +118,11 @@ def test_tiny_variants(dev, over):
     dict(V=1003, dtype="bf16", recipe="zipf", support=1024, K=5, depth=3, R=12),
     dict(V=300, dtype="f32", recipe="zipf", support=300, K=4, depth=3, R=12),
     dict(V=32000, dtype="bf16", recipe="zipf", quantum=0.5, support=700, K=6, depth=3, R=20),
+    # the support's boundary among hundreds of zero logits of both signs
+    # (Gaussian logits rounded to multiples of 8: -0.0 below zero)
+    dict(V=1003, dtype="bf16", recipe="gauss", quantum=8.0, support=128, K=5, depth=3, R=12),
+    dict(V=1003, dtype="f32", recipe="gauss", quantum=8.0, support=128, K=5, depth=3, R=12),
+    dict(V=4099, dtype="bf16", recipe="gauss", quantum=8.0, support=300, K=5, depth=3, R=12),
 ])
 @pytest.mark.parametrize("row", ["auto", "1"])
 def test_edge_shapes(dev, over, row):
