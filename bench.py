@@ -15,10 +15,13 @@ Protocol
   3. HIP events around each rheo_expand_level call (on the stream it launches
      on) give the duration of an expand level (its selection and pool kernels, the
      dominant work); its algorithmic bytes are the draft rows it must read
-     (rows x V x 2 bytes).  The event pass starts behind a spin kernel that
-     holds the stream while the host queues the steps, so the launches run
-     back to back and the events time the kernels rather than the Python
-     loop's launch latency.  Then the same steps are captured as HIP graphs
+     (rows x V x 2 bytes): one event pair around each step's depth
+     consecutive expand calls gives the average launch duration (events
+     around every level, in a pass of their own, give the per-level
+     breakdown).  Both passes start behind a spin kernel that holds the
+     stream while the host queues the steps, so the launches run back to
+     back and the events time the kernels rather than the Python loop's
+     launch latency.  Then the same steps are captured as HIP graphs
      (one per recorded step) and replayed; `value` is the faster of the
      eager launch loop and the graph replay (`mode` says which; both are
      reported), the eager loop alone with --graph 0.
@@ -211,19 +214,23 @@ def main():
     # next) is read in place through these views: no call, no copy
     fr_view = tree.frontier_view()
 
-    def replay(i, events=None, stream_override=None):
+    def replay(i, events=None, stream_override=None, bracket=None):
         # the calls a serving loop makes: expand (x depth), prune, pruned
         # view (which rows the target model computes), verify
         stream = stream_override or torch.cuda.current_stream()
         rec = recs[i % len(recs)]
         ob = out_bufs[i % len(recs)]
         tree.begin_step()
+        if bracket is not None:
+            bracket[0].record(stream)
         for d, rows in enumerate(rec["draft"]):
             if events is not None:
                 events[d][0].record(stream)
             tree.expand_level(rows, rec["T"], rec["rng_key"], stream=stream)
             if events is not None:
                 events[d][1].record(stream)
+        if bracket is not None:
+            bracket[1].record(stream)
         tree.prune(w.R, stream=stream)
         tree.pruned_view(out=pv_buf, stream=stream)
         tree.verify(rec["target"], rec["T"], rec["rng_key"], out=ob, stream=stream)
@@ -263,6 +270,18 @@ def main():
     check(args.steps)
     assert tree.device_error() == 0
     event_pass_ms = ev[0][0][0].elapsed_time(ev[-1][-1][1]) / args.steps
+    # the roofline figure: one event pair around each step's depth
+    # consecutive expand launches (no event packets between the levels)
+    br = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    hold_stream(1.5 * eager_ms * args.steps + 5.0)
+    for i in range(args.steps):
+        replay(i, bracket=br[i])
+    torch.cuda.synchronize()
+    check(args.steps)
+    assert tree.device_error() == 0
+    bracket_ms = sum(a.elapsed_time(b) for a, b in br)
 
     # ---- 3. the same steps replayed as HIP graphs (one per recorded step):
     #      the launch sequence of a step is captured once and replayed; every
@@ -308,9 +327,8 @@ def main():
     tokens_per_step = sum(walk_rows) / len(walk_rows)
 
     exp_ms = [[e[0].elapsed_time(e[1]) for e in ev[i]] for i in range(args.steps)]
-    tot_ms = sum(sum(x) for x in exp_ms)
     n_launch = args.steps * w.depth
-    avg_launch_us = tot_ms * 1e3 / n_launch
+    avg_launch_us = bracket_ms * 1e3 / n_launch
     bytes_per_launch = draft_bytes / w.depth
     achieved = bytes_per_launch / (avg_launch_us * 1e-6) / 1e9
     lvl_us = [sum(exp_ms[i][d] for i in range(args.steps)) * 1e3 / args.steps
@@ -373,6 +391,8 @@ def main():
                      "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4),
                      "traffic": traffic,
                      "avg_launch_us": round(avg_launch_us, 2),
+                     "avg_launch_us_per_level_events": round(
+                         sum(sum(x) for x in exp_ms) * 1e3 / n_launch, 2),
                      "bytes_per_launch": int(bytes_per_launch)},
         "cpu_baseline": cpu,
         "step_hbm_GBps": round(mean_step_bytes / (ms * 1e-3) / 1e9, 1),
