@@ -57,6 +57,7 @@ struct rheo_tree {
     TreeDev dev;
     State state = CREATED;
     int level = 0;
+    uint64_t key_prev = 0;                // rng_key of the last expand_level call
     int R = 0;
     int variant = 0;
     int row_mode = 0;                     // sparse levels: 1 one block per row, 0 chunks,
@@ -217,7 +218,6 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
     rc = rc ? rc : dalloc(t, &d.zq, B * E);
     rc = rc ? rc : dalloc(t, &d.s1row, d.cfull ? B * d.NE : 1);
     rc = rc ? rc : dalloc(t, &d.frontier, B * d.NE);
-    rc = rc ? rc : dalloc(t, &d.fr_u, B * d.NE);
     rc = rc ? rc : dalloc(t, &d.fr_parent, B * d.NE);
     rc = rc ? rc : dalloc(t, &d.fr_token, B * d.NE);
     rc = rc ? rc : dalloc(t, &d.pidx, B * NN);
@@ -298,6 +298,7 @@ int rheo_expand_level(rheo_tree* t, const void* logits, float T, uint64_t key, v
     a.k1 = k_of_T(t->cfg.construct_tempered ? T : 1.0f);
     a.kT = k_of_T(T);
     a.rng_key = key;
+    a.fr_key = t->key_prev;
     hipError_t e = hipSuccess;
     if (t->dev.cfull) {
         // the construction totals over the whole rows, read by the pools
@@ -316,6 +317,7 @@ int rheo_expand_level(rheo_tree* t, const void* logits, float T, uint64_t key, v
     if (e != hipSuccess) return hip_fail(e, "expand launch");
     t->draft[t->level] = logits;
     t->T_expand = T;
+    t->key_prev = key;
     if (++t->level == t->dev.D) t->state = EXPANDED;
     return RHEO_OK;
 }

@@ -200,8 +200,10 @@ __global__ __launch_bounds__(NTD) void k_dpool(TreeDev t, LevelArgs a) {
             pu = 0;
         }
         s_pu = pu;
-        s_u = (level == 0 || bad) ? philox_draw(a.rng_key, P_DRAFT, (uint64_t)b, (uint64_t)pu)
-                                  : t.fr_u[(int64_t)b * NE + j];
+        // the draw of the parent's sampled slot, keyed by the launch that
+        // created the parent
+        s_u = philox_draw((level == 0 || bad) ? a.rng_key : a.fr_key, P_DRAFT, (uint64_t)b,
+                          (uint64_t)pu);
         s_flag = t.dflag[row];
         t.dflag[row] = 0;                        // clean for the next level
         s_y = -1;

@@ -333,9 +333,10 @@ __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, 
 
 // The parent of row j of sequence b: frontier node j of the previous level
 // (the n_expand children with the highest priority, chosen by the previous
-// launch), with the Philox draw of its sampled slot.  One thread.  The
-// loads are issued by row_parent_load and checked by row_parent, so a
-// kernel can let them complete while it streams its row.
+// launch), with the Philox draw of its sampled slot (keyed by that launch's
+// rng_key and the parent's uid).  One thread.  The load is issued by
+// row_parent_load, the draw may be taken early (has_u), and row_parent
+// checks both, so a kernel can do this work while it streams its row.
 struct RowParentRaw {
     int pu;
     uint64_t u;
@@ -343,14 +344,15 @@ struct RowParentRaw {
 __device__ __forceinline__ RowParentRaw row_parent_load(const TreeDev& t, const LevelArgs& a,
                                                         int b, int j) {
     RowParentRaw r{0, 0ull};
-    if (a.level > 0) {
-        r.pu = t.frontier[(int64_t)b * t.NE + j];
-        r.u = t.fr_u[(int64_t)b * t.NE + j];
-    }
+    if (a.level > 0) r.pu = t.frontier[(int64_t)b * t.NE + j];
     return r;
 }
+__device__ __forceinline__ uint64_t parent_draw(const LevelArgs& a, int b, int pu) {
+    return philox_draw(a.fr_key, P_DRAFT, (uint64_t)b, (uint64_t)pu);
+}
 __device__ __forceinline__ void row_parent(const TreeDev& t, const LevelArgs& a, int b, int j,
-                                           const RowParentRaw& raw, int* s_pu, uint64_t* s_u) {
+                                           const RowParentRaw& raw, bool has_u, int* s_pu,
+                                           uint64_t* s_u) {
     const int level = a.level, K = t.K, NE = t.NE;
     int pu = raw.pu;
     const int lo_uid = (level == 0) ? 0 : ((level == 1) ? 1 : 1 + K + (level - 2) * NE * K);
@@ -360,9 +362,9 @@ __device__ __forceinline__ void row_parent(const TreeDev& t, const LevelArgs& a,
         pu = 0;
     }
     *s_pu = pu;
-    uint64_t u = (level == 0) ? philox_draw(a.rng_key, P_DRAFT, (uint64_t)b, 0ull) : raw.u;
-    if (pu == 0 && level > 0) u = philox_draw(a.rng_key, P_DRAFT, (uint64_t)b, 0ull);
-    *s_u = u;
+    // the root (level 0, or the fallback above) is drawn with this launch's key
+    *s_u = (pu == 0) ? philox_draw(a.rng_key, P_DRAFT, (uint64_t)b, 0ull)
+                     : (has_u ? raw.u : parent_draw(a, b, pu));
 }
 
 // ---------------------------------------------------------------------------
@@ -395,7 +397,7 @@ __global__ __launch_bounds__(NTP) void k_pool(TreeDev t, LevelArgs a) {
     // with the Philox draw of its sampled slot; and the chunk lists, with
     // an empty list after them
     const int C4 = (C + 3) & ~3;
-    if (tid == 0) row_parent(t, a, b, j, row_parent_load(t, a, b, j), &s_pu, &s_u);
+    if (tid == 0) row_parent(t, a, b, j, row_parent_load(t, a, b, j), false, &s_pu, &s_u);
     const uint64_t* src = t.sel + (int64_t)row * C * S;
     for (int i = tid; i < C * S; i += NTP) s_m[i] = src[i];
     for (int i = C * S + tid; i < (C + 1) * S; i += NTP) s_m[i] = 0ull;
@@ -1104,8 +1106,11 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
     const char* base = (const char*)a.logits + (int64_t)row * t.stride * (DT ? 2 : 4);
 
     // the parent's frontier entry is loaded while the row streams (after
-    // its first loads are issued) and checked after the row is streamed
+    // its first loads are issued when there are four batches or more), its
+    // draw taken while the last batch is in flight, and both checked after
+    // the row is streamed
     RowParentRaw rp{0, 0ull};
+    bool has_u = false;
     if (tid == 0) s_cnt = 0;
     if (!LS)
         for (int i = tid; i < S; i += NTE) s_top[i] = 0ull;   // id -1 until ranked
@@ -1161,6 +1166,7 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
             }
         }
     };
+    if (NB == 2 && tid == 0) rp = row_parent_load(t, a, b, j);
     {
         uint4 ra[EBATCH], rb[EBATCH];
         load_batch(ra, 0);
@@ -1169,11 +1175,17 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
             load_batch(rb, bt + 1);
             proc_batch(ra, bt);
             if (bt + 2 < NB) load_batch(ra, bt + 2);
-            if (bt == 0 && tid == 0) rp = row_parent_load(t, a, b, j);
+            if (NB >= 4 && bt == 0 && tid == 0) rp = row_parent_load(t, a, b, j);
+            // the parent's draw (a serial Philox chain) while the last
+            // batch is in flight, once the parent's load has returned
+            if (bt == NB - 2 && tid == 0 && level > 0) {
+                rp.u = parent_draw(a, b, rp.pu);
+                has_u = true;
+            }
             proc_batch(rb, bt + 1);
         }
     }
-    if (tid == 0) row_parent(t, a, b, j, rp, &s_pu, &s_u);
+    if (tid == 0) row_parent(t, a, b, j, rp, has_u, &s_pu, &s_u);
     // bf16: the two largest of each half (four distinct vectors)
     if (DT) {
         if constexpr (four) {

@@ -276,8 +276,6 @@ __device__ __forceinline__ void select_frontier(const TreeDev& t, const LevelArg
         }
         if (rk < NE) {
             t.frontier[(int64_t)b * NE + rk] = cb + tid;
-            t.fr_u[(int64_t)b * NE + rk] =     // the draw of its sampled slot
-                philox_draw(a.rng_key, P_DRAFT, (uint64_t)b, (uint64_t)(cb + tid));
             t.fr_parent[(int64_t)b * NE + rk] = tid / K;
             t.fr_token[(int64_t)b * NE + rk] =
                 __hip_atomic_load(&t.tok[nb + cb + tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

@@ -33,7 +33,6 @@ struct TreeDev {
     // frontier of the last expanded level, [B][NE]: node uid, index of its
     // parent in the previous frontier, token
     int32_t* frontier;
-    uint64_t* fr_u;                // Philox draw of each frontier node's sampled slot
     int32_t* fr_parent;
     int32_t* fr_token;
     // pruned tree
@@ -76,6 +75,7 @@ struct LevelArgs {
     float k1;                      // construction kT (untempered unless asked)
     float kT;                      // sampling kT
     uint64_t rng_key;
+    uint64_t fr_key;               // rng_key of the launch that chose this level's parents
 };
 
 struct VerifyArgs {
