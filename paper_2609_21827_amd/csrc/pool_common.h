@@ -231,8 +231,9 @@ __device__ __forceinline__ void emit_root(const TreeDev& t, int64_t nb) {
 // The next frontier (Sec. 2.1; App. C.4, step 1: the next level expands the
 // best-scoring new nodes).  Called by every block of the pool kernel once
 // its children are written: the last row of sequence b to get here ranks
-// the level's P * K new children by priority and keeps the best n_expand,
-// with the Philox draw of each kept node's sampled slot.  s_hi and s_lo are
+// the level's P * K new children by priority and keeps the best n_expand
+// (the next level's rows take the Philox draw of each kept node's sampled
+// slot themselves, keyed by this launch's rng_key).  s_hi and s_lo are
 // LDS arrays of at least 256 entries the caller no longer needs.
 __device__ __forceinline__ void select_frontier(const TreeDev& t, const LevelArgs& a, int b,
                                                 uint64_t* s_hi, uint64_t* s_lo) {
