@@ -156,6 +156,11 @@ def test_headline(dev):
     run_parity(W["headline"], [0, 1], [0, 31, 63], dev=dev)
 
 
+def test_headline_all_sequences(dev):
+    # every sequence of the batch (every row block of every level), two steps
+    run_parity(W["headline"], [20, 21], list(range(64)), dev=dev)
+
+
 @pytest.mark.parametrize("support", [256, 512, 1024])
 def test_headline_supports(dev, support):
     # the larger sparse supports (Sec. 5.5) at the batched shape, where
