@@ -343,25 +343,9 @@ def main():
         if tr.get("workload") == w.name and tr.get("kernel_src_sha256") == kernel_src_hash():
             traffic = tr.get("bytes_per_launch")
 
-    # ---- 4. CPU oracle baseline --------------------------------------------
-    cpu = None
-    if not args.no_cpu:
-        from oracle.harness import oracle_step
-        cache = {}
-        seqs, t_cpu = 0, 0.0
-        budget = args.cpu_seconds
-        while t_cpu < budget and seqs < w.B:
-            oracle_step(w, seqs, 0, row_cache=cache)          # generate rows
-            c0 = time.perf_counter()
-            oracle_step(w, seqs, 0, row_cache=cache)          # timed: method only
-            t_cpu += time.perf_counter() - c0
-            seqs += 1
-        per_seq = t_cpu / seqs
-        cpu = {"value": 1.0 / (per_seq * w.B), "unit": "steps/s", "cores": 1,
-               "kind": "oracle",
-               "sample": f"{seqs} of {w.B} sequences of one {w.name} step "
-                         f"({t_cpu:.1f} s single-threaded, rows pre-generated), "
-                         f"scaled to the whole batch"}
+    # ---- 4. CPU oracle baseline, and the streaming-read ceiling -----------
+    cpu = None if args.no_cpu else cpu_baseline(w, args.cpu_seconds)
+    ceiling = stream_ceiling()
 
     res = {
         "metric": METRIC,
@@ -390,6 +374,7 @@ def main():
                      "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS,
                      "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4),
                      "traffic": traffic,
+                     "stream_read_ceiling_GBps": ceiling,
                      "avg_launch_us": round(avg_launch_us, 2),
                      "avg_launch_us_per_level_events": round(
                          sum(sum(x) for x in exp_ms) * 1e3 / n_launch, 2),
@@ -403,6 +388,110 @@ def main():
     }
     print(json.dumps(res), flush=True)
     tree.close()
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def host_cores():
+    """Cores this process may use (the box's share: at most 16)."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+def _cpu_worker(w, seqs, barrier, q):
+    """One worker of the CPU baseline: generates the rows of its sequences,
+    waits for every worker, then times the oracle on them (method only)."""
+    import torch
+    torch.set_num_threads(1)
+    from oracle.harness import oracle_step
+    cache = {}
+    for b in seqs:
+        oracle_step(w, b, 0, row_cache=cache)
+    barrier.wait()
+    t0 = time.perf_counter()
+    for b in seqs:
+        oracle_step(w, b, 0, row_cache=cache)
+    q.put((t0, time.perf_counter(), len(seqs)))
+
+
+def _cpu_run(w, nworkers, seqs_per_worker):
+    import multiprocessing as mp
+    ctx = mp.get_context("spawn")
+    barrier, q = ctx.Barrier(nworkers), ctx.Queue()
+    procs = []
+    for k in range(nworkers):
+        seqs = [(k * seqs_per_worker + i) % w.B for i in range(seqs_per_worker)]
+        p = ctx.Process(target=_cpu_worker, args=(w, seqs, barrier, q))
+        p.start()
+        procs.append(p)
+    res = [q.get() for _ in procs]
+    for p in procs:
+        p.join()
+    t0 = min(r[0] for r in res)
+    t1 = max(r[1] for r in res)
+    n = sum(r[2] for r in res)
+    return n, t1 - t0
+
+
+def cpu_baseline(w, seconds):
+    """The CPU oracle on the host's cores (one process per core, rows
+    pre-generated, each worker timing its share of one step's sequences),
+    and on one core; steps/s of the whole batch."""
+    cores = host_cores()
+    # one sequence on one core sizes the sample to about `seconds`
+    n1, t1 = _cpu_run(w, 1, 1)
+    per_seq = t1 / n1
+    per_worker = max(1, min(w.B, int(seconds / 2 / per_seq)))
+    n_all, t_all = _cpu_run(w, cores, max(1, min(per_worker, -(-w.B // cores))))
+    n_one, t_one = _cpu_run(w, 1, max(1, min(w.B, int(seconds / 2 / per_seq))))
+    return {"value": round(n_all / t_all / w.B, 5), "unit": "steps/s", "cores": cores,
+            "kind": "oracle", "cpu_model": cpu_model(),
+            "single_core_value": round(n_one / t_one / w.B, 5),
+            "sample": f"{n_all} sequences of one {w.name} step on {cores} processes "
+                      f"({t_all:.1f} s wall), {n_one} on one ({t_one:.1f} s); rows "
+                      f"pre-generated, the method timed; steps/s = sequences/s / B"}
+
+
+def stream_ceiling(gib=2, reps=5):
+    """GB/s of a plain streaming read (16-byte non-temporal loads, 512-thread
+    blocks reading 256 KiB chunks) of a buffer larger than the Infinity
+    Cache: the best of a few grid sizes."""
+    import ctypes
+    import torch
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2609_21827_amd", "libstreamprobe.so"))
+    lib.stream_read_probe.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
+                                      ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    n = gib << 30
+    buf = torch.empty(n, dtype=torch.uint8, device="cuda")
+    buf.fill_(1)
+    out = torch.zeros(1, dtype=torch.int32, device="cuda")
+    st = torch.cuda.current_stream()
+    best = 0.0
+    for blocks in (512, 1024, 2048, 4096):
+        for r in range(reps + 1):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            rc = lib.stream_read_probe(buf.data_ptr(), n, 262144, blocks, out.data_ptr(),
+                                       st.cuda_stream)
+            e1.record()
+            torch.cuda.synchronize()
+            assert rc == 0, rc
+            if r:
+                best = max(best, n / (e0.elapsed_time(e1) * 1e-3) / 1e9)
+    del buf
+    return round(best, 1)
 
 
 def run_sweep(args):

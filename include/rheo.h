@@ -123,6 +123,10 @@ int rheo_begin_step(rheo_tree* tree);
  *                 model's logits at frontier node j of sequence b.
  *   T             sampling temperature (> 0, finite): Y ~ q~_T.
  *   rng_key       key of the step's Philox draws.
+ * T and rng_key are fixed for the whole step: the first call of a step sets
+ * them, and a later rheo_expand_level or the step's rheo_verify with another
+ * value returns RHEO_EINVAL (the stored tail weights and the draws of the
+ * sampled slots depend on both).
  * Writes K children per frontier node (token, proxy, true probability,
  * path score) and, below the last level, selects the n_expand children with
  * the highest path scores as the next frontier.  With support S, the
@@ -186,14 +190,15 @@ int rheo_tree_mask(rheo_tree* tree, uint8_t* mask, int32_t* depth, void* stream)
  *   final_token   [B] int32: the token emitted after them (residual sample,
  *                 or a sample of p below an accepted leaf)
  * The output of a step is accepted[0..accept_len) followed by final_token.
+ * T and rng_key must be the step's (see rheo_expand_level), else RHEO_EINVAL.
  * The kernel's blocks wait for each other (teams of blocks per sequence);
  * its grid never exceeds what the device holds at once, so on a device that
  * runs nothing else at the same time every wait completes.  Work running
- * concurrently on the same device can delay some blocks: a wait longer
- * than about a second then ends the walk and sets device error bit 128.
- * The environment variable RHEO_VERIFY_COOP=1 (read at rheo_create) makes
- * the launch cooperative, which guarantees co-residency at the cost of
- * about 11 us of dispatch delay per call. */
+ * concurrently on the same device can delay some blocks: a wait longer than
+ * about a second then ends that sequence's walk with the failure result
+ * accept_len[b] = final_token[b] = -1 and accepted[b][*] = -1, and sets
+ * device error bit 7 (128).  Callers check accept_len >= 0; a failed
+ * sequence's step is not Algorithm 1's and must be run again. */
 int rheo_verify(rheo_tree* tree, const void* target_logits, float T,
                 uint64_t rng_key, int32_t* accepted, int32_t* accept_len,
                 int32_t* final_token, void* stream);

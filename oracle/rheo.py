@@ -36,7 +36,9 @@ Random choices are *requests* yielded by generator functions:
 so one implementation serves both the Philox driver and exact enumeration.
 """
 
+import bisect
 from dataclasses import dataclass, field
+import itertools
 from fractions import Fraction
 
 import numpy as np
@@ -75,18 +77,24 @@ class ExplicitDist:
     inverse CDF over the ids in ascending order."""
 
     def __init__(self, ids, weights):
-        order = np.argsort(np.asarray(ids, dtype=np.int64), kind="stable")
-        self.ids = [int(ids[i]) for i in order]
-        self.weights = [weights[i] for i in order]
+        ids_np = np.asarray(ids, dtype=np.int64)
+        order = np.argsort(ids_np, kind="stable")
+        self.ids = ids_np[order].tolist()
+        if isinstance(weights, np.ndarray) and weights.dtype.kind in "iu":
+            self.weights = weights[order].tolist()         # exact Python ints
+        else:
+            self.weights = [weights[i] for i in order]
         self._total = sum(self.weights)
+        self._sorted_ids = np.asarray(self.ids, dtype=np.int64)
+        self._cum = None
 
     def total(self):
         return self._total
 
     def weight(self, v):
-        for i, w in zip(self.ids, self.weights):
-            if i == v:
-                return w
+        i = int(np.searchsorted(self._sorted_ids, v))
+        if i < len(self.ids) and self.ids[i] == v:
+            return self.weights[i]
         return 0
 
     def outcomes(self):
@@ -94,12 +102,12 @@ class ExplicitDist:
 
     def pick(self, t):
         """Smallest id whose inclusive prefix weight exceeds ``t``."""
-        acc = 0
-        for i, w in zip(self.ids, self.weights):
-            acc += w
-            if acc > t:
-                return i
-        raise AssertionError("target beyond the total weight")
+        if self._cum is None:
+            self._cum = list(itertools.accumulate(self.weights))
+        k = bisect.bisect_right(self._cum, t)
+        if k >= len(self.ids):
+            raise AssertionError("target beyond the total weight")
+        return self.ids[k]
 
 
 def _num(x):
@@ -141,19 +149,20 @@ class ResidualDist:
     def pick(self, t):
         """Smallest id whose inclusive prefix weight exceeds ``t``.  The prefix
         is non-decreasing, so a bisection over ids finds it; the prefix at an
-        id is F * (sum of P up to it) corrected by the overridden tokens."""
+        id is F * (sum of P up to it) corrected by the overridden tokens at or
+        below it."""
         V = len(self.P)
-        cum = np.cumsum(np.asarray(self.P, dtype=object)) if not isinstance(
-            self.P, np.ndarray) else np.cumsum(self.P.astype(np.int64))
+        if isinstance(self.P, np.ndarray):
+            cum = np.cumsum(self.P.astype(np.int64))      # exact: < 2^31 each, V < 2^18
+        else:
+            cum = np.cumsum(np.asarray(self.P, dtype=object))
         keys = sorted(self.override)
+        corr = list(itertools.accumulate(self.override[u] - self.F * _num(self.P[u])
+                                         for u in keys))
 
         def prefix(v):
-            acc = self.F * int(cum[v])
-            for u in keys:
-                if u > v:
-                    break
-                acc += self.override[u] - self.F * _num(self.P[u])
-            return acc
+            k = bisect.bisect_right(keys, v)
+            return self.F * int(cum[v]) + (corr[k - 1] if k else 0)
 
         lo, hi = 0, V - 1
         assert prefix(hi) > t, "target beyond the total weight"
@@ -190,7 +199,11 @@ class NodeDist:
 
 def rank_order(ids, weights):
     """Ranks by (weight descending, token id ascending) -- the paper sorts
-    by draft probability and leaves ties open; id order is this reading."""
+    by draft probability and leaves ties open; id order is this reading.
+    Integer weights are ordered by a library sort on the same key."""
+    if all(isinstance(x, (int, np.integer)) for x in weights):
+        w = np.asarray(weights, dtype=np.int64)
+        return np.lexsort((np.asarray(ids, dtype=np.int64), -w)).tolist()
     return sorted(range(len(ids)), key=lambda i: (-weights[i], int(ids[i])))
 
 
@@ -220,12 +233,22 @@ def node_dist_from_logits(logits, m, T, support_size=0, construct_tempered=False
     ref = l[sup[0]]
     Tc = T if construct_tempered else 1.0
     if model == "canonical":
-        w = [int(x) for x in numerics.canonical_weights(l[sup], ref, Tc)]
+        wa = numerics.canonical_weights(l[sup], ref, Tc)
+        r = np.lexsort((sup, -wa))                 # (weight desc, id asc)
+        sup_r = sup[r]
+        support = sup_r.tolist()
+        w1 = wa[r].tolist()
+        s1 = int(wa.sum())
+        if construct_full and len(sup) < V:
+            s1 = int(numerics.canonical_weights(l, ref, Tc).sum())
+        tail_np = sup_r[m:]
+        q = numerics.canonical_weights(l[tail_np], l[tail_np[0]], T)
+        return NodeDist(support, w1, s1, ExplicitDist(tail_np, q))
     else:
         w = numerics.fp64_weights(l[sup], ref, Tc)
-    r = rank_order(list(sup), w)
-    support = [int(sup[i]) for i in r]
-    w1 = [w[i] for i in r]
+        r = rank_order(list(sup), w)
+        support = [int(sup[i]) for i in r]
+        w1 = [w[i] for i in r]
     s1 = sum(w1)
     if construct_full and len(sup) < V:
         if model == "canonical":
@@ -235,7 +258,7 @@ def node_dist_from_logits(logits, m, T, support_size=0, construct_tempered=False
     tail_ids = support[m:]
     ref_t = l[tail_ids[0]]
     if model == "canonical":
-        q = [int(x) for x in numerics.canonical_weights(l[tail_ids], ref_t, T)]
+        q = numerics.canonical_weights(l[tail_ids], ref_t, T).tolist()
     else:
         q = numerics.fp64_weights(l[tail_ids], ref_t, T)
     return NodeDist(support, w1, s1, ExplicitDist(tail_ids, q))
@@ -300,7 +323,8 @@ def make_pool(nd, K, m, y, eps=2.0 ** -40, proxy_rule="rheo", adhoc_proxy=None):
         py = min(1.0, as_prob(w1[0], s1) + eps)
     qt = as_prob(nd.tail.weight(y), nd.tail.total())
     pool.append([m + 1, y, SAMPLED, py, qt])
-    fills = [(v, w) for v, w in zip(x[m:], w1[m:]) if v != y][:K - m - 1]
+    fills = list(itertools.islice(((v, w) for v, w in zip(x[m:], w1[m:]) if v != y),
+                                  K - m - 1))
     for j, (v, w) in enumerate(fills):
         p = as_prob(w, s1)
         pool.append([m + 2 + j, v, FILL, p, p])

@@ -57,15 +57,15 @@ struct rheo_tree {
     TreeDev dev;
     State state = CREATED;
     int level = 0;
-    uint64_t key_prev = 0;                // rng_key of the last expand_level call
     int R = 0;
     int variant = 0;
     int row_mode = 0;                     // sparse levels: 1 one block per row, 0 chunks,
                                           // -1 by the number of rows
     int vG = 1, v_segch = 1, v_grid = 1;  // verification team shape
     int row_min = kRowMin;                // fewest rows for the per-row kernel
-    int v_coop = 0;                       // cooperative launch of the verify kernel
-    float T_expand = 1.0f;
+    uint64_t verify_calls = 0;            // barrier epochs of the verify teams
+    float T_step = 1.0f;                  // temperature and key of the current step
+    uint64_t key_step = 0;
     void* blocks[48] = {};
     const void* draft[16] = {};           // dense: each level's draft rows (borrowed)
     int nblocks = 0;
@@ -98,6 +98,16 @@ int check_ptr(const void* p, const char* name) {
 int check_T(float T) {
     if (!(T > 0.0f) || !std::isfinite(T)) return fail(RHEO_EINVAL, "temperature must be finite and > 0");
     if (!std::isfinite(k_of_T(T))) return fail(RHEO_EINVAL, "temperature too small");
+    return RHEO_OK;
+}
+
+// Every call of one step takes the step's temperature and key: the stored
+// tail weights (and, in dense mode, the q~ verification recomputes from the
+// draft rows) and the draws of the sampled slots depend on both.
+int check_step_args(const rheo_tree* t, float T, uint64_t key, const char* call) {
+    if (std::memcmp(&T, &t->T_step, sizeof(float)) != 0 || key != t->key_step)
+        return fail(RHEO_EINVAL, "%s: T and rng_key must be those of the step's first "
+                    "rheo_expand_level", call);
     return RHEO_OK;
 }
 
@@ -224,7 +234,6 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
     rc = rc ? rc : dalloc(t, &d.porder, B * NN);
     rc = rc ? rc : dalloc(t, &d.err, 1);
     rc = rc ? rc : dalloc(t, &d.team_flag, B * 64);
-    rc = rc ? rc : dalloc(t, &d.team_epoch, B);
     rc = rc ? rc : dalloc(t, &d.team_max, B * 64);
     rc = rc ? rc : dalloc(t, &d.team_sum, B * 64);
     rc = rc ? rc : dalloc(t, &d.team_chunk, B * 1024);
@@ -240,7 +249,6 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
     }
     hipError_t e = hipMemset(d.err, 0, sizeof(int32_t));
     if (e == hipSuccess) e = hipMemset(d.team_flag, 0, B * 64 * sizeof(uint64_t));
-    if (e == hipSuccess) e = hipMemset(d.team_epoch, 0, B * sizeof(uint64_t));
     if (e == hipSuccess) e = hipMemset(d.team_max, 0, B * 64 * sizeof(uint64_t));
     if (e == hipSuccess) e = hipMemset(d.team_sum, 0, B * 64 * sizeof(uint64_t));
     if (e == hipSuccess) e = hipMemset(d.row_cnt, 0, B * d.NE * sizeof(uint32_t));
@@ -256,8 +264,6 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
         return hip_fail(e, "initialising tree state");
     }
     e = verify_shape(d, &t->vG, &t->v_segch, &t->v_grid);
-    // RHEO_VERIFY_COOP=1: launch the verify teams cooperatively
-    if (const char* vc = getenv("RHEO_VERIFY_COOP")) t->v_coop = vc[0] == '1';
     if (e != hipSuccess) {
         free_all(t);
         delete t;
@@ -291,6 +297,12 @@ int rheo_expand_level(rheo_tree* t, const void* logits, float T, uint64_t key, v
     int rc = check_ptr(logits, "draft_logits");
     if (rc) return rc;
     if ((rc = check_T(T))) return rc;
+    if (t->level == 0) {
+        t->T_step = T;
+        t->key_step = key;
+    } else if ((rc = check_step_args(t, T, key, "rheo_expand_level"))) {
+        return rc;
+    }
     LevelArgs a;
     a.logits = logits;
     a.level = t->level;
@@ -298,7 +310,7 @@ int rheo_expand_level(rheo_tree* t, const void* logits, float T, uint64_t key, v
     a.k1 = k_of_T(t->cfg.construct_tempered ? T : 1.0f);
     a.kT = k_of_T(T);
     a.rng_key = key;
-    a.fr_key = t->key_prev;
+    a.fr_key = key;                       // the key of the call that chose the parents
     hipError_t e = hipSuccess;
     if (t->dev.cfull) {
         // the construction totals over the whole rows, read by the pools
@@ -316,8 +328,6 @@ int rheo_expand_level(rheo_tree* t, const void* logits, float T, uint64_t key, v
     }
     if (e != hipSuccess) return hip_fail(e, "expand launch");
     t->draft[t->level] = logits;
-    t->T_expand = T;
-    t->key_prev = key;
     if (++t->level == t->dev.D) t->state = EXPANDED;
     return RHEO_OK;
 }
@@ -376,6 +386,7 @@ int rheo_verify(rheo_tree* t, const void* logits, float T, uint64_t key, int32_t
     int rc = check_ptr(logits, "target_logits");
     if (rc) return rc;
     if ((rc = check_T(T))) return rc;
+    if ((rc = check_step_args(t, T, key, "rheo_verify"))) return rc;
     if (!accepted || !accept_len || !final_token) return fail(RHEO_EINVAL, "NULL output");
     VerifyArgs a;
     a.logits = logits;
@@ -387,8 +398,12 @@ int rheo_verify(rheo_tree* t, const void* logits, float T, uint64_t key, int32_t
     a.final_token = final_token;
     a.G = t->vG;
     for (int i = 0; i < 16; ++i) a.draft[i] = t->draft[i];
-    const hipError_t e = launch_verify(t->dev, a, t->v_segch, t->v_grid, t->v_coop,
-                                       (hipStream_t)stream);
+    a.epoch = 64 * ++t->verify_calls;
+    // about a second of polling; RHEO_VERIFY_SPIN (read at each call) lowers
+    // it, so that tests can force the failure path from the host
+    a.spin = 1L << 20;
+    if (const char* sp = getenv("RHEO_VERIFY_SPIN")) a.spin = atol(sp);
+    const hipError_t e = launch_verify(t->dev, a, t->v_segch, t->v_grid, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "verify launch");
     t->state = VERIFIED;
     return RHEO_OK;

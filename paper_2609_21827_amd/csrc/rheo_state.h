@@ -41,7 +41,6 @@ struct TreeDev {
     int32_t* err;                  // sticky device error flag
     // verification team exchange (see verify.hip)
     uint64_t* team_flag;           // [B][GMAX] arrival epochs
-    uint64_t* team_epoch;          // [B] first barrier epoch of the next call
     uint64_t* team_max;            // [B][GMAX] segment maxima: epoch << 32 | order code
     uint64_t* team_sum;            // [B][GMAX] segment weight sums: epoch << 48 | sum
     uint64_t* team_chunk;          // [B][NCMAX] chunk totals of p's weights
@@ -86,6 +85,8 @@ struct VerifyArgs {
     int NV;                        // chunks per segment
     float kT;
     uint64_t rng_key;
+    uint64_t epoch;                // first barrier epoch of this call (host counter)
+    long spin;                     // polls of a team wait before it gives up
     int32_t* accepted;
     int32_t* accept_len;
     int32_t* final_token;
@@ -97,7 +98,7 @@ hipError_t launch_select(const TreeDev& t, const LevelArgs& a, int variant, hipS
 hipError_t launch_dense(const TreeDev& t, const LevelArgs& a, int nvc, hipStream_t s);
 hipError_t launch_prune(const TreeDev& t, int R, hipStream_t s);
 hipError_t verify_shape(const TreeDev& t, int* G, int* segch, int* grid);
-hipError_t launch_verify(const TreeDev& t, const VerifyArgs& a, int segch, int grid, int coop,
+hipError_t launch_verify(const TreeDev& t, const VerifyArgs& a, int segch, int grid,
                          hipStream_t s);
 
 // expand kernel variants: the chunk each selection block holds in registers

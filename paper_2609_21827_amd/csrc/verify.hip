@@ -28,7 +28,12 @@
 //      above, and the fills under the residual with Z_l for S_p.
 // Team exchanges use agent-scope atomic stores and loads only (they are
 // coherent across the XCDs without cache write-back or invalidation), with
-// arrival epochs in per-block flags and bounded waits.
+// arrival epochs in per-block flags and bounded waits.  The epochs of a call
+// come from the host (a per-handle call counter), so no block depends on
+// another block's progress to learn them.  A wait past its spin limit ends
+// the walk: the team's first block then writes the failure result
+// (accept_len = final_token = -1, accepted all -1) and device error bit 128
+// is set.
 #include <cstdlib>
 
 #include "rheo_device.h"
@@ -41,7 +46,6 @@ constexpr int NWV = NTV / WAVE;
 constexpr int GMAX = 64;
 constexpr int NCMAX = 1024;      // chunks: V <= 262143, chunk >= 256 tokens
 constexpr int SPMAX = 1024 + 16; // stored tail + candidates
-constexpr long kSpinLimit = 1L << 20;   // ~1 s: a wait that long is an error
 
 template <int DT>
 __device__ __forceinline__ float velem(const uint4& v, int k) {
@@ -162,7 +166,7 @@ __device__ u128 block_sum_u128(u128 v, u128* sh) {
 // so no separate barrier or read follows.  *s_M receives the maximum.
 // Bounded like team_barrier.
 __device__ bool team_max_exchange(uint64_t* words, int g, int G, uint64_t epoch, float mx,
-                                  int32_t* err, int* s_ok, float* s_M) {
+                                  long spin_limit, int32_t* err, int* s_ok, float* s_M) {
     const uint32_t e32 = (uint32_t)epoch;
     if (threadIdx.x < WAVE) {
         if (threadIdx.x == 0) {
@@ -181,7 +185,7 @@ __device__ bool team_max_exchange(uint64_t* words, int g, int G, uint64_t epoch,
                 v = unord32((uint32_t)w);
             }
             if (__all(ok)) break;
-            if (++spins > kSpinLimit) {
+            if (++spins > spin_limit) {
                 if (threadIdx.x == 0) {
                     atomicOr(err, 128);
                     *s_ok = 0;
@@ -205,8 +209,8 @@ __device__ bool team_max_exchange(uint64_t* words, int g, int G, uint64_t epoch,
 // the 16-bit comparison cannot mistake it for the current one.  wsum holds
 // the block's per-wave sums.  Bounded like team_barrier.
 __device__ bool team_sum_exchange(uint64_t* words, int g, int G, uint64_t epoch,
-                                  const uint64_t* wsum, int nw, int32_t* err, int* s_ok,
-                                  uint64_t* s_total) {
+                                  const uint64_t* wsum, int nw, long spin_limit, int32_t* err,
+                                  int* s_ok, uint64_t* s_total) {
     constexpr uint64_t M48 = (1ull << 48) - 1;
     const uint64_t e16 = epoch & 0xFFFFull;
     __builtin_amdgcn_s_waitcnt(0);
@@ -230,7 +234,7 @@ __device__ bool team_sum_exchange(uint64_t* words, int g, int G, uint64_t epoch,
                 v = w & M48;
             }
             if (__all(ok)) break;
-            if (++spins > kSpinLimit) {
+            if (++spins > spin_limit) {
                 if (threadIdx.x == 0) {
                     atomicOr(err, 128);
                     *s_ok = 0;
@@ -246,8 +250,8 @@ __device__ bool team_sum_exchange(uint64_t* words, int g, int G, uint64_t epoch,
     return *s_ok != 0;
 }
 
-__device__ bool team_barrier(uint64_t* flags, int g, int G, uint64_t epoch, int32_t* err,
-                             int* s_ok) {
+__device__ bool team_barrier(uint64_t* flags, int g, int G, uint64_t epoch, long spin_limit,
+                             int32_t* err, int* s_ok) {
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (threadIdx.x < WAVE) {
@@ -262,7 +266,7 @@ __device__ bool team_barrier(uint64_t* flags, int g, int G, uint64_t epoch, int3
                 ok = __hip_atomic_load(&flags[threadIdx.x], __ATOMIC_RELAXED,
                                        __HIP_MEMORY_SCOPE_AGENT) >= epoch;
             if (__all(ok)) break;
-            if (++spins > kSpinLimit) {
+            if (++spins > spin_limit) {
                 if (threadIdx.x == 0) {
                     atomicOr(err, 128);
                     *s_ok = 0;
@@ -324,9 +328,9 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
     const int NC = (V + CH - 1) / CH;
     const int64_t nb = (int64_t)b * NN;
     uint64_t* flags = t.team_flag + (int64_t)b * GMAX;
-    // barrier epochs of this call: the team's base, read before any block
-    // of the team can pass its first barrier; the leader advances it on exit
-    const uint64_t epoch = t.team_epoch[b];
+    // barrier epochs of this call: a base from the host, 64 above the
+    // previous call's, so words left from earlier calls never match
+    const uint64_t epoch = a.epoch;
     uint64_t* tmax_x = t.team_max + (int64_t)b * GMAX;
     uint64_t* chunk_x = t.team_chunk + (int64_t)b * NCMAX;
     uint32_t* sp_x = t.team_sp + (int64_t)b * SPMAX;
@@ -350,6 +354,7 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
     }
     __syncthreads();
     int level = 0, nacc = 0;
+    bool failed = false;                      // a team wait timed out
     for (;;) {
         const int cur_p = s_curp, fc = s_fc, e = s_e;
         if (level > t.D || cur_p < 0 || cur_p > a.R) {   // unreachable
@@ -465,8 +470,10 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
             for (int k = 0; k < VEC; ++k) mx = fmaxf(mx, velem<DT>(xv, k));
         }
         mx = block_max<NTV>(mx, s_redf);
-        if (!team_max_exchange(tmax_x, g, G, epoch + 3 * level + 1, mx, t.err, &s_ok, &s_M))
+        if (!team_max_exchange(tmax_x, g, G, epoch + 3 * level + 1, mx, a.spin, t.err, &s_ok, &s_M)) {
+            failed = true;
             break;
+        }
         const int nc = s_nc, spos = s_spos;
         const float M = s_M;
         // ---- 2. weights of the segment, chunk totals, and p's weights at
@@ -509,14 +516,19 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
                 s_tp[i] = cweight(load_logit<DT>(row, s_tid[i]), M, a.kT);
             if (cpos >= 0) s_tp[nt + cpos] = cweight(c_l, M, a.kT);
             if (lane == 0) s_red[wid] = wpart;
-            if (!team_sum_exchange(tsum_x, g, G, epoch + 3 * level + 2, s_red, NWV, t.err, &s_ok,
-                                   &s_Sp))
+            if (!team_sum_exchange(tsum_x, g, G, epoch + 3 * level + 2, s_red, NWV, a.spin, t.err,
+                                   &s_ok, &s_Sp)) {
+                failed = true;
                 break;
+            }
         } else {
             if (cpos >= 0 && ctok >= lo_tok && ctok < hi_tok)
                 __hip_atomic_store(&sp_x[nt + cpos], cweight(c_l, M, a.kT), __ATOMIC_RELAXED,
                                    __HIP_MEMORY_SCOPE_AGENT);
-            if (!team_barrier(flags, g, G, epoch + 3 * level + 2, t.err, &s_ok)) break;
+            if (!team_barrier(flags, g, G, epoch + 3 * level + 2, a.spin, t.err, &s_ok)) {
+                failed = true;
+                break;
+            }
         }
         // ---- 3. Algorithm 1 at this layer, by wave 0 (the chunk totals and
         //         the special weights from the team, S_p, the tail deficit,
@@ -693,7 +705,10 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
                                        __HIP_MEMORY_SCOPE_AGENT);
                 }
             }
-            if (!team_barrier(flags, g, G, epoch + 3 * level + 3, t.err, &s_ok)) break;
+            if (!team_barrier(flags, g, G, epoch + 3 * level + 3, a.spin, t.err, &s_ok)) {
+                failed = true;
+                break;
+            }
             if (tid < WAVE) {
                 __builtin_amdgcn_s_setprio(3);
                 u128 part = 0;
@@ -872,7 +887,13 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
         }
         break;
     }
-    if (g == 0 && tid == 0) t.team_epoch[b] = epoch + 64;   // > every epoch this call used
+    // a timed-out wait: the walk did not complete, so the team's first block
+    // (the only one that writes outputs) reports a defined failure instead
+    if (failed && g == 0 && tid == 0) {
+        a.accept_len[b] = -1;
+        a.final_token[b] = -1;
+        for (int i = 0; i < t.D; ++i) a.accepted[(int64_t)b * t.D + i] = -1;
+    }
 }
 
 static const void* verify_fn(const TreeDev& t) {
@@ -910,19 +931,16 @@ hipError_t verify_shape(const TreeDev& t, int* G_out, int* segch, int* grid) {
 
 // The grid never exceeds what the device holds at once (verify_shape), so
 // on a device that runs nothing else every block is resident from the
-// start and the team barriers complete.  coop = 1 asks the runtime to
-// guarantee that (a cooperative launch, which on this platform adds about
-// 11 us of dispatch delay); otherwise a barrier that waits past its spin
-// limit, because other work held part of the device, ends the walk with
-// device error 128 rather than hanging.
-hipError_t launch_verify(const TreeDev& t, const VerifyArgs& a, int segch, int grid, int coop,
+// start and the team barriers complete; a barrier that waits past its spin
+// limit, because other work held part of the device, ends the walk with the
+// failure result and device error 128 rather than hanging.
+hipError_t launch_verify(const TreeDev& t, const VerifyArgs& a, int segch, int grid,
                          hipStream_t s) {
     const void* fn = verify_fn(t);
     TreeDev tt = t;
     VerifyArgs aa = a;
     aa.NV = segch;
     void* args[] = {&tt, &aa};
-    if (coop) return hipLaunchCooperativeKernel(fn, dim3(grid), dim3(NTV), args, 0, s);
     return hipLaunchKernel(fn, dim3(grid), dim3(NTV), args, 0, s);
 }
 

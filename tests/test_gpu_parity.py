@@ -204,7 +204,6 @@ SHAPES = (
     {"RHEO_EXPAND_VARIANT": "1", "RHEO_VERIFY_BLOCKS": "1024"},
     {"RHEO_EXPAND_ROW": "1"},
     {"RHEO_EXPAND_ROW": "0", "RHEO_VERIFY_BLOCKS": "256"},
-    {"RHEO_VERIFY_COOP": "1"},
 )
 
 
@@ -254,6 +253,68 @@ def test_step_order_enforced(dev):
         tree.prune(3)
     with pytest.raises(RheoError):
         tree.expand_level(rows, 0.0, 1)
+    tree.close()
+
+
+@pytest.mark.parametrize("support", [128, 0])
+def test_step_args_fixed(dev, support):
+    """T and rng_key are the step's: a later expand level or the verify call
+    with another value is refused before anything is enqueued."""
+    from paper_2609_21827_amd.binding import RheoError, RHEO_EINVAL
+    from paper_2609_21827_amd.driver import make_tree
+    w = W["tiny"].with_(support=support)
+    tree = make_tree(w, device=dev)
+    dt = torch.float32
+    tree.begin_step()
+    tree.expand_level(torch.zeros((1, 1, w.V), dtype=dt, device=dev), 1.0, 5)
+    rows = torch.zeros((1, w.n_expand, w.V), dtype=dt, device=dev)
+    for T, key in ((0.9, 5), (1.0, 6)):
+        with pytest.raises(RheoError) as e:
+            tree.expand_level(rows, T, key)
+        assert e.value.code == RHEO_EINVAL
+    for _ in range(w.depth - 1):
+        tree.expand_level(rows, 1.0, 5)
+    tree.prune(w.R)
+    target = torch.zeros((1, w.R + 1, w.V), dtype=dt, device=dev)
+    for T, key in ((0.9, 5), (1.0, 6)):
+        with pytest.raises(RheoError) as e:
+            tree.verify(target, T, key)
+        assert e.value.code == RHEO_EINVAL
+    acc, alen, fin = tree.verify(target, 1.0, 5)
+    torch.cuda.synchronize()
+    assert int(alen[0]) >= 0 and tree.device_error() == 0
+    tree.close()
+
+
+def test_verify_timeout_failure_then_recovery(dev):
+    """A team wait that gives up (forced from the host with a zero spin
+    limit) ends each affected walk with the failure result, never a silent
+    partial walk; the next call on the same handle, whose team words still
+    hold the failed call's values, is exact again."""
+    from paper_2609_21827_amd.driver import make_tree, replay_step, run_step
+    w = W["headline"].with_(name="spin", B=16, depth=3, R=20)
+    tree = make_tree(w, device=dev)
+    rec = {}
+    ref = run_step(tree, w, 0, device=dev, record=rec)
+    torch.cuda.synchronize()
+    assert tree.device_error() == 0
+    os.environ["RHEO_VERIFY_SPIN"] = "0"
+    try:
+        out = [x.cpu() for x in replay_step(tree, rec, w.R)]
+    finally:
+        del os.environ["RHEO_VERIFY_SPIN"]
+    assert tree.device_error() & 128
+    failed = 0
+    for b in range(w.B):
+        if int(out[1][b]) == -1:
+            failed += 1
+            assert int(out[2][b]) == -1 and bool((out[0][b] == -1).all()), b
+        else:               # the team's first block saw every exchange complete
+            assert all(torch.equal(o[b], r[b]) for o, r in zip(out, ref)), b
+    assert failed > 0
+    again = [x.cpu() for x in replay_step(tree, rec, w.R)]
+    for o, r in zip(again, ref):
+        assert torch.equal(o, r)
     tree.close()
 
 
