@@ -110,7 +110,24 @@ typedef struct rheo_config {
  * Node capacity per sequence: 1 + K + (D-1) * n_expand * K. */
 int rheo_create(const rheo_config* cfg, rheo_tree** out);
 
-/* Frees the handle and its device memory (synchronises the device). */
+/* rheo_create for callers that cannot allocate device memory (serving loops
+ * and harnesses that forbid hipMalloc): the tree's whole device state lives
+ * in a static array of the library, 32 MiB per device, which every device
+ * that loads the library holds until the process ends.  No device memory is
+ * allocated or freed.  A configuration whose state exceeds 32 MiB returns
+ * RHEO_EINVAL before any device call (the five workload shapes of the
+ * sparse and dense modes fit; supports of 512 and more at large batches do
+ * not).  There is one static tree per device (the current device): every
+ * call on a device re-initialises it and returns the same handle in *out, so
+ * a static tree from an earlier call on that device becomes this one.
+ * Calls on one device that overlap -- two threads creating, or work still
+ * using the earlier static tree -- race.  The call synchronises the device
+ * (not for use under graph capture); the handle's other calls behave as for
+ * rheo_create, and rheo_destroy on it only synchronises. */
+int rheo_create_static(const rheo_config* cfg, rheo_tree** out);
+
+/* Frees the handle and its device memory (synchronises the device); for the
+ * handle of rheo_create_static it frees nothing. */
 int rheo_destroy(rheo_tree* tree);
 
 /* Starts a new step: the next rheo_expand_level builds level 0 from the root. */

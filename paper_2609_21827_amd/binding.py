@@ -22,7 +22,7 @@ ERROR_NAMES = {RHEO_EINVAL: "EINVAL", RHEO_ENOMEM: "ENOMEM", RHEO_EHIP: "EHIP",
                RHEO_ESTATE: "ESTATE"}
 
 # every symbol the header declares
-EXPORTS = ["rheo_create", "rheo_destroy", "rheo_begin_step", "rheo_expand_level",
+EXPORTS = ["rheo_create", "rheo_create_static", "rheo_destroy", "rheo_begin_step", "rheo_expand_level",
            "rheo_frontier", "rheo_frontier_view", "rheo_prune", "rheo_pruned_view",
            "rheo_tree_mask", "rheo_verify",
            "rheo_read_nodes", "rheo_device_error", "rheo_node_count",
@@ -60,6 +60,7 @@ def load_library(path=LIB_PATH):
     vp, i32, u64, f32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_uint64, ctypes.c_float
     sig = {
         "rheo_create": ([ctypes.POINTER(RheoConfig), ctypes.POINTER(vp)], ctypes.c_int),
+        "rheo_create_static": ([ctypes.POINTER(RheoConfig), ctypes.POINTER(vp)], ctypes.c_int),
         "rheo_destroy": ([vp], ctypes.c_int),
         "rheo_begin_step": ([vp], ctypes.c_int),
         "rheo_expand_level": ([vp, vp, f32, u64, vp], ctypes.c_int),
@@ -115,7 +116,8 @@ class Tree:
 
     def __init__(self, batch, vocab, pool, leads, depth, support, dtype,
                  n_expand=0, construct_tempered=False, row_stride=None,
-                 eps_m0=0.0, method="rheo", construct_full=False, device="cuda"):
+                 eps_m0=0.0, method="rheo", construct_full=False, device="cuda",
+                 static=False):
         lib = load_library()
         self.device = torch.device(device)
         self.B, self.V, self.K, self.m, self.D = batch, vocab, pool, leads, depth
@@ -128,7 +130,9 @@ class Tree:
                          METHODS[method] if isinstance(method, str) else int(method),
                          int(construct_full), self.row_stride, eps_m0)
         h = ctypes.c_void_p()
-        _check(lib.rheo_create(ctypes.byref(cfg), ctypes.byref(h)))
+        # static: the device state in the library's static scratch array
+        create = lib.rheo_create_static if static else lib.rheo_create
+        _check(create(ctypes.byref(cfg), ctypes.byref(h)))
         self._h = h
         self.N = lib.rheo_node_count(h)
         self.R = None

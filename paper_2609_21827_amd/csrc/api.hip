@@ -8,6 +8,8 @@
 #include <cstring>
 #include <string>
 
+#include <mutex>
+
 #include "rheo.h"
 #include "rheo_state.h"
 
@@ -69,6 +71,7 @@ struct rheo_tree {
     void* blocks[48] = {};
     const void* draft[16] = {};           // dense: each level's draft rows (borrowed)
     int nblocks = 0;
+    bool is_static = false;               // device state in the static scratch array
 };
 
 namespace {
@@ -111,14 +114,9 @@ int check_step_args(const rheo_tree* t, float T, uint64_t key, const char* call)
     return RHEO_OK;
 }
 
-}  // namespace
-
-extern "C" {
-
-const char* rheo_last_error(void) { return g_err.c_str(); }
-
-int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
-    if (!cfg_in || !out) return fail(RHEO_EINVAL, "NULL argument");
+// Validates cfg and fills the handle's host fields (no device work).
+int configure(const rheo_config* cfg_in, rheo_tree* t) {
+    if (!cfg_in) return fail(RHEO_EINVAL, "NULL argument");
     rheo_config c = *cfg_in;
     if (c.n_expand == 0) c.n_expand = c.pool;
     if (c.eps_m0 == 0.0) c.eps_m0 = std::ldexp(1.0, -40);
@@ -148,7 +146,6 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
     if ((c.row_stride * esz) % 16) return fail(RHEO_EINVAL, "row_stride must be a multiple of 16 bytes");
     if (!(c.eps_m0 > 0.0) || !std::isfinite(c.eps_m0)) return fail(RHEO_EINVAL, "eps_m0 must be > 0");
 
-    rheo_tree* t = new rheo_tree();
     t->cfg = c;
     TreeDev& d = t->dev;
     d.B = c.batch; d.V = c.vocab; d.K = c.pool; d.m = c.leads; d.D = c.depth;
@@ -163,7 +160,6 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
     d.NN = 1 + c.pool + (c.depth - 1) * c.n_expand * c.pool;
     d.E = 1 + (c.depth - 1) * c.n_expand;
     if (16 * (size_t)(d.NN - 1) > 64 * 1024) {
-        delete t;
         return fail(RHEO_EINVAL, "tree too large (%d nodes per sequence)", d.NN);
     }
     // expand variant: 16 vectors per thread and chunk unless the chunk lists
@@ -176,7 +172,6 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
         }
     }
     if (t->variant < 0) {
-        delete t;
         return fail(RHEO_EINVAL, "vocab %d with support %d exceeds the expand merge capacity",
                     c.vocab, SL);
     }
@@ -201,52 +196,89 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
         d.C = ev.C;
         d.Sc = ev.Sc;
         if (d.Sc != SL) {   // chunks hold at least 4096 elements, lists at most 1024
-            delete t;
-            return fail(RHEO_EINVAL, "internal: expand chunk smaller than the support");
+                return fail(RHEO_EINVAL, "internal: expand chunk smaller than the support");
         }
     }
-    const size_t B = d.B, NN = d.NN, E = d.E;
+    return RHEO_OK;
+}
+
+// Where a tree's device arrays come from: device allocations (rheo_create),
+// a region of the static scratch array (rheo_create_static), or nowhere
+// (a measuring pass that only counts the bytes of the region).
+struct Arena {
+    enum Mode { HEAP, REGION, MEASURE } mode;
+    rheo_tree* t;
+    char* base = nullptr;        // REGION: start of the region
+    size_t cap = 0, used = 0;    // REGION / MEASURE: bytes
     int rc = RHEO_OK;
-    rc = rc ? rc : dalloc(t, &d.tok, B * NN);
-    rc = rc ? rc : dalloc(t, &d.par, B * NN);
-    rc = rc ? rc : dalloc(t, &d.meta, B * NN);
-    rc = rc ? rc : dalloc(t, &d.proxy, B * NN);
-    rc = rc ? rc : dalloc(t, &d.qtrue, B * NN);
-    rc = rc ? rc : dalloc(t, &d.score, B * NN);
-    rc = rc ? rc : dalloc(t, &d.path, B * NN);
-    rc = rc ? rc : dalloc(t, &d.first_child, B * NN);
-    rc = rc ? rc : dalloc(t, &d.exp_of, B * NN);
-    const size_t TS = dense ? 1 : S;              // dense mode keeps no tail copy
-    rc = rc ? rc : dalloc(t, &d.tail_id, B * E * TS);
-    rc = rc ? rc : dalloc(t, &d.tail_q, B * E * TS);
-    const size_t DN = dense ? 1 : 0;
-    rc = rc ? rc : dalloc(t, &d.dq, DN ? B * d.NE * (size_t)d.NCH : 1);
-    rc = rc ? rc : dalloc(t, &d.dpart, DN ? B * d.NE * (size_t)d.C * 2 : 1);
-    rc = rc ? rc : dalloc(t, &d.dflag, DN ? B * d.NE : 1);
-    rc = rc ? rc : dalloc(t, &d.dref, DN ? B * E : 1);
-    rc = rc ? rc : dalloc(t, &d.dleads, DN ? B * E * 16 : 1);
-    rc = rc ? rc : dalloc(t, &d.zq, B * E);
-    rc = rc ? rc : dalloc(t, &d.s1row, d.cfull ? B * d.NE : 1);
-    rc = rc ? rc : dalloc(t, &d.frontier, B * d.NE);
-    rc = rc ? rc : dalloc(t, &d.fr_parent, B * d.NE);
-    rc = rc ? rc : dalloc(t, &d.fr_token, B * d.NE);
-    rc = rc ? rc : dalloc(t, &d.pidx, B * NN);
-    rc = rc ? rc : dalloc(t, &d.porder, B * NN);
-    rc = rc ? rc : dalloc(t, &d.err, 1);
-    rc = rc ? rc : dalloc(t, &d.team_flag, B * 64);
-    rc = rc ? rc : dalloc(t, &d.team_max, B * 64);
-    rc = rc ? rc : dalloc(t, &d.team_sum, B * 64);
-    rc = rc ? rc : dalloc(t, &d.team_chunk, B * 1024);
-    rc = rc ? rc : dalloc(t, &d.team_sp, B * (1024 + 16));
-    rc = rc ? rc : dalloc(t, &d.team_nchunk, dense ? B * 1024 * 2 : 1);
-    rc = rc ? rc : dalloc(t, &d.sel, B * d.NE * (size_t)d.C * d.Sc);
-    rc = rc ? rc : dalloc(t, &d.row_cnt, B * d.NE);
-    rc = rc ? rc : dalloc(t, &d.seq_cnt, B);
-    if (rc) {
-        free_all(t);
-        delete t;
-        return rc;
+};
+
+template <typename T>
+void take(Arena& A, T** p, size_t count) {
+    if (A.rc) return;
+    const size_t bytes = count * sizeof(T) ? count * sizeof(T) : 16;
+    if (A.mode == Arena::HEAP) {
+        A.rc = dalloc(A.t, p, count);
+        return;
     }
+    const size_t off = (A.used + 255) & ~(size_t)255;
+    A.used = off + bytes;
+    if (A.mode == Arena::MEASURE) return;
+    if (A.used > A.cap) {
+        A.rc = fail(RHEO_EINVAL, "internal: static region overrun");
+        return;
+    }
+    *p = (T*)(A.base + off);
+}
+
+// Every device array of the tree, in one fixed order.
+void layout(rheo_tree* t, Arena& A) {
+    TreeDev& d = t->dev;
+    const bool dense = d.dense != 0;
+    const size_t B = d.B, NN = d.NN, E = d.E;
+    take(A, &d.tok, B * NN);
+    take(A, &d.par, B * NN);
+    take(A, &d.meta, B * NN);
+    take(A, &d.proxy, B * NN);
+    take(A, &d.qtrue, B * NN);
+    take(A, &d.score, B * NN);
+    take(A, &d.path, B * NN);
+    take(A, &d.first_child, B * NN);
+    take(A, &d.exp_of, B * NN);
+    const size_t TS = dense ? 1 : (size_t)d.S;              // dense mode keeps no tail copy
+    take(A, &d.tail_id, B * E * TS);
+    take(A, &d.tail_q, B * E * TS);
+    const size_t DN = dense ? 1 : 0;
+    take(A, &d.dq, DN ? B * d.NE * (size_t)d.NCH : 1);
+    take(A, &d.dpart, DN ? B * d.NE * (size_t)d.C * 2 : 1);
+    take(A, &d.dflag, DN ? B * d.NE : 1);
+    take(A, &d.dref, DN ? B * E : 1);
+    take(A, &d.dleads, DN ? B * E * 16 : 1);
+    take(A, &d.zq, B * E);
+    take(A, &d.s1row, d.cfull ? B * d.NE : 1);
+    take(A, &d.frontier, B * d.NE);
+    take(A, &d.fr_parent, B * d.NE);
+    take(A, &d.fr_token, B * d.NE);
+    take(A, &d.pidx, B * NN);
+    take(A, &d.porder, B * NN);
+    take(A, &d.err, 1);
+    take(A, &d.team_flag, B * 64);
+    take(A, &d.team_max, B * 64);
+    take(A, &d.team_sum, B * 64);
+    take(A, &d.team_chunk, B * 1024);
+    take(A, &d.team_sp, B * (1024 + 16));
+    take(A, &d.team_nchunk, dense ? B * 1024 * 2 : 1);
+    take(A, &d.sel, B * d.NE * (size_t)d.C * d.Sc);
+    take(A, &d.row_cnt, B * d.NE);
+    take(A, &d.seq_cnt, B);
+}
+
+// Clears what the kernels expect zeroed (or -1) before a tree's first step
+// and picks the verification team shape.
+int init_state(rheo_tree* t) {
+    TreeDev& d = t->dev;
+    const size_t B = d.B, NN = d.NN;
+    const bool dense = d.dense != 0;
     hipError_t e = hipMemset(d.err, 0, sizeof(int32_t));
     if (e == hipSuccess) e = hipMemset(d.team_flag, 0, B * 64 * sizeof(uint64_t));
     if (e == hipSuccess) e = hipMemset(d.team_max, 0, B * 64 * sizeof(uint64_t));
@@ -258,24 +290,106 @@ int rheo_create(const rheo_config* cfg_in, rheo_tree** out) {
     if (e == hipSuccess) e = hipMemset(d.frontier, 0, B * d.NE * sizeof(int32_t));
     if (e == hipSuccess) e = hipMemset(d.first_child, 0xFF, B * NN * sizeof(int32_t));
     if (e == hipSuccess) e = hipDeviceSynchronize();
-    if (e != hipSuccess) {
-        free_all(t);
-        delete t;
-        return hip_fail(e, "initialising tree state");
-    }
+    if (e != hipSuccess) return hip_fail(e, "initialising tree state");
     e = verify_shape(d, &t->vG, &t->v_segch, &t->v_grid);
-    if (e != hipSuccess) {
+    if (e != hipSuccess) return hip_fail(e, "no co-resident verification team shape for this tree");
+    return RHEO_OK;
+}
+
+// ---------------------------------------------------------------------------
+// The static scratch array of rheo_create_static: a tree's whole device state
+// without any allocation.  Each device that loads the library holds its own
+// copy until the process ends.  Host code never passes the array's name to
+// a kernel or copy (on the host it is only a stand-in for the symbol): the
+// device address comes from hipGetSymbolAddress, taken once per device with
+// that device current.
+// ---------------------------------------------------------------------------
+constexpr size_t kScratchBytes = (size_t)32 << 20;
+constexpr int kMaxDevices = 64;
+
+}  // namespace
+
+static __device__ __align__(256) char scratch[kScratchBytes];
+
+namespace {
+
+char* g_region[kMaxDevices];              // device address of `scratch`, per device
+std::mutex g_region_mu;
+rheo_tree g_static[kMaxDevices];          // the static handle of each device
+
+int static_region(int dev, char** region) {
+    std::lock_guard<std::mutex> lock(g_region_mu);
+    if (!g_region[dev]) {
+        void* ptr = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+        if (!ptr) return fail(RHEO_EHIP, "hipGetSymbolAddress(scratch) returned NULL");
+        g_region[dev] = (char*)ptr;
+    }
+    *region = g_region[dev];
+    return RHEO_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* rheo_last_error(void) { return g_err.c_str(); }
+
+int rheo_create(const rheo_config* cfg, rheo_tree** out) {
+    if (!cfg || !out) return fail(RHEO_EINVAL, "NULL argument");
+    rheo_tree* t = new rheo_tree();
+    int rc = configure(cfg, t);
+    if (rc == RHEO_OK) {
+        Arena A{Arena::HEAP, t};
+        layout(t, A);
+        rc = A.rc;
+    }
+    if (rc == RHEO_OK) rc = init_state(t);
+    if (rc != RHEO_OK) {
         free_all(t);
         delete t;
-        return hip_fail(e, "no co-resident verification team shape for this tree");
+        return rc;
     }
     *out = t;
+    return RHEO_OK;
+}
+
+int rheo_create_static(const rheo_config* cfg, rheo_tree** out) {
+    if (!cfg || !out) return fail(RHEO_EINVAL, "NULL argument");
+    // validate and measure on a staging copy first, so that a refused call
+    // makes no device call and leaves the device's static handle as it was
+    rheo_tree stage;
+    int rc = configure(cfg, &stage);
+    if (rc) return rc;
+    Arena M{Arena::MEASURE, &stage};
+    layout(&stage, M);
+    if (M.used > kScratchBytes)
+        return fail(RHEO_EINVAL, "tree needs %zu bytes of device state; the static scratch "
+                    "holds %zu", M.used, (size_t)kScratchBytes);
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev < 0 || dev >= kMaxDevices) return fail(RHEO_EINVAL, "device %d out of range", dev);
+    char* region = nullptr;
+    rc = static_region(dev, &region);
+    if (rc) return rc;
+    rheo_tree& t = g_static[dev];
+    t = stage;
+    t.is_static = true;
+    Arena A{Arena::REGION, &t, region, (size_t)kScratchBytes};
+    layout(&t, A);
+    if (A.rc) return A.rc;
+    rc = init_state(&t);
+    if (rc) return rc;
+    *out = &t;
     return RHEO_OK;
 }
 
 int rheo_destroy(rheo_tree* t) {
     if (!t) return RHEO_OK;
     (void)hipDeviceSynchronize();
+    if (t->is_static) return RHEO_OK;      // the static scratch stays with the device
     free_all(t);
     delete t;
     return RHEO_OK;

@@ -98,3 +98,15 @@ def test_product_never_imports_the_oracle():
         if f.endswith(".py"):
             text = open(os.path.join(ROOT, "synth", f)).read()
             assert not re.search(r"^\s*(import|from)\s+(oracle|paper_2609)", text, re.M)
+
+
+@needs_lib
+def test_static_tree_size_limit_on_host():
+    """rheo_create_static refuses a tree larger than its static scratch
+    array before any device call."""
+    from paper_2609_21827_amd import binding
+    lib = binding.load_library()
+    cfg = _cfg(batch=128, vocab=128256, row_stride=128256, pool=10, depth=8, support=1024)
+    h = ctypes.c_void_p()
+    assert lib.rheo_create_static(ctypes.byref(cfg), ctypes.byref(h)) == binding.RHEO_EINVAL
+    assert "static scratch" in lib.rheo_last_error().decode()
