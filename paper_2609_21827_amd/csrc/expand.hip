@@ -153,6 +153,14 @@ __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, 
     auto filled = [&](uint64_t k) {
         return (uint32_t)key_id(k) >= (uint32_t)t.V ? logit_key(-INFINITY, 0u) : k;
     };
+    // the tail entry of a support key: counting (small supports) ranks
+    // id << 32 | q (~0 off the tail); sorting ranks the complemented id (0
+    // off the tail)
+    auto tail_code = [&](bool tail, uint64_t tk, uint32_t q) -> uint64_t {
+        if constexpr (SORT_TAIL)
+            return tail ? (uint64_t)(0xFFFFFFFFu - (uint32_t)key_id(tk)) + 1 : 0ull;
+        return tail ? (((uint64_t)(uint32_t)key_id(tk) << 32) | q) : ~0ull;
+    };
     const float M = key_value(filled(s_top[0]));
     const float ref0 = key_value(filled(s_top[m]));
     uint64_t part1 = 0, partq = 0;
@@ -171,7 +179,7 @@ __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, 
         const uint32_t q = tail ? cweight(v, ref0, a.kT) : 0u;
         s_q[i] = q;
         partq += q;
-        s_k2[i] = tail ? (uint64_t)(0xFFFFFFFFu - (uint32_t)key_id(tk)) + 1 : 0ull;
+        s_k2[i] = tail_code(tail, tk, q);
     }
     uint64_t S1, Zq;
     psum2<NT>(part1, partq, s_red, &S1, &Zq);
@@ -204,7 +212,7 @@ __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, 
             const uint32_t q = tail ? cweight(key_value(tk), ref_t, a.kT) : 0u;
             s_q[i] = q;
             partq += q;
-            s_k2[i] = tail ? (uint64_t)(0xFFFFFFFFu - (uint32_t)key_id(tk)) + 1 : 0ull;
+            s_k2[i] = tail_code(tail, tk, q);
         }
         Zq = psum<NT>(partq, s_red);
     };
@@ -224,13 +232,11 @@ __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, 
     if constexpr (!SORT_TAIL) {
         auto tail_count = [&]() {
             const uint64_t tt = __umul64hi(u, Zq);
-            rank_prefix<NT>(s_k2, s_q, S, [&](int i, int ir, uint64_t pre) {
-                if (s_k2[i] != 0ull) {
-                    const uint32_t q = s_q[i];
-                    t.tail_id[tail_base + ir] = key_id(s_top[i]);
-                    t.tail_q[tail_base + ir] = q;
-                    if (pre <= tt && tt - pre < (uint64_t)q) *s_yi = i;
-                }
+            id_prefix<NT>(s_k2, S, [&](int i, int ir, uint64_t pre) {
+                const uint32_t q = (uint32_t)s_k2[i];
+                t.tail_id[tail_base + ir] = key_id(s_top[i]);
+                t.tail_q[tail_base + ir] = q;
+                if (pre <= tt && tt - pre < (uint64_t)q) *s_yi = i;
             });
         };
         tail_count();

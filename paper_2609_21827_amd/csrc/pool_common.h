@@ -110,6 +110,50 @@ __device__ __forceinline__ void rank_prefix(const uint64_t* keys, const uint32_t
     }
 }
 
+// Ranks by id and prefix masses of the tail entries e[0..n): e[i] = id << 32
+// | weight for a tail entry, ~0 for an entry off the tail.  For every tail
+// entry i, the count of tail entries with a smaller id and the sum of their
+// weights, split over F lanes (F a power of two, F * n <= NT, F <= 8), each
+// lane scanning a contiguous run of the entries two at a time (e 16-byte
+// aligned); fn(i, count, mass) is called once per tail entry by one lane.
+template <int NT, typename Fn>
+__device__ __forceinline__ void id_prefix(const uint64_t* e, int n, Fn fn) {
+    const int t = threadIdx.x % NT;
+    int F = 1;
+    while (F < 8 && 2 * F * n <= NT) F *= 2;
+    const int sub = t % F;
+    const int L = ((n + F - 1) / F + 1) & ~1;
+    const int j0 = min(sub * L, n), j1 = min(j0 + L, n);
+    const ulonglong2* ep = (const ulonglong2*)e;
+    for (int base = 0; base < n; base += NT / F) {
+        const int i = base + t / F;
+        const uint64_t me = e[i < n ? i : 0];
+        const uint32_t id = (uint32_t)(me >> 32);
+        int c = 0;
+        uint64_t pre = 0;
+        int j = j0;
+        for (; j + 1 < j1; j += 2) {
+            const ulonglong2 x = ep[j / 2];
+            const bool lx = (uint32_t)(x.x >> 32) < id, ly = (uint32_t)(x.y >> 32) < id;
+            c += (int)lx + (int)ly;
+            pre += (uint64_t)(lx ? (uint32_t)x.x : 0u) + (uint64_t)(ly ? (uint32_t)x.y : 0u);
+        }
+        if (j < j1) {
+            const uint64_t x = e[j];
+            const bool lx = (uint32_t)(x >> 32) < id;
+            c += (int)lx;
+            pre += lx ? (uint32_t)x : 0u;
+        }
+        for (int o = 1; o < F; o <<= 1) {
+            c += __shfl_xor(c, o);
+            const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)pre, o);
+            const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(pre >> 32), o);
+            pre += ((uint64_t)hi << 32) | lo;
+        }
+        if (i < n && sub == 0 && me != ~0ull) fn(i, c, pre);
+    }
+}
+
 // Synchronisation and sums over the NT threads that form a pool: one wave
 // (small supports) or the whole block.
 template <int NT>
@@ -256,11 +300,14 @@ __device__ __forceinline__ void select_frontier(const TreeDev& t, const LevelArg
     if (!s_lastseq) return;
     const int n = a.P * K;                       // <= 225
     const int cb = (level == 0) ? 1 : 1 + K + (level - 1) * NE * K;
+    // every child's priority key and token in one round of loads
+    int tok = -1;
     if (tid < n) {
         const int64_t o = nb + cb + tid;
         const double sc = __longlong_as_double((long long)__hip_atomic_load(
             (uint64_t*)&t.score[o], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
         const uint64_t pa = __hip_atomic_load(&t.path[o], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        tok = __hip_atomic_load(&t.tok[o], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         uint64_t hi, lo;
         prio_key(sc, level + 1, pa, hi, lo);
         s_hi[tid] = hi;
@@ -278,8 +325,7 @@ __device__ __forceinline__ void select_frontier(const TreeDev& t, const LevelArg
         if (rk < NE) {
             t.frontier[(int64_t)b * NE + rk] = cb + tid;
             t.fr_parent[(int64_t)b * NE + rk] = tid / K;
-            t.fr_token[(int64_t)b * NE + rk] =
-                __hip_atomic_load(&t.tok[nb + cb + tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            t.fr_token[(int64_t)b * NE + rk] = tok;
         }
     }
 }
