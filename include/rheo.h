@@ -33,7 +33,13 @@
  *     the device state as it was.
  *   - Logit rows: dtype RHEO_F32 or RHEO_BF16, V contiguous elements per row,
  *     consecutive rows row_stride elements apart, base pointer 16-byte aligned
- *     and row_stride a multiple of 16 bytes.  Logits must be finite.
+ *     and row_stride a multiple of 16 bytes.  A logit is finite or -inf (a
+ *     masked token, the truncation of Sec. 3.2: probability 0).  NaN and
+ *     +inf are not allowed and not checked.  Device error bit 9 (512)
+ *     reports the cases where the method is undefined: a draft row whose
+ *     x_{m+1} (the (m+1)-th token by construction weight, ties by id) has
+ *     logit -inf, so q~_T has no reference; a target row with no finite
+ *     logit (see rheo_verify).
  *   - Decisions are exact: each probability is an integer weight (a
  *     fixed-point softmax numerator evaluated by a fixed fp32 operation
  *     sequence), sums are exact 64-bit integers and every sampling or
@@ -215,7 +221,9 @@ int rheo_tree_mask(rheo_tree* tree, uint8_t* mask, int32_t* depth, void* stream)
  * about a second then ends that sequence's walk with the failure result
  * accept_len[b] = final_token[b] = -1 and accepted[b][*] = -1, and sets
  * device error bit 7 (128).  Callers check accept_len >= 0; a failed
- * sequence's step is not Algorithm 1's and must be run again. */
+ * sequence's step is not Algorithm 1's and must be run again.  A walk that
+ * reaches a node whose target row has no finite logit (p undefined) ends
+ * with the same failure result and sets device error bit 9 (512). */
 int rheo_verify(rheo_tree* tree, const void* target_logits, float T,
                 uint64_t rng_key, int32_t* accepted, int32_t* accept_len,
                 int32_t* final_token, void* stream);
@@ -235,7 +243,8 @@ int rheo_read_nodes(rheo_tree* tree, int32_t* token, int32_t* parent,
  * tail, bit 3: residual sample out of range, bit 4: corrupt frontier,
  * bit 5: corrupt verification walk, bit 6: invalid launch shape, bit 7:
  * verification team barrier timed out, bit 8: a support slot left empty by
- * the expand merge).
+ * the expand merge, bit 9: a draft row whose x_{m+1} is -inf or a target
+ * row without a finite logit).
  * Diagnostic only. */
 int rheo_device_error(rheo_tree* tree, int32_t* host_flag);
 

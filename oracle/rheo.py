@@ -207,6 +207,18 @@ def rank_order(ids, weights):
     return sorted(range(len(ids)), key=lambda i: (-weights[i], int(ids[i])))
 
 
+class UndefinedRow(ValueError):
+    """A logit row on which the method is undefined."""
+
+
+def _check_tail_reference(l_ref):
+    """q~_T = q_T / z is evaluated relative to x_{m+1}'s logit; a masked
+    token (logit -inf, probability 0 after the truncation of Sec. 3.2) there
+    leaves it without a reference (and z may vanish): undefined."""
+    if not np.float32(l_ref) > -np.inf:
+        raise UndefinedRow("x_{m+1} has logit -inf")
+
+
 def node_dist_from_logits(logits, m, T, support_size=0, construct_tempered=False,
                           model="canonical", construct_full=False):
     """Build the node's distributions from one row of draft logits.
@@ -242,6 +254,7 @@ def node_dist_from_logits(logits, m, T, support_size=0, construct_tempered=False
         if construct_full and len(sup) < V:
             s1 = int(numerics.canonical_weights(l, ref, Tc).sum())
         tail_np = sup_r[m:]
+        _check_tail_reference(l[tail_np[0]])
         q = numerics.canonical_weights(l[tail_np], l[tail_np[0]], T)
         return NodeDist(support, w1, s1, ExplicitDist(tail_np, q))
     else:
@@ -257,6 +270,7 @@ def node_dist_from_logits(logits, m, T, support_size=0, construct_tempered=False
             s1 = sum(numerics.fp64_weights(l, ref, Tc))
     tail_ids = support[m:]
     ref_t = l[tail_ids[0]]
+    _check_tail_reference(ref_t)
     if model == "canonical":
         q = numerics.canonical_weights(l[tail_ids], ref_t, T).tolist()
     else:
@@ -283,6 +297,8 @@ def target_weights(logits, T, model="canonical"):
     truncates p); weights relative to the row maximum."""
     l = np.asarray(logits, dtype=np.float32)
     ref = l.max()
+    if not ref > -np.inf:
+        raise UndefinedRow("target row has no finite logit")
     if model == "canonical":
         return numerics.canonical_weights(l, ref, T)
     return numerics.fp64_weights(l, ref, T)

@@ -276,6 +276,7 @@ __global__ __launch_bounds__(NTD) void k_dpool(TreeDev t, LevelArgs a) {
         Zq += t.dpart[((int64_t)row * C + c) * 2 + 1];
     }
     const float ref_t = key_value(s_x[m]);
+    if (tid == 0 && !(ref_t > -INFINITY)) atomicOr(t.err, 512);   // x_{m+1} is -inf
     const int nch = NCH;
     if (ref_t == key_value(s_tl[m])) {
         for (int i = tid; i < nch; i += NTD) s_sub[i] = t.dq[(int64_t)row * NCH + i];

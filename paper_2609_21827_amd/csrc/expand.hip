@@ -48,10 +48,11 @@ __device__ __forceinline__ float elem(const uint4& v, int k) {
     return __uint_as_float(w[k]);
 }
 
-// Vector vi (VEC consecutive elements) of a row; elements past V read as the
-// most negative finite value (bf16 0xFF7F, fp32 -inf).  A bf16 pair read as
-// one fp32 word must never be a NaN (the maxima below compare raw words), and
-// 0xFF80 (-inf) in the high half would make it one.
+// Vector vi (VEC consecutive elements) of a row; elements past V read as
+// bf16 0xFFFF (a NaN: it drops out of the raw-word maxima below, whose
+// kernels run with the IEEE mode bit clear, and its order code 0 lies below
+// that of -inf) or fp32 -inf (ranked after every logit by its id).  Every
+// consumer also checks the index against V.
 template <int DT>
 __device__ __forceinline__ uint4 load_row_vec(const char* base, int vi, int V) {
     constexpr int VEC = DT ? 8 : 4;
@@ -64,8 +65,8 @@ __device__ __forceinline__ uint4 load_row_vec(const char* base, int vi, int V) {
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const int e0 = e + 2 * q;
-            const uint32_t lo = (e0 < V) ? p16[e0] : 0xFF7Fu;
-            const uint32_t hi = (e0 + 1 < V) ? p16[e0 + 1] : 0xFF7Fu;
+            const uint32_t lo = (e0 < V) ? p16[e0] : 0xFFFFu;
+            const uint32_t hi = (e0 + 1 < V) ? p16[e0 + 1] : 0xFFFFu;
             w[q] = lo | (hi << 16);
         }
     } else {
@@ -290,6 +291,9 @@ __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, 
     }
 
     if (tid == 0) {
+        // q~_T is taken relative to x_{m+1}: undefined when its logit is
+        // -inf (fewer than m + 1 tokens of the support above the rest)
+        if (!(key_value(s_top[xs(m)]) > -INFINITY)) atomicOr(t.err, 512);
         t.zq[(int64_t)b * t.E + e_idx] = Zq;
         t.first_child[nb + pu] = cb + j * K;
         t.exp_of[nb + pu] = e_idx;
@@ -483,11 +487,12 @@ __device__ __forceinline__ uint64_t row_key_of32(uint32_t k, int e0) {
     return ((uint64_t)o << 32) | (uint64_t)(0xFFFFFFFFu - id);
 }
 
-// max(a, b, c) of finite fp32 values in one instruction (no NaN quieting:
-// the operands are never NaN).
-__device__ __forceinline__ float max3_finite(float a, float b, float c) {
+// max(a, b, c) in one instruction; with the IEEE mode bit clear (the
+// caller's kernel runs ieee_mode_off first) a NaN operand is ignored.
+// Volatile: kept in program order after the mode change.
+__device__ __forceinline__ float max3_nan_drop(float a, float b, float c) {
     float r;
-    asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+    asm volatile("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
     return r;
 }
 
@@ -495,13 +500,16 @@ __device__ __forceinline__ float max3_finite(float a, float b, float c) {
 // word read as fp32 is its high element plus a fraction of one bf16 ulp made
 // of the low element's bits, so the maximum over the raw words and the
 // unpacked low elements, with its low 16 bits cleared, is exactly the
-// largest element; logits and padding are finite, so no word is a NaN).
-// Returned with garbage in the low 16 bits.
+// largest element).  A word whose high element is -inf (and low element not
+// +0) is a NaN and is dropped, which loses nothing: -inf is the least
+// logit, and the low element counts through its own unpacked operand.
+// Padding (0xFFFF) drops out the same way; a vector of padding alone gives
+// a NaN (order code 0).  Returned with garbage in the low 16 bits.
 __device__ __forceinline__ uint32_t bf16x8_max_raw(const uint4& v) {
-    float m = max3_finite(__uint_as_float(v.x), bf_lo(v.x), __uint_as_float(v.y));
-    m = max3_finite(m, bf_lo(v.y), __uint_as_float(v.z));
-    m = max3_finite(m, bf_lo(v.z), __uint_as_float(v.w));
-    m = max3_finite(m, bf_lo(v.w), bf_lo(v.w));
+    float m = max3_nan_drop(__uint_as_float(v.x), bf_lo(v.x), __uint_as_float(v.y));
+    m = max3_nan_drop(m, bf_lo(v.y), __uint_as_float(v.z));
+    m = max3_nan_drop(m, bf_lo(v.z), __uint_as_float(v.w));
+    m = max3_nan_drop(m, bf_lo(v.w), bf_lo(v.w));
     return __float_as_uint(m);
 }
 
@@ -821,6 +829,7 @@ __device__ __forceinline__ void select_block(const TreeDev& t, const LevelArgs& 
     __shared__ int s_redi[NW];
     uint32_t* s_k32 = (uint32_t*)s_keys;
 
+    ieee_mode_off();                             // NaN words drop out of the maxima
     const int tid = threadIdx.x;
     const int lane = tid % WAVE, wid = tid / WAVE;
     const int c = blockIdx.x;
@@ -1100,6 +1109,7 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
     uint64_t* s_keys = LS ? s_top : s_keys_st;
     int* s_cvi = LS ? (int*)s_k2 : s_cvi_st;
 
+    ieee_mode_off();                             // NaN words drop out of the maxima
     const int tid = threadIdx.x, lane = tid % WAVE, wid = tid / WAVE;
     const int row = blockIdx.x;
     const int b = row / a.P, j = row % a.P;

@@ -97,6 +97,15 @@ __device__ __forceinline__ uint4 load_stream16(const void* p) {
     return make_uint4(v.x, v.y, v.z, v.w);
 }
 
+// Clears the IEEE bit of the wave's MODE register (hardware register 1,
+// bit 9).  With it clear, v_max_f32 / v_max3_f32 return the other operand
+// of a NaN operand, signalling or quiet, instead of quieting it.  Kernels
+// that take maxima over raw bf16-pair words call it first: such a word is a
+// NaN whenever its high element is -inf and its low element is not +0, and
+// row padding is a NaN pattern, so both must drop out of the maxima.  It
+// changes nothing for non-NaN operands.
+__device__ __forceinline__ void ieee_mode_off() { __builtin_amdgcn_s_setreg(1 | (9 << 6), 0); }
+
 // bf16 pairs packed in a uint32: low and high element as fp32 (exact).
 __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }

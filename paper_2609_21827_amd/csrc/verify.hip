@@ -33,7 +33,8 @@
 // another block's progress to learn them.  A wait past its spin limit ends
 // the walk: the team's first block then writes the failure result
 // (accept_len = final_token = -1, accepted all -1) and device error bit 128
-// is set.
+// is set.  A visited node whose target row has no finite logit (p
+// undefined) ends the walk with the same result and device error bit 512.
 #include <cstdlib>
 
 #include "rheo_device.h"
@@ -354,7 +355,7 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
     }
     __syncthreads();
     int level = 0, nacc = 0;
-    bool failed = false;                      // a team wait timed out
+    bool failed = false;                      // a team wait timed out, or no finite target logit
     for (;;) {
         const int cur_p = s_curp, fc = s_fc, e = s_e;
         if (level > t.D || cur_p < 0 || cur_p > a.R) {   // unreachable
@@ -476,6 +477,13 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
         }
         const int nc = s_nc, spos = s_spos;
         const float M = s_M;
+        if (!(M > -INFINITY)) {
+            // no finite target logit at this node: p is undefined.  Every
+            // block of the team holds the same M, so all leave here.
+            if (g == 0 && tid == 0) atomicOr(t.err, 512);
+            failed = true;
+            break;
+        }
         // ---- 2. weights of the segment, chunk totals, and p's weights at
         //         the special tokens ------------------------------------------
         uint64_t wpart = 0;                  // this wave's sum over its chunks
@@ -887,8 +895,9 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
         }
         break;
     }
-    // a timed-out wait: the walk did not complete, so the team's first block
-    // (the only one that writes outputs) reports a defined failure instead
+    // a timed-out wait or an undefined target row: the walk did not
+    // complete, so the team's first block (the only one that writes outputs)
+    // reports a defined failure instead
     if (failed && g == 0 && tid == 0) {
         a.accept_len[b] = -1;
         a.final_token[b] = -1;

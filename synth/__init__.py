@@ -24,8 +24,15 @@ fp32 row):
   near_ties > 0 shifts the row's maximum to 0.125 and puts the next fp32
           values below it on low token ids (distinct logits whose integer
           weights coincide)
+  mask > 0 sets each token to -inf with probability `mask` (a keyed 16-bit
+          hash of (node key, token) below mask * 2^16): a masked vocabulary
+  mask_tail > 0 sets the last mask_tail token ids of every row to -inf (a
+          padded vocabulary)
   target  = draft row of the same node + sigma_t * N'_v (an independent
-          noise stream of the same node key), rounded like the draft
+          noise stream of the same node key), rounded like the draft; a
+          masked draft token stays -inf, and mask_target > 0 masks a further
+          keyed fraction of the target's tokens (tokens the draft proposes
+          and the target forbids)
 Noise variates come from 65536-entry quantile tables indexed by a 16-bit
 hash of (node key, token): a discretised N(0,1) or t(3).
 """
@@ -83,6 +90,9 @@ class Workload:
                                 # baseline, App. D.2) or "topk" (no sampled slot)
     eps_m0: float = 2.0 ** -40
     steps: int = 1              # steps the workload description asks for
+    mask: float = 0.0           # fraction of tokens masked to -inf (keyed per row)
+    mask_tail: int = 0          # last token ids masked to -inf in every row
+    mask_target: float = 0.0    # fraction of tokens masked in target rows only
 
     def __post_init__(self):
         if self.n_expand is None:
@@ -239,6 +249,30 @@ def _quantise(w, rows):
 
 def _draft_fp32(w, keys, device):
     """fp32 draft rows for node keys (before dtype rounding)."""
+    return _masked(w, keys, _draft_unmasked(w, keys, device), device)
+
+
+def _mask_hashed(w, keys, row, frac, salt, device):
+    """Tokens whose keyed 16-bit hash lies below frac * 2^16 set to -inf."""
+    v = torch.arange(w.V, dtype=torch.int64, device=device).view(1, -1)
+    lo, hi = _key_words(keys, salt, device)
+    thr = int(round(float(frac) * 65536))
+    return torch.where(_noise_index(lo, hi, v) < thr,
+                       torch.tensor(-np.inf, dtype=torch.float32, device=device), row)
+
+
+def _masked(w, keys, row, device):
+    """Masked vocabulary: tokens set to -inf by a keyed hash, and the last
+    ``mask_tail`` ids of every row."""
+    if w.mask > 0:
+        row = _mask_hashed(w, keys, row, w.mask, 0x3333, device)
+    if w.mask_tail > 0:
+        row = row.clone()
+        row[:, w.V - w.mask_tail:] = -np.inf
+    return row
+
+
+def _draft_unmasked(w, keys, device):
     normal, t3 = _tables(device)
     V = w.V
     if w.recipe == "flat":
@@ -308,10 +342,10 @@ def target_rows(w, keys, sigmas, device="cpu", chunk=256):
         idx = _noise_index(lo, hi, v)
         sg = torch.tensor([np.float32(s) for s in sigmas[i:i + chunk]],
                           dtype=torch.float32, device=device).view(-1, 1)
-        if w.recipe == "flat":
-            out.append(_round(w, base))
-        else:
-            out.append(_round(w, _quantise(w, base + normal[idx] * sg)))
+        row = base if w.recipe == "flat" else _quantise(w, base + normal[idx] * sg)
+        if w.mask_target > 0:
+            row = _mask_hashed(w, ks, row, w.mask_target, 0x4444, device)
+        out.append(_round(w, row))
     return torch.cat(out, 0)
 
 
