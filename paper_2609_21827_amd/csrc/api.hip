@@ -65,7 +65,6 @@ struct rheo_tree {
                                           // -1 by the number of rows
     int vG = 1, v_segch = 1, v_grid = 1;  // verification team shape
     int row_min = kRowMin;                // fewest rows for the per-row kernel
-    uint64_t verify_calls = 0;            // barrier epochs of the verify teams
     float T_step = 1.0f;                  // temperature and key of the current step
     uint64_t key_step = 0;
     void* blocks[48] = {};
@@ -262,6 +261,7 @@ void layout(rheo_tree* t, Arena& A) {
     take(A, &d.pidx, B * NN);
     take(A, &d.porder, B * NN);
     take(A, &d.err, 1);
+    take(A, &d.team_ticket, B);
     take(A, &d.team_flag, B * 64);
     take(A, &d.team_max, B * 64);
     take(A, &d.team_sum, B * 64);
@@ -280,6 +280,7 @@ int init_state(rheo_tree* t) {
     const size_t B = d.B, NN = d.NN;
     const bool dense = d.dense != 0;
     hipError_t e = hipMemset(d.err, 0, sizeof(int32_t));
+    if (e == hipSuccess) e = hipMemset(d.team_ticket, 0, B * sizeof(uint64_t));
     if (e == hipSuccess) e = hipMemset(d.team_flag, 0, B * 64 * sizeof(uint64_t));
     if (e == hipSuccess) e = hipMemset(d.team_max, 0, B * 64 * sizeof(uint64_t));
     if (e == hipSuccess) e = hipMemset(d.team_sum, 0, B * 64 * sizeof(uint64_t));
@@ -512,7 +513,6 @@ int rheo_verify(rheo_tree* t, const void* logits, float T, uint64_t key, int32_t
     a.final_token = final_token;
     a.G = t->vG;
     for (int i = 0; i < 16; ++i) a.draft[i] = t->draft[i];
-    a.epoch = 64 * ++t->verify_calls;
     // about a second of polling; RHEO_VERIFY_SPIN (read at each call) lowers
     // it, so that tests can force the failure path from the host
     a.spin = 1L << 20;

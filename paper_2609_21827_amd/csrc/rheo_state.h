@@ -40,6 +40,7 @@ struct TreeDev {
     int32_t* porder;               // [B][NN]: uid of each pruned index
     int32_t* err;                  // sticky device error flag
     // verification team exchange (see verify.hip)
+    uint64_t* team_ticket;         // [B] blocks of each team so far (monotonic)
     uint64_t* team_flag;           // [B][GMAX] arrival epochs
     uint64_t* team_max;            // [B][GMAX] segment maxima: epoch << 32 | order code
     uint64_t* team_sum;            // [B][GMAX] segment weight sums: epoch << 48 | sum
@@ -85,7 +86,6 @@ struct VerifyArgs {
     int NV;                        // chunks per segment
     float kT;
     uint64_t rng_key;
-    uint64_t epoch;                // first barrier epoch of this call (host counter)
     long spin;                     // polls of a team wait before it gives up
     int32_t* accepted;
     int32_t* accept_len;

@@ -28,9 +28,15 @@
 //      above, and the fills under the residual with Z_l for S_p.
 // Team exchanges use agent-scope atomic stores and loads only (they are
 // coherent across the XCDs without cache write-back or invalidation), with
-// arrival epochs in per-block flags and bounded waits.  The epochs of a call
-// come from the host (a per-handle call counter), so no block depends on
-// another block's progress to learn them.  A wait past its spin limit ends
+// arrival epochs in per-block flags and bounded waits.  The epochs of a
+// launch come from a per-team ticket counter in device memory: each block
+// of the team takes one ticket as it starts, so the G blocks of the n-th
+// launch for that team hold tickets nG .. nG + G - 1 and all compute n,
+// whatever order they start in, and the next launch on the stream (which
+// starts only after every block of this one has ended) computes n + 1.
+// Replays of a captured graph therefore never see their own earlier
+// words as current, and no block depends on another block's progress to
+// learn the epoch.  A wait past its spin limit ends
 // the walk: the team's first block then writes the failure result
 // (accept_len = final_token = -1, accepted all -1) and device error bit 128
 // is set.  A visited node whose target row has no finite logit (p
@@ -329,9 +335,11 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
     const int NC = (V + CH - 1) / CH;
     const int64_t nb = (int64_t)b * NN;
     uint64_t* flags = t.team_flag + (int64_t)b * GMAX;
-    // barrier epochs of this call: a base from the host, 64 above the
-    // previous call's, so words left from earlier calls never match
-    const uint64_t epoch = a.epoch;
+    // this block's ticket: the launch number for the team, ticket / G
+    uint64_t ticket = 0;
+    if (tid == 0)
+        ticket = __hip_atomic_fetch_add(&t.team_ticket[b], 1ull, __ATOMIC_RELAXED,
+                                        __HIP_MEMORY_SCOPE_AGENT);
     uint64_t* tmax_x = t.team_max + (int64_t)b * GMAX;
     uint64_t* chunk_x = t.team_chunk + (int64_t)b * NCMAX;
     uint32_t* sp_x = t.team_sp + (int64_t)b * SPMAX;
@@ -347,13 +355,18 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
     const int lo_tok = c0 * CH, hi_tok = min(V, c1 * CH);
 
     // the root: pruned index 0; its first child and expanded index
+    __shared__ uint64_t s_epoch;
     if (tid == 0) {
         s_cur = 0;
         s_curp = 0;
         s_fc = t.first_child[nb];
         s_e = t.exp_of[nb];
+        // barrier epochs of this launch: a window of 64 above the previous
+        // launch's (a walk uses 3 per layer, at most 48)
+        s_epoch = 64 * (ticket / (uint64_t)G + 1);
     }
     __syncthreads();
+    const uint64_t epoch = s_epoch;
     int level = 0, nacc = 0;
     bool failed = false;                      // a team wait timed out, or no finite target logit
     for (;;) {

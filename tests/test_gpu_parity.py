@@ -357,11 +357,15 @@ def test_frontier_view_matches_copy(dev):
     tree.close()
 
 
-def test_graph_replay_matches_eager(dev):
-    """A captured step replays bit-exactly, several times, with eager steps
-    and synchronisations between the replays."""
+@pytest.mark.parametrize("support", [128, 0])
+@pytest.mark.parametrize("between", [True, False])
+def test_graph_replay_matches_eager(dev, support, between):
+    """A captured step replays bit-exactly, several times: with eager steps
+    and synchronisations between the replays, and back to back (the
+    verification teams' barrier words then hold the previous replay's
+    values; the dense walk's team barriers once took those for current)."""
     from paper_2609_21827_amd.driver import make_tree, run_step
-    w = W["llama3"].with_(B=3, depth=4, R=20)
+    w = W["llama3"].with_(B=3, depth=4, R=20, support=support)
     tree = make_tree(w, device=dev)
     rec = {}
     acc, alen, fin = run_step(tree, w, 0, device=dev, record=rec)
@@ -390,8 +394,9 @@ def test_graph_replay_matches_eager(dev):
         torch.cuda.synchronize()
         for a, b in zip(out, ref):
             assert torch.equal(a.cpu(), b), f"replay {r}"
-        run_step(tree, w, 1 + r, device=dev)          # eager work in between
-        torch.cuda.synchronize()
+        if between:
+            run_step(tree, w, 1 + r, device=dev)      # eager work in between
+            torch.cuda.synchronize()
     assert tree.device_error() == 0
     tree.close()
 
