@@ -131,28 +131,63 @@ __global__ __launch_bounds__(NTD) void k_dweights(TreeDev t, LevelArgs a) {
     const uint64_t kb = s_kb;
     const int idmax = s_idmax;
 
+    // Per element: w1 relative to the row maximum (never above it, so no
+    // upper clamp), q relative to the guess of x_{m+1}; weights are summed
+    // in pairs in 32 bits (each <= 2^30) before the 64-bit totals.  Each
+    // vector's q total goes to LDS, and the totals of the sub-chunks (64
+    // consecutive vectors: one wave's at one step) are formed there.  A
+    // weight equal to the kk-th one is only marked per element; the exact
+    // test of the rank tie runs for the marked elements alone (rare).
     uint64_t s1 = 0, zq = 0;
     bool flag = false;
+    constexpr int NG = NVC < 16 ? NVC : 16;          // vectors per LDS round
+    __shared__ uint64_t s_vq[NG][NTD];
+    for (int g0 = 0; g0 < NVC; g0 += NG) {
 #pragma unroll
-    for (int i = 0; i < NVC; ++i) {
-        const int e0 = (v0 + i * NTD + tid) * VEC;
-        uint64_t sq = 0;
+        for (int ii = 0; ii < NG; ++ii) {
+            const int i = g0 + ii;
+            const int e0 = (v0 + i * NTD + tid) * VEC;
+            // (elements past V read as -inf: weight 0 on both counts, and
+            // no tie, since idmax < V)
+            uint64_t sq = 0;
+            uint32_t hit = 0;
 #pragma unroll
-        for (int k = 0; k < VEC; ++k) {
-            const int id = e0 + k;
-            if (id < V) {
-                const float l = delem<DT>(r[i], k);
-                const uint32_t w1 = cweight(l, M, a.k1);
-                s1 += w1;
-                sq += cweight(l, ref, a.kT);
-                if (w1 == wmin && id < idmax && logit_key(l, (uint32_t)id) < kb) flag = true;
+            for (int k = 0; k < VEC; k += 2) {
+                const float la = delem<DT>(r[i], k), lb = delem<DT>(r[i], k + 1);
+                const uint32_t wa = cweight_below(la, M, a.k1);
+                const uint32_t wb = cweight_below(lb, M, a.k1);
+                s1 += (uint64_t)(wa + wb);
+                sq += (uint64_t)(cweight(la, ref, a.kT) + cweight(lb, ref, a.kT));
+                hit |= (uint32_t)(wa == wmin) << k;
+                hit |= (uint32_t)(wb == wmin) << (k + 1);
             }
+            if (hit) {
+#pragma unroll
+                for (int k = 0; k < VEC; ++k) {
+                    const int id = e0 + k;
+                    if (((hit >> k) & 1u) && id < idmax &&
+                        logit_key(delem<DT>(r[i], k), (uint32_t)id) < kb)
+                        flag = true;
+                }
+            }
+            zq += sq;
+            s_vq[ii][tid] = sq;
         }
-        zq += sq;
-        // total of q over this wave's 64 consecutive vectors (one sub-chunk)
-        const uint64_t wsum = wave_sum_u64(sq);
-        const int sub = (v0 + i * NTD) / WAVE + wid;
-        if (lane == 0 && sub < t.NCH) t.dq[(int64_t)row * t.NCH + sub] = wsum;
+        __syncthreads();
+        // sub-chunk (ii, wave w): lanes 64 w .. 64 w + 63 of row ii, summed
+        // by 4 threads of 16 entries each
+        for (int q = tid; q < NG * (NTD / WAVE) * 4; q += NTD) {
+            const int part = q & 3, sc = q >> 2;
+            const int ii = sc / (NTD / WAVE), w = sc % (NTD / WAVE);
+            uint64_t x = 0;
+#pragma unroll
+            for (int l = 0; l < 16; ++l) x += s_vq[ii][w * WAVE + part * 16 + l];
+            x += __shfl_xor(x, 1);
+            x += __shfl_xor(x, 2);
+            const int sub = (v0 + (g0 + ii) * NTD) / WAVE + w;
+            if (part == 0 && sub < t.NCH) t.dq[(int64_t)row * t.NCH + sub] = x;
+        }
+        __syncthreads();
     }
     s1 = block_sum_u64<NTD>(s1, s_red);
     zq = block_sum_u64<NTD>(zq, s_red);

@@ -49,9 +49,7 @@ __device__ inline uint64_t philox_draw(uint64_t key, uint64_t purpose,
 // taken as the truncating conversion of the exact product 2^30 P * 2^n
 // (a scaling by a power of two, exact; below t = -31 it is < 1, so 0).
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ uint32_t cweight(float l, float ref, float kT) {
-    float t = __fmul_rn(__fsub_rn(l, ref), kT);
-    t = fmaxf(fminf(t, 0.0f), -64.0f);
+__device__ __forceinline__ uint32_t cweight_of_t(float t) {
     const float n = rintf(t);
     const float f = __fsub_rn(t, n);
     float p = 0x1.430912p+17f;
@@ -62,6 +60,15 @@ __device__ __forceinline__ uint32_t cweight(float l, float ref, float kT) {
     p = __fadd_rn(__fmul_rn(p, f), 0x1.62e430p+29f);
     p = __fadd_rn(__fmul_rn(p, f), 0x1.000000p+30f);
     return (uint32_t)__builtin_amdgcn_ldexpf(p, (int)n);
+}
+__device__ __forceinline__ uint32_t cweight(float l, float ref, float kT) {
+    const float t = __fmul_rn(__fsub_rn(l, ref), kT);
+    return cweight_of_t(fmaxf(fminf(t, 0.0f), -64.0f));
+}
+// The same weight for l <= ref (then t <= 0 and the upper clamp is void).
+__device__ __forceinline__ uint32_t cweight_below(float l, float ref, float kT) {
+    const float t = __fmul_rn(__fsub_rn(l, ref), kT);
+    return cweight_of_t(fmaxf(t, -64.0f));
 }
 
 // Order-preserving map of an fp32 value to uint32 (-0 folded onto +0).
