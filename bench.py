@@ -287,6 +287,7 @@ def main():
     #      the launch sequence of a step is captured once and replayed; every
     #      replay must still reproduce the discovery outputs -------------------
     graph_ms = None
+    graph_error = None
     if args.graph:
         try:
             cap = torch.cuda.Stream()
@@ -315,6 +316,7 @@ def main():
             if graph_ms < eager_ms:
                 ms, steps_per_s, mode = graph_ms, args.steps / (g1 - g0), "hip-graph"
         except (RuntimeError, AssertionError) as e:
+            graph_error = str(e)
             log(f"graph replay unavailable ({e}); reporting the eager launch loop")
 
     # algorithmic bytes: every draft row once, the target rows on each walk
@@ -369,6 +371,7 @@ def main():
         "mode": mode,
         "eager_ms_per_step": round(eager_ms, 4),
         "graph_ms_per_step": None if graph_ms is None else round(graph_ms, 4),
+        "graph_error": graph_error,
         "event_pass_ms_per_step": round(event_pass_ms, 4),
         "roofline": {"bound": "hbm", "kernel": expand_kernel_name(w),
                      "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS,
