@@ -74,34 +74,35 @@ class Bern:
 
 class ExplicitDist:
     """Integer (or rational) weights on a list of token ids.  Sampling is by
-    inverse CDF over the ids in ascending order."""
+    inverse CDF over the ids in ascending order, or, with ``ranked``, over
+    the ids in the order given (a sparse node's tail in rank order)."""
 
-    def __init__(self, ids, weights):
+    def __init__(self, ids, weights, ranked=False):
         ids_np = np.asarray(ids, dtype=np.int64)
-        order = np.argsort(ids_np, kind="stable")
+        order = (np.arange(len(ids_np)) if ranked
+                 else np.argsort(ids_np, kind="stable"))
         self.ids = ids_np[order].tolist()
         if isinstance(weights, np.ndarray) and weights.dtype.kind in "iu":
             self.weights = weights[order].tolist()         # exact Python ints
         else:
             self.weights = [weights[i] for i in order]
         self._total = sum(self.weights)
-        self._sorted_ids = np.asarray(self.ids, dtype=np.int64)
+        self._index = {v: i for i, v in enumerate(self.ids)}
         self._cum = None
 
     def total(self):
         return self._total
 
     def weight(self, v):
-        i = int(np.searchsorted(self._sorted_ids, v))
-        if i < len(self.ids) and self.ids[i] == v:
-            return self.weights[i]
-        return 0
+        i = self._index.get(int(v))
+        return 0 if i is None else self.weights[i]
 
     def outcomes(self):
         return [(i, w) for i, w in zip(self.ids, self.weights) if w > 0]
 
     def pick(self, t):
-        """Smallest id whose inclusive prefix weight exceeds ``t``."""
+        """First id, in this distribution's order, whose inclusive prefix
+        weight exceeds ``t``."""
         if self._cum is None:
             self._cum = list(itertools.accumulate(self.weights))
         k = bisect.bisect_right(self._cum, t)
@@ -228,7 +229,9 @@ def node_dist_from_logits(logits, m, T, support_size=0, construct_tempered=False
     The construction distribution q is untempered unless
     ``construct_tempered`` (Sec. 5.4).  The tail q~ = q_T / z on the support
     minus x_1..x_m (App. C.1) is evaluated relative to the logit of x_{m+1},
-    so its largest weight is 2**30 and its total never vanishes.
+    so its largest weight is 2**30 and its total never vanishes.  Y ~ q~ is
+    drawn by inverse CDF over the tail in rank order (x_{m+1}, x_{m+2}, ...)
+    when S > 0, and over token ids when the support is the vocabulary.
 
     ``construct_full``: the other reading of the sparse mode, where the
     truncation touches only the sampled token (Sec. 5.5, discussion of
@@ -238,6 +241,9 @@ def node_dist_from_logits(logits, m, T, support_size=0, construct_tempered=False
     l = np.asarray(logits, dtype=np.float32)
     V = l.shape[0]
     ids = np.arange(V, dtype=np.int64)
+    # a sparse node samples Y over its tail in rank order, a dense one over
+    # token ids (reading of the inverse CDF's order)
+    ranked = bool(support_size and support_size > 0)
     order = np.lexsort((ids, -l.astype(np.float64)))
     if support_size and support_size < V:
         order = order[:support_size]
@@ -256,7 +262,7 @@ def node_dist_from_logits(logits, m, T, support_size=0, construct_tempered=False
         tail_np = sup_r[m:]
         _check_tail_reference(l[tail_np[0]])
         q = numerics.canonical_weights(l[tail_np], l[tail_np[0]], T)
-        return NodeDist(support, w1, s1, ExplicitDist(tail_np, q))
+        return NodeDist(support, w1, s1, ExplicitDist(tail_np, q, ranked=ranked))
     else:
         w = numerics.fp64_weights(l[sup], ref, Tc)
         r = rank_order(list(sup), w)
@@ -275,7 +281,7 @@ def node_dist_from_logits(logits, m, T, support_size=0, construct_tempered=False
         q = numerics.canonical_weights(l[tail_ids], ref_t, T).tolist()
     else:
         q = numerics.fp64_weights(l[tail_ids], ref_t, T)
-    return NodeDist(support, w1, s1, ExplicitDist(tail_ids, q))
+    return NodeDist(support, w1, s1, ExplicitDist(tail_ids, q, ranked=ranked))
 
 
 def node_dist_from_weights(ids, w1, q_tail=None, m=1):

@@ -244,6 +244,7 @@ void layout(rheo_tree* t, Arena& A) {
     take(A, &d.path, B * NN);
     take(A, &d.first_child, B * NN);
     take(A, &d.exp_of, B * NN);
+    take(A, &d.tidx, B * NN);
     const size_t TS = dense ? 1 : (size_t)d.S;              // dense mode keeps no tail copy
     take(A, &d.tail_id, B * E * TS);
     take(A, &d.tail_q, B * E * TS);

@@ -454,7 +454,7 @@ __global__ __launch_bounds__(NTD) void k_dpool(TreeDev t, LevelArgs a) {
         }
         const double qtrue = (kind == SAMPLED) ? __ddiv_rn((double)qy, (double)Zq) : proxy;
         emit_child(t, level, nb, pu, parent_rec(t, level, nb, pu), cb + j * K + s, s, kind, tok,
-                   proxy, qtrue);
+                   proxy, qtrue, -1);
     }
     // the next frontier: the last row of the sequence to finish selects it
     select_frontier(t, a, b, s_sub, s_sub + 256);

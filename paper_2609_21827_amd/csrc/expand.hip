@@ -39,7 +39,7 @@ constexpr int SMAX = 1024;    // largest support
 constexpr int MERGE_MAX = 2048;  // chunk-list keys one row merges (C * Sc)
 constexpr int NTE = 512;      // threads per k_expand_row block
 constexpr int EBATCH = 8;     // 16-byte vectors per thread and batch of k_expand_row
-constexpr int kCountTailMax = 256;  // largest support whose tail is ordered by counting
+constexpr int kLargeSupport = 256;  // supports above it: the large class of k_expand_row
 
 template <int DT>
 __device__ __forceinline__ float elem(const uint4& v, int k) {
@@ -119,10 +119,9 @@ __host__ __device__ inline PoolLds pool_lds(int S, int C, int top_min = 0, int k
 // The pool of one row from its support s_top (App. C.1), formed by NT
 // threads (tid < NT).  Children fields the frontier selection reads in other
 // blocks (token, score, path) are published with agent-scope atomics.
-// SORT_TAIL: order the tail by sorting (supports above kCountTailMax)
-// rather than by counting; both give the same order.  A support slot left
-// empty (no candidate reached it) is flagged and filled with a -inf key.
-template <int NT, bool SORT_TAIL>
+// A support slot left empty (no candidate reached it) is flagged and filled
+// with a -inf key.
+template <int NT>
 __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, int row,
                                           uint8_t* lds, const PoolLds& L, int pu,
                                           const ParentRec& pr, uint64_t u, uint64_t* s_red,
@@ -146,21 +145,20 @@ __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, 
 
     // Construction weights w1 (untempered unless asked) and, taking the rank
     // by (w1 desc, id asc) to be the support order, the tail weights of q~_T
-    // relative to x_{m+1} = s_top[m], both totals in one exchange, and the
-    // tail's id keys (larger key = smaller id; 0 off the tail).  The support
-    // is in (logit desc, id asc) order and the weight never grows along it,
-    // so the rank differs from the position only where two different logits
-    // share a weight: then the ranks and the tail are computed again.
+    // relative to x_{m+1} = s_top[m], both totals in one exchange.  The
+    // support is in (logit desc, id asc) order and the weight never grows
+    // along it, so the rank differs from the position only where two
+    // different logits share a weight: then the ranks and the tail are
+    // computed again.
+    //
+    // The tail, x_{m+1} .. x_S in rank order, is written to the tree in that
+    // order (token, q~ weight) for verification, and Y ~ q~_T is the entry
+    // whose interval [mass before, mass before + q) holds
+    // t = floor(U64 Zq / 2^64): the inverse CDF over the tail in rank order.
+    // With at most one support entry per thread (S <= NT) the masses before
+    // every entry come with the totals, from the same exchange.
     auto filled = [&](uint64_t k) {
         return (uint32_t)key_id(k) >= (uint32_t)t.V ? logit_key(-INFINITY, 0u) : k;
-    };
-    // the tail entry of a support key: counting (small supports) ranks
-    // id << 32 | q (~0 off the tail); sorting ranks the complemented id (0
-    // off the tail)
-    auto tail_code = [&](bool tail, uint64_t tk, uint32_t q) -> uint64_t {
-        if constexpr (SORT_TAIL)
-            return tail ? (uint64_t)(0xFFFFFFFFu - (uint32_t)key_id(tk)) + 1 : 0ull;
-        return tail ? (((uint64_t)(uint32_t)key_id(tk) << 32) | q) : ~0ull;
     };
     const float M = key_value(filled(s_top[0]));
     const float ref0 = key_value(filled(s_top[m]));
@@ -176,27 +174,34 @@ __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, 
         const uint32_t w = cweight(v, M, a.k1);
         s_w1[i] = w;
         part1 += w;
-        const bool tail = i >= m;
-        const uint32_t q = tail ? cweight(v, ref0, a.kT) : 0u;
+        const uint32_t q = (i >= m) ? cweight(v, ref0, a.kT) : 0u;
         s_q[i] = q;
         partq += q;
-        s_k2[i] = tail_code(tail, tk, q);
     }
-    uint64_t S1, Zq;
-    psum2<NT>(part1, partq, s_red, &S1, &Zq);
+    const bool one_each = S <= NT;           // thread tid holds support entry tid
+    uint64_t S1, Zq, qbefore = 0;
+    if (one_each) psum2_scan<NT>(part1, partq, s_red, &S1, &Zq, &qbefore);
+    else psum2<NT>(part1, partq, s_red, &S1, &Zq);
     if (t.cfull) S1 = t.s1row[row];          // construction over the whole vocabulary
     if (NT == WAVE) wave_sync();             // (a block sum has synchronised)
+    const int64_t tail_base = ((int64_t)b * t.E + e_idx) * S;
     bool tie = false;
     for (int i = tid + 1; i < S; i += NT)
         tie |= s_w1[i] == s_w1[i - 1] && (s_top[i] >> 32) != (s_top[i - 1] >> 32);
-    // Counting (small supports) goes ahead with the rank by weight taken to
-    // be the support order and learns at the barrier that ends the tail
-    // whether two different logits share a weight; only then (rarely) are
-    // the ranks, the tail weights and the tail computed again.  Sorting
-    // (large supports) checks first.
-    bool ident = true;
-    if constexpr (SORT_TAIL) ident = !pany<NT>(tie);
-    auto reorder = [&]() {
+    // the tail and Y with the rank taken to be the position (one entry per
+    // thread); the barrier of pany ends it, and tells whether two different
+    // logits share a weight, which (rarely) sends everything through the
+    // ranks below
+    if (one_each && tid >= m && tid < S) {
+        const uint32_t q = s_q[tid];
+        t.tail_id[tail_base + tid - m] = key_id(s_top[tid]);
+        t.tail_q[tail_base + tid - m] = q;
+        const uint64_t tt = __umul64hi(u, Zq);
+        if (qbefore <= tt && tt - qbefore < (uint64_t)q) *s_yi = tid;
+    }
+    const bool ident = !pany<NT>(tie);
+    if (NT == WAVE) wave_sync();
+    if (!ident) {
         for (int i = tid; i < S; i += NT)
             s_k2[i] = ((uint64_t)s_w1[i] << 32) |
                       (uint64_t)(0xFFFFFFFFu - (uint32_t)key_id(s_top[i]));
@@ -208,79 +213,34 @@ __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, 
         const float ref_t = key_value(s_top[s_xs[m]]);
         partq = 0;
         for (int i = tid; i < S; i += NT) {
-            const bool tail = s_wr[i] >= m;
-            const uint64_t tk = s_top[i];
-            const uint32_t q = tail ? cweight(key_value(tk), ref_t, a.kT) : 0u;
+            const uint32_t q = (s_wr[i] >= m) ? cweight(key_value(s_top[i]), ref_t, a.kT) : 0u;
             s_q[i] = q;
             partq += q;
-            s_k2[i] = tail_code(tail, tk, q);
         }
         Zq = psum<NT>(partq, s_red);
-    };
-    if (!ident) reorder();
+    }
     // position in the support of rank r, and rank of position i
     auto xs = [&](int r) -> int { return ident ? r : (int)s_xs[r]; };
     auto wr = [&](int i) -> int { return ident ? i : (int)s_wr[i]; };
-
-    // The tail in token-id order: every tail entry's place among the tail
-    // ids and the q~ mass of the entries before it.  The tail is written to
-    // the tree in that order (q~ for verification), and Y ~ q~_T is the
-    // entry whose interval [mass before, mass before + q) holds
-    // t = floor(U64 Zq / 2^64): the inverse CDF over token ids.  Small
-    // supports count, for every entry, the smaller ids and their mass;
-    // large ones sort the tail by id and take a prefix sum.
-    const int64_t tail_base = ((int64_t)b * t.E + e_idx) * S;
-    if constexpr (!SORT_TAIL) {
-        auto tail_count = [&]() {
-            const uint64_t tt = __umul64hi(u, Zq);
-            id_prefix<NT>(s_k2, S, [&](int i, int ir, uint64_t pre) {
-                const uint32_t q = (uint32_t)s_k2[i];
-                t.tail_id[tail_base + ir] = key_id(s_top[i]);
-                t.tail_q[tail_base + ir] = q;
-                if (pre <= tt && tt - pre < (uint64_t)q) *s_yi = i;
-            });
-        };
-        tail_count();
-        const bool anytie = pany<NT>(tie);      // also the barrier after the tail
-        if (NT == WAVE) wave_sync();
-        if (anytie) {
-            ident = false;
-            if (tid == 0) *s_yi = -1;
-            reorder();                           // (synchronises before the new tail)
-            tail_count();
-            psync<NT>();
-        }
-    } else {
+    if (!(ident && one_each)) {
+        // contiguous runs of ranks m .. S-1 per thread, a block scan of
+        // their masses
+        if (tid == 0) *s_yi = -1;
         const uint64_t tt = __umul64hi(u, Zq);
-        // sort keys: the complement of (id, position) for the tail, so that
-        // the descending sort puts ids in ascending order; 0 (last) for the
-        // leads and the padding
-        const int n2 = pow2_at_least(S);
-        psync<NT>();
-        for (int i = tid; i < n2; i += NT) {
-            const bool tail = i < S && s_k2[i] != 0ull;
-            s_k2[i] = tail ? ~(((uint64_t)(uint32_t)key_id(s_top[i]) << 32) | (uint32_t)i) : 0ull;
-        }
-        psync<NT>();
-        bitonic_sort_desc<NT>(s_k2, n2);
         const int ntail = S - m;
-        const int per = n2 > NT ? n2 / NT : 1;       // sorted entries per thread
-        const int r0 = tid * per;
+        const int per = (ntail + NT - 1) / NT;
+        const int r0 = min(S, m + tid * per), r1 = min(S, r0 + per);
         uint64_t mine = 0;
-        for (int r = r0; r < r0 + per; ++r)
-            if (r < ntail) mine += s_q[(uint32_t)~s_k2[r]];
+        for (int r = r0; r < r1; ++r) mine += s_q[xs(r)];
         uint64_t tot;
         uint64_t pre = pscan_excl<NT>(mine, s_red, &tot);
-        for (int r = r0; r < r0 + per; ++r) {
-            if (r < ntail) {
-                const uint64_t kk = ~s_k2[r];
-                const int i = (int)(uint32_t)kk;
-                const uint32_t q = s_q[i];
-                t.tail_id[tail_base + r] = (int)(kk >> 32);
-                t.tail_q[tail_base + r] = q;
-                if (pre <= tt && tt - pre < (uint64_t)q) *s_yi = i;
-                pre += q;
-            }
+        for (int r = r0; r < r1; ++r) {
+            const int i = xs(r);
+            const uint32_t q = s_q[i];
+            t.tail_id[tail_base + r - m] = key_id(s_top[i]);
+            t.tail_q[tail_base + r - m] = q;
+            if (pre <= tt && tt - pre < (uint64_t)q) *s_yi = i;
+            pre += q;
         }
         psync<NT>();
     }
@@ -337,7 +297,8 @@ __device__ __forceinline__ void pool_form(const TreeDev& t, const LevelArgs& a, 
         }
         const double qtrue = (kind == SAMPLED) ? __ddiv_rn((double)s_q[item], (double)Zq) : proxy;
         emit_child(t, level, nb, pu, pr, cb + j * K + s, s, kind, key_id(s_top[item]), proxy,
-                   qtrue);
+                   qtrue,
+                   wr(item) >= m ? wr(item) - m : -1);
     }
 }
 
@@ -381,7 +342,6 @@ __device__ __forceinline__ void row_parent(const TreeDev& t, const LevelArgs& a,
 // k_pool: one block per row: parent, support (merge of the chunk lists),
 // pool, and, by the last row of each sequence, the next frontier
 // ---------------------------------------------------------------------------
-template <bool SORT_TAIL>
 __global__ __launch_bounds__(NTP) void k_pool(TreeDev t, LevelArgs a) {
     extern __shared__ __align__(16) uint8_t s_pdyn[];
     __shared__ uint64_t s_red[2 * NTP / WAVE];
@@ -463,7 +423,7 @@ __global__ __launch_bounds__(NTP) void k_pool(TreeDev t, LevelArgs a) {
     __syncthreads();
 
     // the pool, formed by the whole block
-    pool_form<NTP, SORT_TAIL>(t, a, row, s_pdyn, L, s_pu, pr, s_u, s_red, &s_yi);
+    pool_form<NTP>(t, a, row, s_pdyn, L, s_pu, pr, s_u, s_red, &s_yi);
     if (level + 1 >= t.D) return;
 
     // the next frontier: the last row of the sequence to finish selects it
@@ -1058,7 +1018,7 @@ __device__ __forceinline__ void select_block(const TreeDev& t, const LevelArgs& 
 // once (double-buffered batches of 16-byte vectors; only each vector's
 // exact maximum is kept, as a 16-bit order code in registers); the
 // threshold comes from the largest vector maxima every thread offers (two,
-// or four for supports above 128), and for supports above kCountTailMax
+// or four for supports above 128), and for supports above kLargeSupport
 // (LS) is raised to the exact S-th largest vector maximum by two rounds of
 // a 256-bin histogram; only the candidate vectors are read again; their
 // elements at or above the threshold are ranked (LS: sorted) into the
@@ -1388,7 +1348,7 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
     }
     __syncthreads();
 
-    pool_form<NTE, LS>(t, a, row, s_pdyn, L, s_pu, pr, s_u, s_red, &s_yi);
+    pool_form<NTE>(t, a, row, s_pdyn, L, s_pu, pr, s_u, s_red, &s_yi);
     if (level + 1 >= t.D) return;
     select_frontier(t, a, b, s_top, s_k2);
 }
@@ -1443,8 +1403,7 @@ hipError_t launch_expand(const TreeDev& t, const LevelArgs& a, int variant, hipS
     hipError_t e = launch_select(t, a, variant, s);
     if (e != hipSuccess) return e;
     const size_t shm = (size_t)pool_lds(t.S, t.C).bytes;
-    if (t.S > kCountTailMax) k_pool<true><<<t.B * a.P, NTP, shm, s>>>(t, a);
-    else k_pool<false><<<t.B * a.P, NTP, shm, s>>>(t, a);
+    k_pool<<<t.B * a.P, NTP, shm, s>>>(t, a);
     return hipGetLastError();
 }
 
@@ -1515,7 +1474,7 @@ static hipError_t launch_row(const TreeDev& t, const LevelArgs& a, int nq, hipSt
 
 template <int DT>
 static hipError_t launch_row_dt(const TreeDev& t, const LevelArgs& a, int nq, hipStream_t s) {
-    if (t.S > kCountTailMax) return launch_row<DT, 2>(t, a, nq, s);
+    if (t.S > kLargeSupport) return launch_row<DT, 2>(t, a, nq, s);
     if (t.S > NTE / 4) return launch_row<DT, 1>(t, a, nq, s);
     return launch_row<DT, 0>(t, a, nq, s);
 }

@@ -207,6 +207,38 @@ __device__ __forceinline__ void psum2(uint64_t a, uint64_t b, uint64_t* sh, uint
         block_sum2_u64<NT>(a, b, sh, ra, rb);
     }
 }
+// Totals of a and b over the pool's NT threads and the exclusive prefix of
+// b in thread order, in one exchange (sh: 2 * NT / WAVE words for a block).
+template <int NT>
+__device__ __forceinline__ void psum2_scan(uint64_t a, uint64_t b, uint64_t* sh, uint64_t* ra,
+                                           uint64_t* rb, uint64_t* b_before) {
+    const uint64_t binc = wave_incl_scan_u64(b);
+    const uint64_t asum = wave_sum_u64(a);
+    if (NT == WAVE) {
+        *ra = asum;
+        *rb = lane_u64(binc, WAVE - 1);
+        *b_before = binc - b;
+        return;
+    }
+    constexpr int NW = NT / WAVE;
+    const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE;
+    __syncthreads();
+    if (l == WAVE - 1) {
+        sh[w] = asum;
+        sh[NW + w] = binc;
+    }
+    __syncthreads();
+    uint64_t x = 0, y = 0, before = 0;
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+        x += sh[i];
+        y += sh[NW + i];
+        before += (i < w) ? sh[NW + i] : 0ull;
+    }
+    *ra = x;
+    *rb = y;
+    *b_before = before + binc - b;
+}
 // Exclusive prefix sum of one 64-bit value per thread over the pool's NT
 // threads (sh: NT / WAVE words for a block); *total receives the sum.
 template <int NT>
@@ -242,13 +274,15 @@ __device__ __forceinline__ ParentRec parent_rec(const TreeDev& t, int level, int
 // One child record of expanded row j (slot s, 0-based; App. C.1): the
 // fields the frontier selection reads in other blocks (token, score, path)
 // are published with agent-scope atomics.
+// tail: the child's place in its parent's stored tail (-1: not in it)
 __device__ __forceinline__ void emit_child(const TreeDev& t, int level, int64_t nb, int pu,
                                            const ParentRec& pr, int uid, int s, int kind,
-                                           int tok, double proxy, double qtrue) {
+                                           int tok, double proxy, double qtrue, int tail) {
     const double pscore = pr.score;
     const uint64_t ppath = pr.path;
     const int64_t o = nb + uid;
     t.par[o] = pu;
+    t.tidx[o] = tail;
     t.meta[o] = (level + 1) | ((s + 1) << 8) | (kind << 16);
     t.proxy[o] = proxy;
     t.qtrue[o] = qtrue;

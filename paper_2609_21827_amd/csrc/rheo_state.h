@@ -26,6 +26,7 @@ struct TreeDev {
     uint64_t* path;                // slot path, 4 bits per level from bit 59 down
     int32_t* first_child;          // uid of slot-1 child, -1 if not expanded
     int32_t* exp_of;               // expanded index, -1 if not expanded
+    int32_t* tidx;                 // place in the parent's stored tail (sparse), else -1
     // truncated tail distribution q~ of each expanded node, sorted by id
     int32_t* tail_id;              // [B][E][S]
     uint32_t* tail_q;              // [B][E][S]

@@ -90,17 +90,6 @@ __device__ __forceinline__ uint4 load_vec(const char* row, int vi, int V) {
     return make_uint4(w[0], w[1], w[2], w[3]);
 }
 
-// Position of v in the id-sorted list, -1 if absent; lower bound in *lb.
-__device__ inline int find_sorted(const int32_t* ids, int n, int v, int* lb = nullptr) {
-    int lo = 0, hi = n;
-    while (lo < hi) {
-        const int mid = (lo + hi) >> 1;
-        if (ids[mid] < v) lo = mid + 1; else hi = mid;
-    }
-    if (lb) *lb = lo;
-    return (lo < n && ids[lo] == v) ? lo : -1;
-}
-
 // 128-bit wave / block sums and scans (values < 2^127), on DPP row moves
 // with explicit carries between the 64-bit halves.
 __device__ __forceinline__ void add_u128(uint64_t& lo, uint64_t& hi, uint64_t blo, uint64_t bhi) {
@@ -297,7 +286,7 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
     const int SEGCH = a.NV;                  // chunks per segment
 
     __shared__ uint64_t s_chunk[NCMAX];
-    __shared__ int32_t s_tid[SPMAX];         // stored tail ids (sorted)
+    __shared__ __align__(16) int32_t s_tid[SPMAX];   // stored tail ids (rank order)
     __shared__ uint32_t s_tq[SPMAX];         // stored tail weights Q
     __shared__ uint32_t s_tp[SPMAX];         // p's weights at tail tokens, then candidates
     __shared__ u128 s_cn[CH];
@@ -388,7 +377,7 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
             sp_q = t.tail_q[tb + tid];
         }
         bool keep = false;
-        int kind = -1, ctok = -1, cpidx = -1, cfc = -1, ce = -1;
+        int kind = -1, ctok = -1, cpidx = -1, cfc = -1, ce = -1, ctail = -1;
         if (tid < WAVE && fc >= 0 && lane < K) {
             const int64_t o = nb + fc + lane;
             cpidx = t.pidx[o];
@@ -396,6 +385,7 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
             ctok = t.tok[o];
             cfc = t.first_child[o];
             ce = t.exp_of[o];
+            ctail = DN ? -1 : t.tidx[o];        // its place in the stored tail
             keep = cpidx > 0;
         }
         const uint64_t Zq = (fc >= 0) ? t.zq[(int64_t)b * t.E + e] : 1;
@@ -455,6 +445,7 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
                 s_c_pidx[cpos] = cpidx;
                 s_c_fc[cpos] = cfc;
                 s_c_e[cpos] = ce;
+                s_c_tail[cpos] = ctail;
             }
             if (lane == 0) {
                 s_nc = __popcll(msk);
@@ -616,8 +607,7 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
             }
             Sp = DN ? wave_sum_u64(part) : s_Sp;
             wave_sync();
-            if (lane < nc) s_c_tail[lane] = DN ? -1 : find_sorted(s_tid, nt, s_c_tok[lane]);
-            wave_sync();
+
             // RRSw (App. D.2): the leads -- the candidates before the sampled
             // child -- are tested first, under p; the sampled child is then
             // tested under what remains, of mass Z_l.  Algorithm 1 tests the
@@ -783,12 +773,28 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
             // F * P_v - N_v summed over the special tokens of chunk cidx
             u128 d = 0;
             if (residual) {
-                int lb;
-                find_sorted(s_tid, nt, cidx * CH, &lb);
-                for (int i = lb; i < nt && s_tid[i] < (cidx + 1) * CH; ++i) {
+                // the stored tail is in rank order: every entry is checked,
+                // four ids per LDS load, the (rare) hits handled one by one
+                auto live = [&](int i) {
                     const u128 pz = (u128)s_tp[i] * Zq, qs = (u128)s_tq[i] * Zl;
                     d += pz < qs ? pz : qs;       // F P - N for a live tail token
+                };
+                const int4* t4 = (const int4*)s_tid;
+                const int n4 = nt >> 2;
+#pragma unroll 4
+                for (int g4 = 0; g4 < n4; ++g4) {
+                    const int4 v = t4[g4];
+                    const bool hx = v.x / CH == cidx, hy = v.y / CH == cidx;
+                    const bool hz = v.z / CH == cidx, hw = v.w / CH == cidx;
+                    if (hx | hy | hz | hw) {
+                        if (hx) live(4 * g4);
+                        if (hy) live(4 * g4 + 1);
+                        if (hz) live(4 * g4 + 2);
+                        if (hw) live(4 * g4 + 3);
+                    }
                 }
+                for (int i = 4 * n4; i < nt; ++i)
+                    if (s_tid[i] / CH == cidx) live(i);
             }
             for (int ci = 0; ci < nc; ++ci) {
                 if (!s_c_zero[ci]) continue;
@@ -831,7 +837,7 @@ __global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
         if (tt >= pre && tt < pre + mysum) {
             u128 acc = pre;
             for (int c = ca; c < cz; ++c) {
-                const u128 w = chunk_w(c);
+                const u128 w = (cz - ca == 1) ? mysum : chunk_w(c);   // (one chunk: known)
                 if (tt < acc + w) {
                     s_cstar = c;
                     s_tt = tt - acc;
