@@ -84,11 +84,11 @@ __device__ __forceinline__ uint4 load_row_vec(const char* base, int vi, int V) {
 // empty list after them, the support, ranking keys and per-entry
 // arrays; the level's priority keys (<= 225 of them) reuse the regions of
 // the support and the ranking keys.  The ranking-key region holds a power
-// of two >= S keys (sorted in place for large supports).  top_min and
+// of two >= S keys.  top_min and
 // k2_min (entries, bytes) enlarge the first two regions for callers that
 // use them as scratch before the pool.
 struct PoolLds {
-    int m, top, k2, w1, q, tq, wr, xs, ir, tx, bytes;
+    int m, top, k2, w1, q, wr, xs, bytes;
 };
 __host__ __device__ inline int pad16(int x) { return (x + 15) & ~15; }
 __host__ __device__ inline int pow2_at_least(int x) {
@@ -107,12 +107,9 @@ __host__ __device__ inline PoolLds pool_lds(int S, int C, int top_min = 0, int k
     L.k2 = L.top + pad16(8 * S2);
     L.w1 = L.k2 + pad16(k2b);
     L.q = L.w1 + pad16(4 * S);
-    L.tq = L.q + pad16(4 * S);
-    L.wr = L.tq + pad16(4 * S);
+    L.wr = L.q + pad16(4 * S);
     L.xs = L.wr + pad16(2 * S);
-    L.ir = L.xs + pad16(2 * S);
-    L.tx = L.ir + pad16(2 * S);
-    L.bytes = L.tx + pad16(2 * S);
+    L.bytes = L.xs + pad16(2 * S);
     return L;
 }
 

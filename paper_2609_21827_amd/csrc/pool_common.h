@@ -64,96 +64,6 @@ __device__ __forceinline__ void rank_all(const uint64_t* keys, int n, int16_t* r
     if (i < n && sub == 0) rank[i] = (int16_t)c;
 }
 
-// Ranks and prefix masses of n keys in LDS: for every key i, the count of
-// larger keys and the sum of w over them, split over F lanes as in rank_all;
-// fn(i, count, mass) is called once per key by one lane.  Keys larger than
-// every other (e.g. 0 for "none") may repeat; the others must be unique.
-template <int NT, typename Fn>
-__device__ __forceinline__ void rank_prefix(const uint64_t* keys, const uint32_t* w, int n,
-                                            Fn fn) {
-    const int t = threadIdx.x % NT;
-    int F = 1;
-    while (F < 16 && 2 * F * n <= NT) F *= 2;
-    const int sub = t % F;
-    // lane `sub` of an entry's F lanes takes entries [j0, j1), a run whose
-    // length and start are multiples of 4: keys read two and weights four
-    // at a time (both arrays 16-byte aligned)
-    const int L = ((n + F - 1) / F + 3) & ~3;
-    const int j0 = min(sub * L, n), j1 = min(j0 + L, n);
-    const ulonglong2* kp = (const ulonglong2*)keys;
-    const uint4* wp = (const uint4*)w;
-    for (int base = 0; base < n; base += NT / F) {
-        const int i = base + t / F;
-        const uint64_t k = keys[i < n ? i : 0];
-        int c = 0;
-        uint64_t pre = 0;
-        int j = j0;
-        for (; j + 3 < j1; j += 4) {
-            const ulonglong2 ka = kp[j / 2], kb = kp[j / 2 + 1];
-            const uint4 ww = wp[j / 4];
-            c += (int)(ka.x > k) + (int)(ka.y > k) + (int)(kb.x > k) + (int)(kb.y > k);
-            pre += (uint64_t)(ka.x > k ? ww.x : 0u) + (uint64_t)(ka.y > k ? ww.y : 0u) +
-                   (uint64_t)(kb.x > k ? ww.z : 0u) + (uint64_t)(kb.y > k ? ww.w : 0u);
-        }
-        for (; j < j1; ++j) {
-            const bool gt = keys[j] > k;
-            c += (int)gt;
-            pre += gt ? (uint64_t)w[j] : 0ull;
-        }
-        for (int o = 1; o < F; o <<= 1) {
-            c += __shfl_xor(c, o);
-            const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)pre, o);
-            const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(pre >> 32), o);
-            pre += ((uint64_t)hi << 32) | lo;
-        }
-        if (i < n && sub == 0) fn(i, c, pre);
-    }
-}
-
-// Ranks by id and prefix masses of the tail entries e[0..n): e[i] = id << 32
-// | weight for a tail entry, ~0 for an entry off the tail.  For every tail
-// entry i, the count of tail entries with a smaller id and the sum of their
-// weights, split over F lanes (F a power of two, F * n <= NT, F <= 8), each
-// lane scanning a contiguous run of the entries two at a time (e 16-byte
-// aligned); fn(i, count, mass) is called once per tail entry by one lane.
-template <int NT, typename Fn>
-__device__ __forceinline__ void id_prefix(const uint64_t* e, int n, Fn fn) {
-    const int t = threadIdx.x % NT;
-    int F = 1;
-    while (F < 8 && 2 * F * n <= NT) F *= 2;
-    const int sub = t % F;
-    const int L = ((n + F - 1) / F + 1) & ~1;
-    const int j0 = min(sub * L, n), j1 = min(j0 + L, n);
-    const ulonglong2* ep = (const ulonglong2*)e;
-    for (int base = 0; base < n; base += NT / F) {
-        const int i = base + t / F;
-        const uint64_t me = e[i < n ? i : 0];
-        const uint32_t id = (uint32_t)(me >> 32);
-        int c = 0;
-        uint64_t pre = 0;
-        int j = j0;
-        for (; j + 1 < j1; j += 2) {
-            const ulonglong2 x = ep[j / 2];
-            const bool lx = (uint32_t)(x.x >> 32) < id, ly = (uint32_t)(x.y >> 32) < id;
-            c += (int)lx + (int)ly;
-            pre += (uint64_t)(lx ? (uint32_t)x.x : 0u) + (uint64_t)(ly ? (uint32_t)x.y : 0u);
-        }
-        if (j < j1) {
-            const uint64_t x = e[j];
-            const bool lx = (uint32_t)(x >> 32) < id;
-            c += (int)lx;
-            pre += lx ? (uint32_t)x : 0u;
-        }
-        for (int o = 1; o < F; o <<= 1) {
-            c += __shfl_xor(c, o);
-            const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)pre, o);
-            const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(pre >> 32), o);
-            pre += ((uint64_t)hi << 32) | lo;
-        }
-        if (i < n && sub == 0 && me != ~0ull) fn(i, c, pre);
-    }
-}
-
 // Synchronisation and sums over the NT threads that form a pool: one wave
 // (small supports) or the whole block.
 template <int NT>
