@@ -25,6 +25,8 @@
 //    the next level's rows expand (Sec. 2.1; App. C.4, step 1).
 // No block waits for another; children fields pass between blocks only
 // through agent-coherent atomic stores and loads.
+#include <type_traits>
+
 #include "rheo_device.h"
 #include "rheo_state.h"
 #include "pool_common.h"
@@ -619,7 +621,7 @@ __device__ void exact_select_fallback(const char* base, int V, int vfirst, uint3
                                       int (*s_tie)[NT / WAVE]) {
     constexpr int VEC = DT ? 8 : 4;
     constexpr int NW = NT / WAVE;
-    static_assert(NQ % 4 == 0 && NQ <= 32, "re-read in groups of four vectors");
+    static_assert(NQ % 4 == 0 && NQ <= 64, "re-read in groups of four vectors");
     const int tid = threadIdx.x, lane = tid % WAVE, wid = tid / WAVE;
     // an opaque trip count keeps each pass a loop (re-reading per pass)
     // rather than one straight-line block holding every element
@@ -1046,7 +1048,11 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
     constexpr int NM = DT ? NQ / 2 : NQ;
     constexpr int CV = LS ? CAPV_L : CAPV;      // candidate vectors held
     constexpr int CC = LS ? CAPC_L : CAPC;      // candidates held
-    static_assert(NQ % (2 * EBATCH) == 0 && NQ <= 32, "batches come in pairs");
+    static_assert(NQ % (2 * EBATCH) == 0 && NQ <= 64, "batches come in pairs");
+    // candidate-vector masks: bf16 vector 2 qi at bit qi, 2 qi + 1 at bit
+    // HALF + qi; fp32 vector q at bit q
+    using mask_t = typename std::conditional<(NQ > 32), uint64_t, uint32_t>::type;
+    constexpr int HALF = NQ > 32 ? 32 : 16;
     extern __shared__ __align__(16) uint8_t s_pdyn[];
     __shared__ __align__(16) uint64_t s_keys_st[LS ? 2 : CAPC];
     __shared__ int16_t s_rank[LS ? 2 : CAPC];
@@ -1057,7 +1063,7 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
     __shared__ int s_cnt;
     __shared__ uint64_t s_red[2 * NW];
     __shared__ int s_redi[NW];
-    __shared__ int s_tie[32][NW];
+    __shared__ int s_tie[NQ][NW];
     __shared__ int s_pu, s_yi;
     __shared__ uint64_t s_u;
     const PoolLds L = row_lds(t.S, LS);
@@ -1219,7 +1225,7 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
     //      s_cvi; if a wave has more than its region holds, but all fit, they
     //      are written again into one list with slots reserved per wave
     constexpr int WCAPR = CV / NW;
-    uint32_t take = 0;
+    mask_t take = 0;
     {
         // vectors of this thread inside the row: q < nqv
         int nqv = min(NQ, max(0, (NVR - lane - (NTE - WAVE) + NTE - 1) / NTE));
@@ -1230,28 +1236,31 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
             const uint32_t hc = (h == 0x8000u) ? 0x7FFFu : h;
             const rs_ushort2 h2 = {(unsigned short)hc, (unsigned short)hc};
             const rs_ushort2 one = {1, 1};
-            uint32_t below = 0;
+            mask_t below = 0;
 #pragma unroll
             for (int qi = 0; qi < NM; ++qi) {
                 const rs_ushort2 c = __builtin_bit_cast(rs_ushort2, vm[qi]);
                 const rs_ushort2 d = __builtin_elementwise_min(__builtin_elementwise_sub_sat(h2, c), one);
-                below |= __builtin_bit_cast(uint32_t, d) << qi;
+                if constexpr (HALF == 16)
+                    below |= __builtin_bit_cast(uint32_t, d) << qi;
+                else
+                    below |= ((mask_t)d.x << qi) | ((mask_t)d.y << (HALF + qi));
             }
-            const uint32_t vlo = (1u << ((nqv + 1) >> 1)) - 1u;
-            const uint32_t vhi = ((1u << (nqv >> 1)) - 1u) << 16;
+            const mask_t vlo = ((mask_t)1 << ((nqv + 1) >> 1)) - 1u;
+            const mask_t vhi = (((mask_t)1 << (nqv >> 1)) - 1u) << HALF;
             take = ~below & (vlo | vhi);
         } else {
 #pragma unroll
-            for (int q = 0; q < NQ; ++q) take |= (uint32_t)(__uint_as_float(vm[q]) >= tau) << q;
-            take &= nqv >= 32 ? 0xFFFFFFFFu : (1u << nqv) - 1u;
+            for (int q = 0; q < NQ; ++q) take |= (mask_t)(__uint_as_float(vm[q]) >= tau) << q;
+            take &= nqv >= 8 * (int)sizeof(mask_t) ? ~(mask_t)0 : ((mask_t)1 << nqv) - 1u;
         }
     }
-    const int tn = __popc(take);
+    const int tn = __popcll((uint64_t)take);
     const int texcl = wave_excl_scan(tn);
     auto push_vectors = [&](int pos, int* dst, int cap) {
-        for (uint32_t mk = take; mk != 0u; mk &= mk - 1u) {
-            const int bb = __builtin_ctz(mk);
-            const int q = DT ? ((bb < 16) ? 2 * bb : 2 * (bb - 16) + 1) : bb;
+        for (mask_t mk = take; mk != 0u; mk &= mk - 1u) {
+            const int bb = __builtin_ctzll((uint64_t)mk);
+            const int q = DT ? ((bb < HALF) ? 2 * bb : 2 * (bb - HALF) + 1) : bb;
             if (pos < cap) dst[pos] = vidx(q);
             ++pos;
         }
@@ -1450,12 +1459,13 @@ hipError_t launch_row_wsum(const TreeDev& t, const LevelArgs& a, hipStream_t s) 
     return hipGetLastError();
 }
 
-// Vectors per thread k_expand_row needs for a row of V elements (16 or 32),
+// Vectors per thread k_expand_row needs for a row of V elements (16, 32 or 48),
 // or 0 if the row is too long for it.
 int expand_row_nq(int dtype, int V) {
     const int nvr = (V + (dtype ? 8 : 4) - 1) / (dtype ? 8 : 4);
     if (nvr <= NTE * 16) return 16;
     if (nvr <= NTE * 32) return 32;
+    if (nvr <= NTE * 48) return 48;
     return 0;
 }
 
@@ -1465,6 +1475,7 @@ static hipError_t launch_row(const TreeDev& t, const LevelArgs& a, int nq, hipSt
     const size_t shm = (size_t)row_lds(t.S, SC == 2).bytes;
     if (nq == 16) k_expand_row<DT, 16, SC><<<grid, NTE, shm, s>>>(t, a);
     else if (nq == 32) k_expand_row<DT, 32, SC><<<grid, NTE, shm, s>>>(t, a);
+    else if (nq == 48) k_expand_row<DT, 48, SC><<<grid, NTE, shm, s>>>(t, a);
     else return hipErrorInvalidValue;
     return hipGetLastError();
 }

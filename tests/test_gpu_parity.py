@@ -113,6 +113,10 @@ def test_tiny_variants(dev, over):
     dict(V=4099, dtype="f32", recipe="zipf_t3", support=64, K=6, depth=5, R=40, B=2),
     dict(V=128256, dtype="bf16", recipe="zipf", support=512, K=8, depth=2, R=10),
     dict(V=70001, dtype="bf16", recipe="zipf", quantum=2.0, support=128, K=4, depth=2, R=6),
+    # rows of more than 16384 vectors: 48 vectors per thread in the row kernel
+    dict(V=70001, dtype="f32", recipe="zipf", support=128, K=4, depth=2, R=6),
+    dict(V=180001, dtype="bf16", recipe="zipf", quantum=1.0, support=256, K=4, depth=2, R=6),
+    dict(V=160001, dtype="bf16", recipe="zipf", support=512, K=6, depth=2, R=10),
     # supports above 256: the whole row as the support, a support that is
     # no power of two, and massive ties at the threshold
     dict(V=1003, dtype="bf16", recipe="zipf", support=1024, K=5, depth=3, R=12),
