@@ -12,9 +12,9 @@ canonical model ("the kernel's precision")
     weight(l; ref, T) = floor(2**30 * 2**t) with t = fl32(fl32(l - ref) * kT),
     kT = fl32(log2(e) / T); 2**t is evaluated as 2**n * P(f) with n = rint(t),
     f = t - n in [-1/2, 1/2] (exact) and P the degree-6 Taylor polynomial of
-    2**f in Horner form with every product and sum rounded separately in
-    fp32 (no fused multiply-add), coefficients c_k = fp32((ln 2)^k / k! * 2**30)
-    correctly rounded.  t is clamped to <= 0; t < -31 gives weight 0.  The
+    2**f in Horner form, each step p <- fl32(p * f + c_k) one fused
+    multiply-add (a single rounding, IEEE 754 fusedMultiplyAdd), coefficients
+    c_k = fp32((ln 2)^k / k! * 2**30) correctly rounded.  t is clamped to <= 0; t < -31 gives weight 0.  The
     integer result is (uint32)(P * 2**30) >> (-n), i.e. floor(P * 2**(30+n)).
     Weights are <= 2**30; sums over <= 262143 tokens fit in 48 bits.
 
@@ -56,6 +56,27 @@ def _poly_coeffs():
 POLY = _poly_coeffs()
 
 
+def fma32(a, b, c):
+    """Correctly rounded fp32 fused multiply-add a * b + c of fp32 arrays.
+    The product is exact in fp64 (48 significant bits); the sum is rounded
+    to odd in fp64 (rounded to nearest, its exact error from TwoSum (Knuth),
+    and the odd one of the two fp64 neighbours of the exact sum when that
+    error is not 0); rounding that to nearest fp32 gives the correctly
+    rounded sum, since fp64 carries more than two bits beyond fp32 (Boldo
+    and Melquiond, "Emulation of FMA and correctly rounded sums: proved
+    algorithms using rounding to odd", IEEE Trans. Computers 57(4), 2008)."""
+    x = np.asarray(a, dtype=np.float32).astype(np.float64) * np.asarray(b, np.float32).astype(np.float64)
+    y = np.asarray(c, dtype=np.float32).astype(np.float64)
+    x, y = np.broadcast_arrays(x, y)
+    s = x + y
+    bp = s - x
+    e = (x - (s - bp)) + (y - bp)
+    even = (s.view(np.uint64) & np.uint64(1)) == 0
+    step = np.nextafter(s, np.where(e > 0, np.inf, -np.inf))
+    s = np.where((e != 0) & even, step, s)
+    return s.astype(np.float32)
+
+
 def k_of_T(T):
     """kT = fp32(log2(e) / T) with T taken as an fp32 value (the ABI's type)."""
     return np.float32(LOG2E / float(np.float32(T)))
@@ -77,8 +98,7 @@ def canonical_weights(logits, ref, T):
     f = (t - n).astype(np.float32)
     p = np.full(f.shape, POLY[6], dtype=np.float32)
     for c in POLY[5::-1]:
-        p = (p * f).astype(np.float32)
-        p = (p + c).astype(np.float32)
+        p = fma32(p, f, c)
     u = p.astype(np.uint32)
     sh = (-n).astype(np.int64).astype(np.uint32)
     w = (u >> sh).astype(np.int64)

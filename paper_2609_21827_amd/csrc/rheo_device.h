@@ -44,8 +44,9 @@ __device__ inline uint64_t philox_draw(uint64_t key, uint64_t purpose,
 // t = fl(fl(l - ref) * kT), kT = fl32(log2(e) / T), t clamped to <= 0 and
 // weight 0 below t = -31.  2^t = 2^n * P(f), n = rint(t), f = t - n, P the
 // degree-6 Taylor polynomial of 2^f with coefficients (ln 2)^k / k! * 2^30
-// rounded to fp32, evaluated in Horner form with separately rounded
-// products and sums.  Result: floor(2^30 P 2^n) = (uint32)(2^30 P) >> -n,
+// rounded to fp32, evaluated in Horner form, each step one fused
+// multiply-add (v_fma_f32: a single rounding).  Result: floor(2^30 P 2^n) =
+// (uint32)(2^30 P) >> -n,
 // taken as the truncating conversion of the exact product 2^30 P * 2^n
 // (a scaling by a power of two, exact; below t = -31 it is < 1, so 0).
 // ---------------------------------------------------------------------------
@@ -53,12 +54,12 @@ __device__ __forceinline__ uint32_t cweight_of_t(float t) {
     const float n = rintf(t);
     const float f = __fsub_rn(t, n);
     float p = 0x1.430912p+17f;
-    p = __fadd_rn(__fmul_rn(p, f), 0x1.5d87fep+20f);
-    p = __fadd_rn(__fmul_rn(p, f), 0x1.3b2ab6p+23f);
-    p = __fadd_rn(__fmul_rn(p, f), 0x1.c6b08ep+25f);
-    p = __fadd_rn(__fmul_rn(p, f), 0x1.ebfbe0p+27f);
-    p = __fadd_rn(__fmul_rn(p, f), 0x1.62e430p+29f);
-    p = __fadd_rn(__fmul_rn(p, f), 0x1.000000p+30f);
+    p = __fmaf_rn(p, f, 0x1.5d87fep+20f);
+    p = __fmaf_rn(p, f, 0x1.3b2ab6p+23f);
+    p = __fmaf_rn(p, f, 0x1.c6b08ep+25f);
+    p = __fmaf_rn(p, f, 0x1.ebfbe0p+27f);
+    p = __fmaf_rn(p, f, 0x1.62e430p+29f);
+    p = __fmaf_rn(p, f, 0x1.000000p+30f);
     return (uint32_t)__builtin_amdgcn_ldexpf(p, (int)n);
 }
 __device__ __forceinline__ uint32_t cweight(float l, float ref, float kT) {

@@ -277,8 +277,10 @@ __device__ bool team_barrier(uint64_t* flags, int g, int G, uint64_t epoch, long
     return *s_ok != 0;
 }
 
+// At least four blocks per compute unit (128 registers a lane): the team
+// shape is sized from how many blocks the device holds at once.
 template <int DT, int DN>
-__global__ __launch_bounds__(NTV) void k_verify(TreeDev t, VerifyArgs a) {
+__global__ __launch_bounds__(NTV, 4) void k_verify(TreeDev t, VerifyArgs a) {
     constexpr int VEC = DT ? 8 : 4;
     constexpr int ESZ = DT ? 2 : 4;
     constexpr int CH = WAVE * VEC;           // tokens per chunk

@@ -73,6 +73,50 @@ def test_canonical_weights_track_exp(T):
     assert np.all(w[exact < 2.0 ** -2] == 0)
 
 
+def _f32_round(q):
+    """Round-to-nearest-even fp32 of an exact rational (by comparison with
+    the neighbours of a close guess; independent of numerics.fma32)."""
+    g = np.float32(float(q))
+    cands = [np.nextafter(g, np.float32(-np.inf)), g, np.nextafter(g, np.float32(np.inf))]
+    def key(v):
+        return (abs(F(float(v)) - q), int(np.array(v, np.float32).view(np.uint32)) & 1)
+    return min(cands, key=key)
+
+
+def test_fma32_is_correctly_rounded():
+    # the canonical Horner steps are fused multiply-adds (one rounding); the
+    # oracle's emulation must round a * b + c exactly once, including the
+    # products that land near a midpoint of two fp32 values
+    rng = np.random.default_rng(11)
+    a = rng.uniform(-2 ** 20, 2 ** 20, 4000).astype(np.float32)
+    b = rng.uniform(-0.5, 0.5, 4000).astype(np.float32)
+    c = rng.uniform(-2 ** 30, 2 ** 30, 4000).astype(np.float32)
+    # hard cases: c cancels most of a * b, and c = -(a * b rounded) + tiny
+    ab32 = (a * b).astype(np.float32)
+    c2 = (-ab32).astype(np.float32)
+    c3 = (-ab32 + np.float32(2.0 ** -30)).astype(np.float32)
+    A = np.concatenate([a, a, a])
+    B = np.concatenate([b, b, b])
+    C = np.concatenate([c, c2, c3])
+    got = numerics.fma32(A, B, C)
+    for x, y, z, g in zip(A[::7], B[::7], C[::7], got[::7]):
+        want = _f32_round(F(float(x)) * F(float(y)) + F(float(z)))
+        assert np.float32(g) == want, (x, y, z)
+    # and it differs from the separately rounded product and sum somewhere
+    sep = ((A * B).astype(np.float32) + C).astype(np.float32)
+    assert np.any(sep != got)
+    # a double-rounding trap: 4(1 + 2^-23) * 4(1 - 2^-23) + (2^28 + 32) lies
+    # 2^-42 below the midpoint 2^28 + 48 of two fp32 values; rounded to fp64
+    # first it becomes the midpoint, which then rounds to even (2^28 + 64)
+    x = np.float32(4.0 * (1 + 2.0 ** -23))
+    y = np.float32(4.0 - 2.0 ** -21)
+    z = np.float32(2.0 ** 28 + 32)
+    want = _f32_round(F(float(x)) * F(float(y)) + F(float(z)))
+    assert want == np.float32(2.0 ** 28 + 32)
+    assert np.float32(np.float64(x) * np.float64(y) + np.float64(z)) != want
+    assert numerics.fma32(np.array([x]), np.array([y]), np.array([z]))[0] == want
+
+
 def test_canonical_weight_edges():
     w = numerics.canonical_weights(np.array([0.0, -0.0, 5.0, -1e-30], np.float32), 0.0, 1.0)
     assert list(w) == [2 ** 30] * 4          # t clamped at 0: the reference weight
