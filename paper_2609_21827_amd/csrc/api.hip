@@ -270,7 +270,6 @@ void layout(rheo_tree* t, Arena& A) {
     take(A, &d.team_sp, B * (1024 + 16));
     take(A, &d.team_nchunk, dense ? B * 1024 * 2 : 1);
     take(A, &d.sel, B * d.NE * (size_t)d.C * d.Sc);
-    take(A, &d.row_cnt, B * d.NE);
     take(A, &d.seq_cnt, B);
 }
 
@@ -285,7 +284,6 @@ int init_state(rheo_tree* t) {
     if (e == hipSuccess) e = hipMemset(d.team_flag, 0, B * 64 * sizeof(uint64_t));
     if (e == hipSuccess) e = hipMemset(d.team_max, 0, B * 64 * sizeof(uint64_t));
     if (e == hipSuccess) e = hipMemset(d.team_sum, 0, B * 64 * sizeof(uint64_t));
-    if (e == hipSuccess) e = hipMemset(d.row_cnt, 0, B * d.NE * sizeof(uint32_t));
     if (e == hipSuccess) e = hipMemset(d.seq_cnt, 0, B * sizeof(uint32_t));
     if (e == hipSuccess && dense) e = hipMemset(d.dflag, 0, B * d.NE * sizeof(int32_t));
     if (e == hipSuccess) e = hipMemset(d.pidx, 0xFF, B * NN * sizeof(int32_t));

@@ -60,7 +60,6 @@ struct TreeDev {
     int32_t* dflag;                // [B * NE]
     float* dref;                   // [B][E]
     int32_t* dleads;               // [B][E][16]
-    uint32_t* row_cnt;             // [B * NE] chunk blocks arrived (0 between launches)
     uint32_t* seq_cnt;             // [B] rows whose pool is written (0 between launches)
     int C, Sc;
     int rrsw;                      // verification leads first (App. D.2)
