@@ -93,7 +93,7 @@ def hold_stream(ms):
 
 
 def expand_kernel_name(w):
-    return ("expand level (k_expand_row; k_select + k_pool below 64 rows)" if w.support > 0
+    return ("expand level (k_expand_row)" if w.support > 0
             else "expand level (k_select + k_dweights + k_dpool)")
 
 

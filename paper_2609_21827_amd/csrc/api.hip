@@ -40,8 +40,9 @@ constexpr int kMaxV = 262143;
 float k_of_T(float T) { return (float)(1.4426950408889634 / (double)T); }
 
 // tokens of one 64-vector sub-chunk (16-byte vectors of bf16 or fp32)
-// Rows in a level from which one block per row fills the chip.
-constexpr int kRowMin = 64;
+// Rows in a level from which the per-row kernel runs (it is the faster of
+// the two at every level size measured, down to a single row).
+constexpr int kRowMin = 1;
 
 int WAVE_TOKENS(int dtype) { return 64 * (dtype == RHEO_BF16 ? 8 : 4); }
 
@@ -174,8 +175,8 @@ int configure(const rheo_config* cfg_in, rheo_tree* t) {
         return fail(RHEO_EINVAL, "vocab %d with support %d exceeds the expand merge capacity",
                     c.vocab, SL);
     }
-    // sparse levels with at least kRowMin rows run one block per row (the
-    // row streamed once, no chunk lists) when the row fits it;
+    // sparse levels run one block per row (the row streamed once, no chunk
+    // lists) when the row fits it and the level has at least row_min rows;
     // RHEO_EXPAND_ROW=0 or 1 forces the chunked or the per-row kernel
     t->row_mode = (!dense && expand_row_nq(c.dtype, c.vocab) > 0) ? -1 : 0;
     if (const char* er = getenv("RHEO_EXPAND_ROW")) {

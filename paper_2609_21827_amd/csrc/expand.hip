@@ -797,6 +797,7 @@ __device__ __forceinline__ void select_block(const TreeDev& t, const LevelArgs& 
     const int v0 = c * NTC * NVC;                           // first vector of the chunk
     const int nvalid = min(V - v0 * VEC, NTC * NVC * VEC);  // >= 1: C = ceil(V / chunk)
     const int nsel = min(t.Sc, nvalid);
+    const int NVR = (V + VEC - 1) / VEC;                    // vectors of the row
     const char* base = (const char*)a.logits + (int64_t)row * t.stride * (DT ? 2 : 4);
     uint64_t* out = t.sel + ((int64_t)row * t.C + c) * t.Sc;
 
@@ -848,10 +849,10 @@ __device__ __forceinline__ void select_block(const TreeDev& t, const LevelArgs& 
     // the nsel-th largest offered code gives tau = the smallest value with
     // code h (each offered maximum is a distinct vector holding an element
     // >= tau), found four bits at a time (offer_threshold).  Elements past
-    // the row end read as -inf
-    // (fp32) or the lowest finite bf16, so tau may fall to that value: then
-    // every element of the chunk is a candidate.  Supports larger than the
-    // offers use all vector maxima.
+    // the row end read as -inf (fp32) or a NaN word (bf16), so in a row's
+    // last chunk tau may fall to -inf; vectors wholly past the row end are
+    // never candidates, so the candidates are then the chunk's valid
+    // elements.  Supports larger than the offers use all vector maxima.
     static_assert(NTC == 256, "one histogram bin per thread");
     uint32_t h = 0;
     if (nsel <= 2 * NTC) {
@@ -892,7 +893,7 @@ __device__ __forceinline__ void select_block(const TreeDev& t, const LevelArgs& 
         for (int i = 0; i < NVC; ++i) {
             const float vmax = DT ? ((i & 1) ? bf_hi(vm[i / 2]) : bf_lo(vm[i / 2]))
                                   : __uint_as_float(vm[i]);
-            const bool take = vmax >= tau;
+            const bool take = vmax >= tau && v0 + i * NTC + tid < NVR;
             const uint64_t msk = __ballot(take);
             if (take) {
                 const int pos = wpos + (int)__builtin_amdgcn_mbcnt_hi(
@@ -924,7 +925,7 @@ __device__ __forceinline__ void select_block(const TreeDev& t, const LevelArgs& 
         for (int i = 0; i < NVC; ++i) {
             const float vmax = DT ? ((i & 1) ? bf_hi(vm[i / 2]) : bf_lo(vm[i / 2]))
                                   : __uint_as_float(vm[i]);
-            const bool take = vmax >= tau;
+            const bool take = vmax >= tau && v0 + i * NTC + tid < NVR;
             const uint64_t msk = __ballot(take);
             if (take) {
                 const int pos = wpos + (int)__builtin_amdgcn_mbcnt_hi(

@@ -128,9 +128,9 @@ def test_tiny_variants(dev, over):
     dict(V=1003, dtype="f32", recipe="gauss", quantum=8.0, support=128, K=5, depth=3, R=12),
     dict(V=4099, dtype="bf16", recipe="gauss", quantum=8.0, support=300, K=5, depth=3, R=12),
 ])
-@pytest.mark.parametrize("row", ["auto", "1"])
+@pytest.mark.parametrize("row", ["auto", "0"])
 def test_edge_shapes(dev, over, row):
-    """row "1": every sparse level on the one-block-per-row kernel."""
+    """row "0": every sparse level on the chunked pair."""
     w = W["tiny"].with_(name="edge", sigma=1.5, sigma_t=0.8, **over)
     tree_kw = {}
     if w.V % 8:
