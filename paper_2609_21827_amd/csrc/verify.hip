@@ -5,11 +5,16 @@
 // what the device holds at once; see launch_verify).
 // At each layer the current node's target row is split into G segments of
 // whole 64*VEC-token chunks; every block holds its segment in registers:
-//   1. segment maximum -> team exchange -> row maximum M
+//   1. the row maximum M.  Dense mode: segment maximum -> team exchange.
+//      Sparse mode: every block reads the target logits at all special
+//      tokens (the candidates and the stored tail of q~) and takes their
+//      maximum as a guess of M, which step 2 uses and checks: M is at least
+//      the guess, and equals it when no segment exceeds it (nearly always:
+//      the target's argmax is almost always among the draft's top tokens);
+//      otherwise M is exchanged and step 2 repeated
 //   2. canonical weights P_v of p = softmax(target / T) (relative to M) for
 //      the segment, the totals of its chunks, and P at the special tokens
-//      (the candidates, and the stored tail of q~) that fall in it ->
-//      team exchange
+//      -> team exchange (sparse: with the guess's check)
 //   3. every block takes the same Algorithm 1 decision from the exchanged
 //      totals with exact integer tests:
 //        s != -1: accept Y iff (U+1) Q_Y S_p <= 2^32 P_Y Z_q; otherwise the
@@ -198,15 +203,21 @@ __device__ bool team_max_exchange(uint64_t* words, int g, int G, uint64_t epoch,
 }
 
 // The team's total of p's weights (sparse mode): every block publishes the
-// sum over its segment (< 2^48: at most 2^18 tokens of weight <= 2^30) in
-// one word with the low 16 bits of the epoch, after its chunk totals; the
-// words then carry every segment's sum, so the total needs no further read.
-// A word left from an earlier barrier is fewer than 2^16 epochs old, so
-// the 16-bit comparison cannot mistake it for the current one.  wsum holds
-// the block's per-wave sums.  Bounded like team_barrier.
+// sum over its segment (< 2^48 - 1: at most 2^18 - 1 tokens of weight
+// <= 2^30) in one word with the low 16 bits of the epoch, after its chunk
+// totals; the words then carry every segment's sum, so the total needs no
+// further read.  A block whose weights were taken relative to a guessed
+// maximum that its segment exceeds publishes 2^48 - 1 instead (no sum
+// reaches it), and *s_miss tells every block of the team.  A word left from
+// an earlier barrier is fewer than 2^16 epochs old, so the 16-bit
+// comparison cannot mistake it for the current one.  wsum holds the block's
+// per-wave sums, kMiss for a wave that saw the guess exceeded.  Bounded like
+// team_barrier.
+constexpr uint64_t kMiss = (1ull << 48) - 1;
+
 __device__ bool team_sum_exchange(uint64_t* words, int g, int G, uint64_t epoch,
                                   const uint64_t* wsum, int nw, long spin_limit, int32_t* err,
-                                  int* s_ok, uint64_t* s_total) {
+                                  int* s_ok, uint64_t* s_total, int* s_miss) {
     constexpr uint64_t M48 = (1ull << 48) - 1;
     const uint64_t e16 = epoch & 0xFFFFull;
     __builtin_amdgcn_s_waitcnt(0);
@@ -215,11 +226,16 @@ __device__ bool team_sum_exchange(uint64_t* words, int g, int G, uint64_t epoch,
         if (threadIdx.x == 0) {
             *s_ok = 1;
             uint64_t sum = 0;
-            for (int w = 0; w < nw; ++w) sum += wsum[w];
-            __hip_atomic_store(&words[g], (e16 << 48) | (sum & M48), __ATOMIC_RELAXED,
-                               __HIP_MEMORY_SCOPE_AGENT);
+            bool miss = false;
+            for (int w = 0; w < nw; ++w) {
+                miss |= wsum[w] == kMiss;
+                sum += wsum[w];
+            }
+            __hip_atomic_store(&words[g], (e16 << 48) | (miss ? kMiss : sum & M48),
+                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
         uint64_t v = 0;
+        bool miss = false;
         long spins = 0;
         for (;;) {
             bool ok = true;
@@ -228,6 +244,7 @@ __device__ bool team_sum_exchange(uint64_t* words, int g, int G, uint64_t epoch,
                                                      __HIP_MEMORY_SCOPE_AGENT);
                 ok = (w >> 48) == e16;
                 v = w & M48;
+                miss = v == kMiss;
             }
             if (__all(ok)) break;
             if (++spins > spin_limit) {
@@ -239,8 +256,12 @@ __device__ bool team_sum_exchange(uint64_t* words, int g, int G, uint64_t epoch,
             }
             __builtin_amdgcn_s_sleep(1);
         }
+        const bool any_miss = __ballot(miss) != 0;
         v = wave_sum_u64(v);
-        if (threadIdx.x == 0) *s_total = v;
+        if (threadIdx.x == 0) {
+            *s_total = v;
+            *s_miss = any_miss ? 1 : 0;
+        }
     }
     __syncthreads();
     return *s_ok != 0;
@@ -291,7 +312,13 @@ __global__ __launch_bounds__(NTV, 4) void k_verify(TreeDev t, VerifyArgs a) {
     __shared__ __align__(16) int32_t s_tid[SPMAX];   // stored tail ids (rank order)
     __shared__ uint32_t s_tq[SPMAX];         // stored tail weights Q
     __shared__ uint32_t s_tp[SPMAX];         // p's weights at tail tokens, then candidates
-    __shared__ u128 s_cn[CH];
+    // the chunk scan of the final sample (s_cn), and before it the live
+    // tail tokens' deficits of every chunk in two limbs (s_dlo, s_dhi)
+    __shared__ __align__(16) uint64_t s_scr[2 * NCMAX];
+    static_assert(2 * CH <= 2 * NCMAX, "s_cn fits the scratch");
+    u128* const s_cn = (u128*)s_scr;
+    uint64_t* const s_dlo = s_scr;
+    uint64_t* const s_dhi = s_scr + NCMAX;
     __shared__ u128 s_w128[NWV];
     __shared__ uint64_t s_red[NWV];
     __shared__ float s_redf[NWV];
@@ -307,7 +334,7 @@ __global__ __launch_bounds__(NTV, 4) void k_verify(TreeDev t, VerifyArgs a) {
     __shared__ uint64_t s_U[16], s_Ufin;         // the layer's uniforms
     __shared__ u128 s_F, s_Zrem, s_tt;
     __shared__ float s_M;
-    __shared__ int s_ok;
+    __shared__ int s_ok, s_miss;
 
     const int tid = threadIdx.x;
     const int lane = tid % WAVE, wid = tid / WAVE;
@@ -402,8 +429,12 @@ __global__ __launch_bounds__(NTV, 4) void k_verify(TreeDev t, VerifyArgs a) {
         // exchange); dense mode, the block that owns the token
         float sp_l = 0.0f;                   // logit of this thread's tail token
         if (sp_id >= 0) sp_l = load_logit<DT>(row, sp_id);
-        float c_l = 0.0f;                    // logit of this lane's candidate
-        if (keep && (!DN || (ctok >= lo_tok && ctok < hi_tok))) c_l = load_logit<DT>(row, ctok);
+        // logit of this lane's child (sparse: every child, pruned or kept,
+        // so that the leads -- the draft's top tokens, not in the stored
+        // tail -- enter the guess of the row maximum)
+        float c_l = 0.0f;
+        if (DN ? keep && ctok >= lo_tok && ctok < hi_tok : ctok >= 0)
+            c_l = load_logit<DT>(row, ctok);
         // dense mode: q~ at this node comes from its draft row (borrowed),
         // the logit of its x_{m+1} and its leads
         const char* drow = nullptr;
@@ -462,87 +493,164 @@ __global__ __launch_bounds__(NTV, 4) void k_verify(TreeDev t, VerifyArgs a) {
             if (fin) s_Ufin = d;
             else s_U[lane] = d >> 32;
         }
-        // ---- 1. row maximum over the segment -------------------------------
-        float mx = -INFINITY;
+        // Weights of the segment relative to Mw: every chunk's total to the
+        // team, the wave's sum returned; *over is set if an element of the
+        // thread exceeds Mw.  The tail past V reads as -inf, of weight 0 for
+        // a finite Mw, so no element needs a bounds test (which would
+        // branch per element and serialise the weights).
+        auto seg_weights = [&](float Mw, bool* over) -> uint64_t {
+            uint64_t wpart = 0;
+            bool ov = false;
 #pragma unroll
-        for (int j = 0; j < JREG; ++j) {
-            if (c0 + wid + NWV * j < c1) {
+            for (int j = 0; j < JREG; ++j) {
+                const int c = c0 + wid + NWV * j;
+                if (c < c1) {
+                    const uint4 xv = xr[j];
+                    uint64_t sum = 0;
 #pragma unroll
-                for (int k = 0; k < VEC; ++k) mx = fmaxf(mx, velem<DT>(xr[j], k));
+                    for (int k = 0; k < VEC; ++k) {
+                        const float l = velem<DT>(xv, k);
+                        ov |= l > Mw;
+                        sum += cweight(l, Mw, a.kT);
+                    }
+                    sum = wave_sum_u64(sum);
+                    wpart += sum;
+                    if (lane == 0)
+                        __hip_atomic_store(&chunk_x[c], sum, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT);
+                }
+            }
+            for (int c = c0 + wid + NWV * JREG; c < c1; c += NWV) {
+                const uint4 xv = load_vec<DT>(row, c * WAVE + lane, V);
+                uint64_t sum = 0;
+#pragma unroll
+                for (int k = 0; k < VEC; ++k) {
+                    const float l = velem<DT>(xv, k);
+                    ov |= l > Mw;
+                    sum += cweight(l, Mw, a.kT);
+                }
+                sum = wave_sum_u64(sum);
+                wpart += sum;
+                if (lane == 0)
+                    __hip_atomic_store(&chunk_x[c], sum, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+            }
+            *over = ov;
+            return wpart;
+        };
+        // the maximum of the thread's elements of the segment
+        auto seg_max = [&]() -> float {
+            float mx = -INFINITY;
+#pragma unroll
+            for (int j = 0; j < JREG; ++j) {
+                if (c0 + wid + NWV * j < c1) {
+#pragma unroll
+                    for (int k = 0; k < VEC; ++k) mx = fmaxf(mx, velem<DT>(xr[j], k));
+                }
+            }
+            for (int c = c0 + wid + NWV * JREG; c < c1; c += NWV) {
+                const uint4 xv = load_vec<DT>(row, c * WAVE + lane, V);
+#pragma unroll
+                for (int k = 0; k < VEC; ++k) mx = fmaxf(mx, velem<DT>(xv, k));
+            }
+            return mx;
+        };
+        float M;
+        if constexpr (!DN) {
+            // ---- 1. the row maximum is guessed as the largest target logit
+            //         at the special tokens and the pruned children (all of
+            //         them in every block); the segment's weights, chunk
+            //         totals and p's weights at the special tokens relative
+            //         to the guess in one pass, which also notes any element
+            //         above the guess; one exchange carries the sums and
+            //         whether any segment exceeds the guess.  The row maximum is at least the guess, so when
+            //         no segment exceeds it, it is the row maximum and every
+            //         weight is the one relative to it.  Otherwise, and at
+            //         a node that was not expanded (no special tokens), the
+            //         maximum is exchanged first and the pass follows.
+            auto special_weights = [&](float Mw) {
+                if (tid < nt) s_tp[tid] = cweight(sp_l, Mw, a.kT);
+                for (int i = tid + NTV; i < nt; i += NTV)
+                    s_tp[i] = cweight(load_logit<DT>(row, s_tid[i]), Mw, a.kT);
+                if (cpos >= 0) s_tp[nt + cpos] = cweight(c_l, Mw, a.kT);
+            };
+            // a node that was not expanded has no special tokens: no guess
+            bool miss = fc < 0;
+            M = -INFINITY;
+            if (!miss) {
+                float gm = (tid < nt) ? sp_l : -INFINITY;
+                for (int i = tid + NTV; i < nt; i += NTV)
+                    gm = fmaxf(gm, load_logit<DT>(row, s_tid[i]));
+                if (ctok >= 0) gm = fmaxf(gm, c_l);
+                gm = block_max<NTV>(gm, s_redf);
+                bool over;
+                const uint64_t wpart = seg_weights(gm, &over);
+                special_weights(gm);
+                over = __ballot(over) != 0;
+                if (lane == 0) s_red[wid] = over ? kMiss : wpart;
+                if (!team_sum_exchange(tsum_x, g, G, epoch + 3 * level + 1, s_red, NWV, a.spin,
+                                       t.err, &s_ok, &s_Sp, &s_miss)) {
+                    failed = true;
+                    break;
+                }
+                M = gm;
+                miss = s_miss != 0;
+            }
+            if (miss) {
+                // (the segment read again: cheaper here than keeping more live)
+                float mx = -INFINITY;
+                for (int c = c0 + wid; c < c1; c += NWV) {
+                    const uint4 xv = load_vec<DT>(row, c * WAVE + lane, V);
+#pragma unroll
+                    for (int k = 0; k < VEC; ++k) mx = fmaxf(mx, velem<DT>(xv, k));
+                }
+                mx = block_max<NTV>(mx, s_redf);
+                if (!team_max_exchange(tmax_x, g, G, epoch + 3 * level + 2, mx, a.spin, t.err,
+                                       &s_ok, &s_M)) {
+                    failed = true;
+                    break;
+                }
+                M = s_M;
+                bool over;
+                const uint64_t wpart = seg_weights(M, &over);
+                special_weights(M);
+                if (lane == 0) s_red[wid] = wpart;
+                if (!team_sum_exchange(tsum_x, g, G, epoch + 3 * level + 3, s_red, NWV, a.spin,
+                                       t.err, &s_ok, &s_Sp, &s_miss)) {
+                    failed = true;
+                    break;
+                }
+            }
+        } else {
+            // ---- 1. row maximum over the segment ---------------------------
+            const float mx = block_max<NTV>(seg_max(), s_redf);
+            if (!team_max_exchange(tmax_x, g, G, epoch + 3 * level + 1, mx, a.spin, t.err, &s_ok,
+                                   &s_M)) {
+                failed = true;
+                break;
+            }
+            M = s_M;
+            // ---- 2. weights of the segment, chunk totals, and p's weights
+            //         at the candidates this block owns ----------------------
+            if (M > -INFINITY) {
+                bool over;
+                (void)seg_weights(M, &over);
+                if (cpos >= 0 && ctok >= lo_tok && ctok < hi_tok)
+                    __hip_atomic_store(&sp_x[nt + cpos], cweight(c_l, M, a.kT), __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+            }
+            if (!team_barrier(flags, g, G, epoch + 3 * level + 2, a.spin, t.err, &s_ok)) {
+                failed = true;
+                break;
             }
         }
-        for (int c = c0 + wid + NWV * JREG; c < c1; c += NWV) {
-            const uint4 xv = load_vec<DT>(row, c * WAVE + lane, V);
-#pragma unroll
-            for (int k = 0; k < VEC; ++k) mx = fmaxf(mx, velem<DT>(xv, k));
-        }
-        mx = block_max<NTV>(mx, s_redf);
-        if (!team_max_exchange(tmax_x, g, G, epoch + 3 * level + 1, mx, a.spin, t.err, &s_ok, &s_M)) {
-            failed = true;
-            break;
-        }
         const int nc = s_nc, spos = s_spos;
-        const float M = s_M;
         if (!(M > -INFINITY)) {
             // no finite target logit at this node: p is undefined.  Every
             // block of the team holds the same M, so all leave here.
             if (g == 0 && tid == 0) atomicOr(t.err, 512);
             failed = true;
             break;
-        }
-        // ---- 2. weights of the segment, chunk totals, and p's weights at
-        //         the special tokens ------------------------------------------
-        uint64_t wpart = 0;                  // this wave's sum over its chunks
-#pragma unroll
-        for (int j = 0; j < JREG; ++j) {
-            const int c = c0 + wid + NWV * j;
-            if (c < c1) {
-                uint64_t sum = 0;
-#pragma unroll
-                for (int k = 0; k < VEC; ++k) {
-                    const int v = (c * WAVE + lane) * VEC + k;
-                    if (v < V) sum += cweight(velem<DT>(xr[j], k), M, a.kT);
-                }
-                sum = wave_sum_u64(sum);
-                wpart += sum;
-                if (lane == 0)
-                    __hip_atomic_store(&chunk_x[c], sum, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            }
-        }
-        for (int c = c0 + wid + NWV * JREG; c < c1; c += NWV) {
-            const uint4 xv = load_vec<DT>(row, c * WAVE + lane, V);
-            uint64_t sum = 0;
-#pragma unroll
-            for (int k = 0; k < VEC; ++k) {
-                const int v = (c * WAVE + lane) * VEC + k;
-                if (v < V) sum += cweight(velem<DT>(xv, k), M, a.kT);
-            }
-            sum = wave_sum_u64(sum);
-            wpart += sum;
-            if (lane == 0)
-                __hip_atomic_store(&chunk_x[c], sum, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-        if constexpr (!DN) {
-            // p's weights at every special token, from the logits read with
-            // the segment; the team's total arrives with the exchange
-            if (tid < nt) s_tp[tid] = cweight(sp_l, M, a.kT);
-            for (int i = tid + NTV; i < nt; i += NTV)
-                s_tp[i] = cweight(load_logit<DT>(row, s_tid[i]), M, a.kT);
-            if (cpos >= 0) s_tp[nt + cpos] = cweight(c_l, M, a.kT);
-            if (lane == 0) s_red[wid] = wpart;
-            if (!team_sum_exchange(tsum_x, g, G, epoch + 3 * level + 2, s_red, NWV, a.spin, t.err,
-                                   &s_ok, &s_Sp)) {
-                failed = true;
-                break;
-            }
-        } else {
-            if (cpos >= 0 && ctok >= lo_tok && ctok < hi_tok)
-                __hip_atomic_store(&sp_x[nt + cpos], cweight(c_l, M, a.kT), __ATOMIC_RELAXED,
-                                   __HIP_MEMORY_SCOPE_AGENT);
-            if (!team_barrier(flags, g, G, epoch + 3 * level + 2, a.spin, t.err, &s_ok)) {
-                failed = true;
-                break;
-            }
         }
         // ---- 3. Algorithm 1 at this layer, by wave 0 (the chunk totals and
         //         the special weights from the team, S_p, the tail deficit,
@@ -760,11 +868,29 @@ __global__ __launch_bounds__(NTV, 4) void k_verify(TreeDev t, VerifyArgs a) {
         // ---- final sample u* ~ r (one block of the team) --------------------
         if (g != 0) break;
         if constexpr (!DN) {
-            // the chunk totals, published before the second exchange
-            for (int c = tid; c < NC; c += NTV)
+            // the chunk totals, published before the second exchange; for
+            // the residual, every chunk's sum of min(P_v Zq, Q_v Z_l) over
+            // the live tail tokens in it, gathered from the tail entries in
+            // two limbs: the deficit is below 2^71 (P_v <= 2^30, Zq < 2^40),
+            // so its low 40 bits and the rest (< 2^31), summed over at most
+            // 1023 entries, stay below 2^64
+            for (int c = tid; c < NC; c += NTV) {
                 s_chunk[c] = __hip_atomic_load(&chunk_x[c], __ATOMIC_RELAXED,
                                                __HIP_MEMORY_SCOPE_AGENT);
+                s_dlo[c] = 0;
+                s_dhi[c] = 0;
+            }
             __syncthreads();
+            if (residual) {
+                for (int i = tid; i < nt; i += NTV) {
+                    const u128 pz = (u128)s_tp[i] * Zq, qs = (u128)s_tq[i] * Zl;
+                    const u128 d = pz < qs ? pz : qs;
+                    const int c = s_tid[i] / CH;
+                    atomicAdd(&s_dlo[c], (uint64_t)d & ((1ull << 40) - 1));
+                    atomicAdd(&s_dhi[c], (uint64_t)(d >> 40));
+                }
+                __syncthreads();
+            }
         }
         const u128 F = s_F;
         const u128 tt = s_tt;
@@ -774,30 +900,8 @@ __global__ __launch_bounds__(NTV, 4) void k_verify(TreeDev t, VerifyArgs a) {
         auto special_def = [&](int cidx, u128* def_out) {
             // F * P_v - N_v summed over the special tokens of chunk cidx
             u128 d = 0;
-            if (residual) {
-                // the stored tail is in rank order: every entry is checked,
-                // four ids per LDS load, the (rare) hits handled one by one
-                auto live = [&](int i) {
-                    const u128 pz = (u128)s_tp[i] * Zq, qs = (u128)s_tq[i] * Zl;
-                    d += pz < qs ? pz : qs;       // F P - N for a live tail token
-                };
-                const int4* t4 = (const int4*)s_tid;
-                const int n4 = nt >> 2;
-#pragma unroll 4
-                for (int g4 = 0; g4 < n4; ++g4) {
-                    const int4 v = t4[g4];
-                    const bool hx = v.x / CH == cidx, hy = v.y / CH == cidx;
-                    const bool hz = v.z / CH == cidx, hw = v.w / CH == cidx;
-                    if (hx | hy | hz | hw) {
-                        if (hx) live(4 * g4);
-                        if (hy) live(4 * g4 + 1);
-                        if (hz) live(4 * g4 + 2);
-                        if (hw) live(4 * g4 + 3);
-                    }
-                }
-                for (int i = 4 * n4; i < nt; ++i)
-                    if (s_tid[i] / CH == cidx) live(i);
-            }
+            // the live tail tokens (sparse), gathered per chunk above
+            if (!DN && residual) d = (u128)s_dlo[cidx] + ((u128)s_dhi[cidx] << 40);
             for (int ci = 0; ci < nc; ++ci) {
                 if (!s_c_zero[ci]) continue;
                 const int v = s_c_tok[ci];

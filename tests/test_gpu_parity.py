@@ -139,6 +139,43 @@ def test_edge_shapes(dev, over, row):
     run_parity(w, range(3), list(range(w.B)), dev=dev, tree_kw=tree_kw, env=env)
 
 
+def _root_guess_misses(w, steps):
+    """Root rows (always verified) whose target maximum lies outside the
+    draft's top-S: there the row maximum is not at a special token."""
+    n = 0
+    for step in steps:
+        keys = [synth.root_key(w, b, step) for b in range(w.B)]
+        d = synth.as_fp32_numpy(synth.draft_rows(w, keys))
+        t = synth.as_fp32_numpy(synth.target_rows(
+            w, keys, [synth.seq_sigma_t(w, b) for b in range(w.B)]))
+        S = min(w.support, w.V)
+        for b in range(w.B):
+            n += int(t[b].argmax()) not in set(np.argsort(-d[b], kind="stable")[:S].tolist())
+    return n
+
+
+@pytest.mark.parametrize("over", [
+    dict(V=1003, dtype="bf16", support=16),
+    dict(V=1001, dtype="f32", support=16),
+    dict(V=4099, dtype="bf16", support=300),
+])
+def test_verify_row_max_off_special_tokens(dev, over):
+    """Target rows far from the draft (sigma_t = 8): the row maximum is
+    seldom at a special token, so the verification layer's guess of it
+    misses and the maximum is exchanged before the weights are redone."""
+    w = W["tiny"].with_(name="guess_miss", recipe="zipf", K=5, depth=3, R=12, B=4,
+                        sigma=1.5, sigma_t=8.0, **over)
+    assert _root_guess_misses(w, range(4)) >= 8
+    run_parity(w, range(4), list(range(w.B)), dev=dev,
+               tree_kw={"row_stride": (w.V + 7) // 8 * 8})
+
+
+def test_verify_row_max_off_special_tokens_llama3(dev):
+    w = W["llama3"].with_(name="llama3_guess_miss", sigma_t=6.0, B=2)
+    assert _root_guess_misses(w, [0]) == 2
+    run_parity(w, [0], [0, 1], dev=dev)
+
+
 def test_llama2(dev):
     run_parity(W["llama2"], range(3), [0], dev=dev)
 
