@@ -64,7 +64,9 @@ __device__ __forceinline__ uint32_t cweight_of_t(float t) {
 }
 __device__ __forceinline__ uint32_t cweight(float l, float ref, float kT) {
     const float t = __fmul_rn(__fsub_rn(l, ref), kT);
-    return cweight_of_t(fmaxf(fminf(t, 0.0f), -64.0f));
+    // t clamped to [-64, 0] in one instruction (t is never NaN for a finite
+    // ref; a signed zero may come out either way, of the same weight)
+    return cweight_of_t(__builtin_amdgcn_fmed3f(t, -64.0f, 0.0f));
 }
 // The same weight for l <= ref (then t <= 0 and the upper clamp is void).
 __device__ __forceinline__ uint32_t cweight_below(float l, float ref, float kT) {

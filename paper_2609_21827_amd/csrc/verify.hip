@@ -507,12 +507,15 @@ __global__ __launch_bounds__(NTV, 4) void k_verify(TreeDev t, VerifyArgs a) {
                 if (c < c1) {
                     const uint4 xv = xr[j];
                     uint64_t sum = 0;
+                    float vmx = -INFINITY;
 #pragma unroll
-                    for (int k = 0; k < VEC; ++k) {
-                        const float l = velem<DT>(xv, k);
-                        ov |= l > Mw;
-                        sum += cweight(l, Mw, a.kT);
+                    for (int k = 0; k < VEC; k += 2) {
+                        // a pair's weights (each <= 2^30) summed in 32 bits
+                        const float la = velem<DT>(xv, k), lb = velem<DT>(xv, k + 1);
+                        vmx = fmaxf(vmx, fmaxf(la, lb));
+                        sum += (uint64_t)(cweight(la, Mw, a.kT) + cweight(lb, Mw, a.kT));
                     }
+                    ov |= vmx > Mw;
                     sum = wave_sum_u64(sum);
                     wpart += sum;
                     if (lane == 0)
@@ -523,12 +526,14 @@ __global__ __launch_bounds__(NTV, 4) void k_verify(TreeDev t, VerifyArgs a) {
             for (int c = c0 + wid + NWV * JREG; c < c1; c += NWV) {
                 const uint4 xv = load_vec<DT>(row, c * WAVE + lane, V);
                 uint64_t sum = 0;
+                float vmx = -INFINITY;
 #pragma unroll
-                for (int k = 0; k < VEC; ++k) {
-                    const float l = velem<DT>(xv, k);
-                    ov |= l > Mw;
-                    sum += cweight(l, Mw, a.kT);
+                for (int k = 0; k < VEC; k += 2) {
+                    const float la = velem<DT>(xv, k), lb = velem<DT>(xv, k + 1);
+                    vmx = fmaxf(vmx, fmaxf(la, lb));
+                    sum += (uint64_t)(cweight(la, Mw, a.kT) + cweight(lb, Mw, a.kT));
                 }
+                ov |= vmx > Mw;
                 sum = wave_sum_u64(sum);
                 wpart += sum;
                 if (lane == 0)
