@@ -568,9 +568,10 @@ __global__ __launch_bounds__(NTV, 4) void k_verify(TreeDev t, VerifyArgs a) {
             //         totals and p's weights at the special tokens relative
             //         to the guess in one pass, which also notes any element
             //         above the guess; one exchange carries the sums and
-            //         whether any segment exceeds the guess.  The row maximum is at least the guess, so when
-            //         no segment exceeds it, it is the row maximum and every
-            //         weight is the one relative to it.  Otherwise, and at
+            //         whether any segment exceeds the guess.  The row
+            //         maximum is at least the guess, so when no segment
+            //         exceeds it, it is the row maximum and every weight is
+            //         the one relative to it.  Otherwise, and at
             //         a node that was not expanded (no special tokens), the
             //         maximum is exchanged first and the pass follows.
             auto special_weights = [&](float Mw) {
