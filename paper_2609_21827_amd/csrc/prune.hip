@@ -15,7 +15,7 @@
 namespace rheo {
 
 constexpr int NTR = 256;
-constexpr int PSPLIT = 8;          // blocks per sequence
+constexpr int PSPLIT = 16;         // blocks per sequence
 
 __global__ __launch_bounds__(NTR) void k_prune(TreeDev t, int R) {
     extern __shared__ ulonglong2 s_key[];    // the sequence's n keys
