@@ -874,7 +874,7 @@ __global__ __launch_bounds__(NTV, 4) void k_verify(TreeDev t, VerifyArgs a) {
         // ---- final sample u* ~ r (one block of the team) --------------------
         if (g != 0) break;
         if constexpr (!DN) {
-            // the chunk totals, published before the second exchange; for
+            // the chunk totals, published before the sum exchange; for
             // the residual, every chunk's sum of min(P_v Zq, Q_v Z_l) over
             // the live tail tokens in it, gathered from the tail entries in
             // two limbs: the deficit is below 2^71 (P_v <= 2^30, Zq < 2^40),
