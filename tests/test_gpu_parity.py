@@ -117,6 +117,10 @@ def test_tiny_variants(dev, over):
     dict(V=70001, dtype="f32", recipe="zipf", support=128, K=4, depth=2, R=6),
     dict(V=180001, dtype="bf16", recipe="zipf", quantum=1.0, support=256, K=4, depth=2, R=6),
     dict(V=160001, dtype="bf16", recipe="zipf", support=512, K=6, depth=2, R=10),
+    # rows too long for the row kernel (more than 24576 vectors): the
+    # chunked pair on every level; the largest vocabulary the library takes
+    dict(V=100003, dtype="f32", recipe="zipf", support=128, K=4, depth=2, R=6),
+    dict(V=262143, dtype="bf16", recipe="zipf", support=256, K=4, depth=2, R=6),
     # supports above 256: the whole row as the support, a support that is
     # no power of two, and massive ties at the threshold
     dict(V=1003, dtype="bf16", recipe="zipf", support=1024, K=5, depth=3, R=12),
