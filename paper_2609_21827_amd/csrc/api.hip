@@ -184,6 +184,11 @@ int configure(const rheo_config* cfg_in, rheo_tree* t) {
         else if (er[0] == '1' && t->row_mode != 0) t->row_mode = 1;
     }
     if (const char* rm = getenv("RHEO_ROW_MIN")) t->row_min = atoi(rm);
+    // levels with more rows than the device holds 512-thread row blocks at
+    // once run 256-thread blocks (twice the vectors per thread, twice the
+    // blocks resident); RHEO_ROW_NARROW=0 or 1 forces the choice
+    t->dev.row_narrow = -1;
+    if (const char* rn = getenv("RHEO_ROW_NARROW")) t->dev.row_narrow = rn[0] == '1' ? 1 : 0;
     const char* env = getenv("RHEO_EXPAND_VARIANT");
     if (env) {
         const int v = atoi(env);
@@ -294,6 +299,8 @@ int init_state(rheo_tree* t) {
     if (e != hipSuccess) return hip_fail(e, "initialising tree state");
     e = verify_shape(d, &t->vG, &t->v_segch, &t->v_grid);
     if (e != hipSuccess) return hip_fail(e, "no co-resident verification team shape for this tree");
+    e = expand_row_slots(d, &d.row_slots);
+    if (e != hipSuccess) return hip_fail(e, "row kernel occupancy");
     return RHEO_OK;
 }
 

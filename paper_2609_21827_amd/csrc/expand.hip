@@ -1039,12 +1039,12 @@ __host__ __device__ inline PoolLds row_lds(int S, bool ls) {
 
 // SC: the support class -- 0: S <= 128 (two offers per thread), 1: S <= 256
 // (four offers), 2: larger supports (LS).
-template <int DT, int NQ, int SC>
-__global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
+template <int DT, int NQ, int SC, int NTB>
+__global__ __launch_bounds__(NTB) void k_expand_row(TreeDev t, LevelArgs a) {
     constexpr bool LS = SC == 2;
     constexpr bool four = SC >= 1;
     constexpr int VEC = DT ? 8 : 4;
-    constexpr int NW = NTE / WAVE;
+    constexpr int NW = NTB / WAVE;
     constexpr int NB = NQ / EBATCH;
     constexpr int NM = DT ? NQ / 2 : NQ;
     constexpr int CV = LS ? CAPV_L : CAPV;      // candidate vectors held
@@ -1080,7 +1080,7 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
     const int S = t.S, K = t.K, V = t.V;
     const int level = a.level;
     const int64_t nb = (int64_t)b * t.NN;
-    const int NVR = (V + VEC - 1) / VEC;          // vectors of the row, <= NTE * NQ
+    const int NVR = (V + VEC - 1) / VEC;          // vectors of the row, <= NTB * NQ
     const int NVF = V / VEC;                       // whole vectors
     const int nsel = S;                            // S <= V
     const char* base = (const char*)a.logits + (int64_t)row * t.stride * (DT ? 2 : 4);
@@ -1093,7 +1093,7 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
     bool has_u = false;
     if (tid == 0) s_cnt = 0;
     if (!LS)
-        for (int i = tid; i < S; i += NTE) s_top[i] = 0ull;   // id -1 until ranked
+        for (int i = tid; i < S; i += NTB) s_top[i] = 0ull;   // id -1 until ranked
 
     // ---- the row, streamed: vector q of this thread is vidx(q) ------------
     // vm: each vector's maximum -- bf16: the 16-bit order codes of vectors
@@ -1107,10 +1107,10 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
     // a fixed slot per wave its reads kept to one offset, and the waves of
     // a block finished streaming up to several µs apart.
     const int wsu = __builtin_amdgcn_readfirstlane(wid);
-    auto vidx = [&](int q) -> int { return (((wsu + q) & (NW - 1)) * WAVE + lane) + NTE * q; };
+    auto vidx = [&](int q) -> int { return (((wsu + q) & (NW - 1)) * WAVE + lane) + NTB * q; };
     auto load_batch = [&](uint4 (&r)[EBATCH], int bt) {
         // plain loads when every lane of the block reads whole vectors
-        if (NTE - 1 + NTE * (bt * EBATCH + EBATCH - 1) < NVF) {
+        if (NTB - 1 + NTB * (bt * EBATCH + EBATCH - 1) < NVF) {
 #pragma unroll
             for (int e = 0; e < EBATCH; ++e)
                 r[e] = load_stream16(base + (int64_t)vidx(bt * EBATCH + e) * 16);
@@ -1181,7 +1181,7 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
 
     // ---- threshold: h = the nsel-th largest of the offered codes (a lower
     //      bound of the nsel-th largest vector maximum)
-    uint32_t h = offer_threshold<NTE>(c1, c2, c3, c4, four, nsel, s_thr);
+    uint32_t h = offer_threshold<NTB>(c1, c2, c3, c4, four, nsel, s_thr);
     if constexpr (LS) {
         // raised to the nsel-th largest vector maximum: the high byte of its
         // code, then the low byte, from histograms of the codes >= h
@@ -1192,7 +1192,7 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
             }
             return ord32(__uint_as_float(vm[q])) >> 16;
         };
-        for (int i = tid; i < 256; i += NTE) s_hist[i] = 0;
+        for (int i = tid; i < 256; i += NTB) s_hist[i] = 0;
         __syncthreads();
 #pragma unroll
         for (int q = 0; q < NQ; ++q) {
@@ -1200,9 +1200,9 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
             if (c >= h && vidx(q) < NVR) atomicAdd(&s_hist[c >> 8], 1);
         }
         __syncthreads();
-        const int2 hi8 = suffix_pick256<NTE>(s_hist, nsel, s_thr);
+        const int2 hi8 = suffix_pick256<NTB>(s_hist, nsel, s_thr);
         if (hi8.x >= 0) {
-            for (int i = tid; i < 256; i += NTE) s_hist[i] = 0;
+            for (int i = tid; i < 256; i += NTB) s_hist[i] = 0;
             __syncthreads();
 #pragma unroll
             for (int q = 0; q < NQ; ++q) {
@@ -1211,7 +1211,7 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
                     atomicAdd(&s_hist[c & 0xFFu], 1);
             }
             __syncthreads();
-            const int2 lo8 = suffix_pick256<NTE>(s_hist, nsel - hi8.y, s_thr);
+            const int2 lo8 = suffix_pick256<NTB>(s_hist, nsel - hi8.y, s_thr);
             if (lo8.x >= 0) h = max(h, ((uint32_t)hi8.x << 8) | (uint32_t)lo8.x);
         }
     }
@@ -1229,7 +1229,7 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
     mask_t take = 0;
     {
         // vectors of this thread inside the row: q < nqv
-        int nqv = min(NQ, max(0, (NVR - lane - (NTE - WAVE) + NTE - 1) / NTE));
+        int nqv = min(NQ, max(0, (NVR - lane - (NTB - WAVE) + NTB - 1) / NTB));
         while (nqv < NQ && vidx(nqv) < NVR) ++nqv;      // at most twice
         if (DT) {
             // code >= h is maximum >= tau, except that a -0 maximum passes
@@ -1320,10 +1320,10 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
         }
     };
     if (!ovf || contig) {
-        if constexpr (LS) {
-            for (int e = tid; e - tid < nv; e += NTE) gather(e);
+        if constexpr (LS || CAPV > NTB) {
+            for (int e = tid; e - tid < nv; e += NTB) gather(e);
         } else {
-            gather(tid);                          // nv <= CAPV <= NTE
+            gather(tid);                          // nv <= CAPV <= NTB
         }
     } else if (tid == 0) {
         s_cnt = CC + 1;                          // too many: exact fallback below
@@ -1333,7 +1333,7 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
     if (cnt > CC) {
         __syncthreads();
         if (tid == 0) s_cnt = 0;
-        exact_select_fallback<DT, NTE, NQ>(
+        exact_select_fallback<DT, NTB, NQ>(
             base, V, 0, h, nsel, CC,
             [=](float v, int id) {
                 const int pos = atomicAdd(&s_cnt, 1);
@@ -1347,15 +1347,15 @@ __global__ __launch_bounds__(NTE) void k_expand_row(TreeDev t, LevelArgs a) {
     if constexpr (LS) {
         // sorted in place (padding 0 sorts last; at least nsel entries)
         const int n2 = pow2_at_least(max(cnt, nsel));
-        for (int i = cnt + tid; i < n2; i += NTE) s_keys[i] = 0ull;
+        for (int i = cnt + tid; i < n2; i += NTB) s_keys[i] = 0ull;
         __syncthreads();
-        bitonic_sort_desc<NTE>(s_keys, n2);
+        bitonic_sort_desc<NTB>(s_keys, n2);
     } else {
-        rank_keys<NTE>(s_keys, cnt, s_rank, s_top, nsel);     // placed as ranked
+        rank_keys<NTB>(s_keys, cnt, s_rank, s_top, nsel);     // placed as ranked
     }
     __syncthreads();
 
-    pool_form<NTE>(t, a, row, s_pdyn, L, s_pu, pr, s_u, s_red, &s_yi);
+    pool_form<NTB>(t, a, row, s_pdyn, L, s_pu, pr, s_u, s_red, &s_yi);
     if (level + 1 >= t.D) return;
     select_frontier(t, a, b, s_top, s_k2);
 }
@@ -1470,13 +1470,28 @@ int expand_row_nq(int dtype, int V) {
     return 0;
 }
 
+// A level of more rows than the device holds 512-thread blocks at once
+// runs 256-thread blocks with twice the vectors per thread (rows of up to
+// 32 vectors per 512 threads), which the device holds twice as many of: the
+// rows past the first round no longer wait for a whole block to end.
+static bool row_narrow(const TreeDev& t, int rows, int nq) {
+    if (nq > 32) return false;
+    if (t.row_narrow >= 0) return t.row_narrow == 1;
+    return t.row_slots > 0 && rows > t.row_slots;
+}
+
 template <int DT, int SC>
 static hipError_t launch_row(const TreeDev& t, const LevelArgs& a, int nq, hipStream_t s) {
     const dim3 grid(t.B * a.P);
     const size_t shm = (size_t)row_lds(t.S, SC == 2).bytes;
-    if (nq == 16) k_expand_row<DT, 16, SC><<<grid, NTE, shm, s>>>(t, a);
-    else if (nq == 32) k_expand_row<DT, 32, SC><<<grid, NTE, shm, s>>>(t, a);
-    else if (nq == 48) k_expand_row<DT, 48, SC><<<grid, NTE, shm, s>>>(t, a);
+    const bool narrow = row_narrow(t, t.B * a.P, nq);
+    if (narrow && nq == 32)
+        k_expand_row<DT, 64, SC, NTE / 2><<<grid, NTE / 2, shm, s>>>(t, a);
+    else if (narrow && nq == 16)
+        k_expand_row<DT, 32, SC, NTE / 2><<<grid, NTE / 2, shm, s>>>(t, a);
+    else if (nq == 16) k_expand_row<DT, 16, SC, NTE><<<grid, NTE, shm, s>>>(t, a);
+    else if (nq == 32) k_expand_row<DT, 32, SC, NTE><<<grid, NTE, shm, s>>>(t, a);
+    else if (nq == 48) k_expand_row<DT, 48, SC, NTE><<<grid, NTE, shm, s>>>(t, a);
     else return hipErrorInvalidValue;
     return hipGetLastError();
 }
@@ -1486,6 +1501,38 @@ static hipError_t launch_row_dt(const TreeDev& t, const LevelArgs& a, int nq, hi
     if (t.S > kLargeSupport) return launch_row<DT, 2>(t, a, nq, s);
     if (t.S > NTE / 4) return launch_row<DT, 1>(t, a, nq, s);
     return launch_row<DT, 0>(t, a, nq, s);
+}
+
+template <int DT, int SC>
+static const void* row_fn(int nq) {
+    if (nq == 16) return (const void*)&k_expand_row<DT, 16, SC, NTE>;
+    if (nq == 32) return (const void*)&k_expand_row<DT, 32, SC, NTE>;
+    if (nq == 48) return (const void*)&k_expand_row<DT, 48, SC, NTE>;
+    return nullptr;
+}
+
+template <int DT>
+static const void* row_fn_dt(int S, int nq) {
+    if (S > kLargeSupport) return row_fn<DT, 2>(nq);
+    if (S > NTE / 4) return row_fn<DT, 1>(nq);
+    return row_fn<DT, 0>(nq);
+}
+
+// How many 512-thread blocks of this tree's row kernel the device holds at
+// once (0 when the rows are too long for the row kernel).
+hipError_t expand_row_slots(const TreeDev& t, int* slots) {
+    *slots = 0;
+    const int nq = expand_row_nq(t.dtype, t.V);
+    const void* fn = t.dtype ? row_fn_dt<1>(t.S, nq) : row_fn_dt<0>(t.S, nq);
+    if (!fn) return hipSuccess;
+    int dev = 0, cus = 0, per = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e == hipSuccess)
+        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &per, fn, NTE, (size_t)row_lds(t.S, t.S > kLargeSupport).bytes);
+    if (e == hipSuccess) *slots = per * cus;
+    return e;
 }
 
 hipError_t launch_expand_row(const TreeDev& t, const LevelArgs& a, hipStream_t s) {

@@ -65,6 +65,8 @@ struct TreeDev {
     int rrsw;                      // verification leads first (App. D.2)
     int topk;                      // pure top-K pools, no sampled slot
     int cfull;                     // construction over the whole vocabulary (sparse)
+    int row_slots;                 // 512-thread row-kernel blocks the device holds at once
+    int row_narrow;                // 256-thread row blocks: 1 always, 0 never, -1 above row_slots
     uint64_t* s1row;               // [B * NE]: its total per row of the level
 };
 
@@ -113,6 +115,7 @@ hipError_t launch_row_wsum(const TreeDev& t, const LevelArgs& a, hipStream_t s);
 hipError_t launch_tree_mask(const TreeDev& t, int R, uint8_t* mask, int32_t* depth,
                             hipStream_t s);
 int expand_row_nq(int dtype, int V);
+hipError_t expand_row_slots(const TreeDev& t, int* slots);
 int expand_variant_count(int dtype);
 int expand_variant_nvc(int v);
 ExpandVariant expand_variant(int dtype, int v, int V, int S);

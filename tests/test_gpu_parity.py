@@ -132,14 +132,15 @@ def test_tiny_variants(dev, over):
     dict(V=1003, dtype="f32", recipe="gauss", quantum=8.0, support=128, K=5, depth=3, R=12),
     dict(V=4099, dtype="bf16", recipe="gauss", quantum=8.0, support=300, K=5, depth=3, R=12),
 ])
-@pytest.mark.parametrize("row", ["auto", "0"])
+@pytest.mark.parametrize("row", ["auto", "0", "narrow"])
 def test_edge_shapes(dev, over, row):
-    """row "0": every sparse level on the chunked pair."""
+    """row "0": every sparse level on the chunked pair; "narrow": the row
+    kernel with 256-thread blocks wherever it takes the row."""
     w = W["tiny"].with_(name="edge", sigma=1.5, sigma_t=0.8, **over)
     tree_kw = {}
     if w.V % 8:
         tree_kw["row_stride"] = (w.V + 7) // 8 * 8
-    env = {"RHEO_EXPAND_ROW": row} if row != "auto" else None
+    env = {"0": {"RHEO_EXPAND_ROW": "0"}, "narrow": {"RHEO_ROW_NARROW": "1"}}.get(row)
     run_parity(w, range(3), list(range(w.B)), dev=dev, tree_kw=tree_kw, env=env)
 
 
@@ -249,6 +250,8 @@ SHAPES = (
     {"RHEO_EXPAND_VARIANT": "1", "RHEO_VERIFY_BLOCKS": "1024"},
     {"RHEO_EXPAND_ROW": "1"},
     {"RHEO_EXPAND_ROW": "0", "RHEO_VERIFY_BLOCKS": "256"},
+    {"RHEO_ROW_NARROW": "1"},
+    {"RHEO_ROW_NARROW": "0"},
 )
 
 
