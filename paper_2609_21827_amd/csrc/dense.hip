@@ -244,6 +244,20 @@ __global__ __launch_bounds__(NTD) void k_dpool(TreeDev t, LevelArgs a) {
         s_y = -1;
         s_cs = -1;
     }
+    // the row's construction and tail totals and its sub-chunk tail totals
+    // (relative to the guess of x_{m+1}), loaded now: they arrive while the
+    // top of the row is ranked
+    uint64_t S1 = 0, Zq = 0;
+    for (int c = 0; c < C; ++c) {
+        S1 += t.dpart[((int64_t)row * C + c) * 2 + 0];
+        Zq += t.dpart[((int64_t)row * C + c) * 2 + 1];
+    }
+    uint64_t dqv[NCHMAX / NTD];
+#pragma unroll
+    for (int q = 0; q < NCHMAX / NTD; ++q) {
+        const int i = tid + q * NTD;
+        dqv[q] = (i < NCH) ? t.dq[(int64_t)row * NCH + i] : 0ull;
+    }
     row_top_by_logit(t, row, s_list, s_tl);
     const float M = key_value(s_tl[0]);
 
@@ -304,17 +318,14 @@ __global__ __launch_bounds__(NTD) void k_dpool(TreeDev t, LevelArgs a) {
     }
     __syncthreads();
 
-    // sums, x_{m+1} and the tail totals
-    uint64_t S1 = 0, Zq = 0;
-    for (int c = 0; c < C; ++c) {
-        S1 += t.dpart[((int64_t)row * C + c) * 2 + 0];
-        Zq += t.dpart[((int64_t)row * C + c) * 2 + 1];
-    }
+    // x_{m+1} and the tail totals
     const float ref_t = key_value(s_x[m]);
     if (tid == 0 && !(ref_t > -INFINITY)) atomicOr(t.err, 512);   // x_{m+1} is -inf
     const int nch = NCH;
     if (ref_t == key_value(s_tl[m])) {
-        for (int i = tid; i < nch; i += NTD) s_sub[i] = t.dq[(int64_t)row * NCH + i];
+#pragma unroll
+        for (int q = 0; q < NCHMAX / NTD; ++q)
+            if (tid + q * NTD < nch) s_sub[tid + q * NTD] = dqv[q];
     } else {
         // the guess of x_{m+1} was wrong (construction-weight ties): tail
         // totals again, relative to the right logit, one sub-chunk per wave
