@@ -113,7 +113,18 @@ typedef struct rheo_config {
 } rheo_config;
 
 /* Allocates a tree for cfg (host pointer, copied).  *out receives the handle.
- * Node capacity per sequence: 1 + K + (D-1) * n_expand * K. */
+ * Node capacity per sequence: 1 + K + (D-1) * n_expand * K.
+ * Launch shapes, read from the environment here and never changing a
+ * result: RHEO_EXPAND_ROW (0: sparse levels on the chunked kernel pair, 1:
+ * on the one-block-per-row kernel wherever the row fits it), RHEO_ROW_MIN
+ * (fewest rows of a level for the per-row kernel, default 1),
+ * RHEO_ROW_NARROW (1 or 0: the per-row kernel's 256-thread blocks always or
+ * never; by default when a level has more rows than the device holds
+ * 512-thread blocks at once), RHEO_EXPAND_VARIANT (chunk size of the
+ * chunked pair), RHEO_VERIFY_BLOCKS (blocks of all verification teams,
+ * default 1024, capped by what the device holds at once).  RHEO_VERIFY_SPIN,
+ * read at each rheo_verify, sets the polls of a team wait before it gives up
+ * (see rheo_verify). */
 int rheo_create(const rheo_config* cfg, rheo_tree** out);
 
 /* rheo_create for callers that cannot allocate device memory (serving loops
