@@ -162,10 +162,12 @@ int configure(const rheo_config* cfg_in, rheo_tree* t) {
     if (16 * (size_t)(d.NN - 1) > 64 * 1024) {
         return fail(RHEO_EINVAL, "tree too large (%d nodes per sequence)", d.NN);
     }
-    // expand variant: 16 vectors per thread and chunk unless the chunk lists
-    // would not fit the merge; RHEO_EXPAND_VARIANT picks another that fits
+    // expand variant: 16 vectors per thread and chunk (dense mode: 8, whose
+    // twice as many chunk blocks run its selection and weight passes about
+    // 4 % faster at the headline shape) unless the chunk lists would not fit
+    // the merge; RHEO_EXPAND_VARIANT picks another that fits
     t->variant = -1;
-    for (int v = 2; v < expand_variant_count(c.dtype); ++v) {
+    for (int v = dense ? 1 : 2; v < expand_variant_count(c.dtype); ++v) {
         if (variant_fits(c.dtype, v, c.vocab, SL, dense)) {
             t->variant = v;
             break;
