@@ -5,16 +5,16 @@
 // what the device holds at once; see launch_verify).
 // At each layer the current node's target row is split into G segments of
 // whole 64*VEC-token chunks; every block holds its segment in registers:
-//   1. the row maximum M.  Dense mode: segment maximum -> team exchange.
-//      Sparse mode: every block reads the target logits at all special
-//      tokens (the candidates and the stored tail of q~) and takes their
-//      maximum as a guess of M, which step 2 uses and checks: M is at least
-//      the guess, and equals it when no segment exceeds it (nearly always:
-//      the target's argmax is almost always among the draft's top tokens);
-//      otherwise M is exchanged and step 2 repeated
+//   1. the row maximum M: every block reads the target logits at all
+//      special tokens (the children, and in sparse mode the stored tail of
+//      q~) and takes their maximum as a guess of M, which step 2 uses and
+//      checks: M is at least the guess, and equals it when no segment
+//      exceeds it (nearly always: the target's argmax is almost always
+//      among the draft's top tokens); otherwise M is exchanged and step 2
+//      repeated
 //   2. canonical weights P_v of p = softmax(target / T) (relative to M) for
 //      the segment, the totals of its chunks, and P at the special tokens
-//      -> team exchange (sparse: with the guess's check)
+//      -> team exchange of the segment sums, with the guess's check
 //   3. every block takes the same Algorithm 1 decision from the exchanged
 //      totals with exact integer tests:
 //        s != -1: accept Y iff (U+1) Q_Y S_p <= 2^32 P_Y Z_q; otherwise the
@@ -360,7 +360,6 @@ __global__ __launch_bounds__(NTV, 4) void k_verify(TreeDev t, VerifyArgs a) {
                                         __HIP_MEMORY_SCOPE_AGENT);
     uint64_t* tmax_x = t.team_max + (int64_t)b * GMAX;
     uint64_t* chunk_x = t.team_chunk + (int64_t)b * NCMAX;
-    uint32_t* sp_x = t.team_sp + (int64_t)b * SPMAX;
     uint64_t* tsum_x = t.team_sum + (int64_t)b * GMAX;
     uint64_t* nchunk_x = t.team_nchunk + (int64_t)b * NCMAX * 2;   // dense residual totals
     auto nchunk_at = [&](int c) -> u128 {
@@ -370,7 +369,6 @@ __global__ __launch_bounds__(NTV, 4) void k_verify(TreeDev t, VerifyArgs a) {
     };
     const int c0 = g * SEGCH;                 // first chunk of this segment
     const int c1 = min(NC, c0 + SEGCH);
-    const int lo_tok = c0 * CH, hi_tok = min(V, c1 * CH);
 
     // the root: pruned index 0; its first child and expanded index
     __shared__ uint64_t s_epoch;
@@ -424,17 +422,15 @@ __global__ __launch_bounds__(NTV, 4) void k_verify(TreeDev t, VerifyArgs a) {
             const int c = c0 + wid + NWV * j;
             xr[j] = (c < c1) ? load_vec<DT>(row, c * WAVE + lane, V) : make_uint4(0, 0, 0, 0);
         }
-        // the logits of the special tokens: sparse mode, every block reads
-        // all of them (each block then has p's weights at them without an
-        // exchange); dense mode, the block that owns the token
+        // the logits of the special tokens: every block reads all of them
+        // (each block then has p's weights at them without an exchange)
         float sp_l = 0.0f;                   // logit of this thread's tail token
         if (sp_id >= 0) sp_l = load_logit<DT>(row, sp_id);
-        // logit of this lane's child (sparse: every child, pruned or kept,
-        // so that the leads -- the draft's top tokens, not in the stored
-        // tail -- enter the guess of the row maximum)
+        // logit of this lane's child (every child, pruned or kept, so that
+        // the leads -- the draft's top tokens, not in a stored tail -- enter
+        // the guess of the row maximum)
         float c_l = 0.0f;
-        if (DN ? keep && ctok >= lo_tok && ctok < hi_tok : ctok >= 0)
-            c_l = load_logit<DT>(row, ctok);
+        if (ctok >= 0) c_l = load_logit<DT>(row, ctok);
         // dense mode: q~ at this node comes from its draft row (borrowed),
         // the logit of its x_{m+1} and its leads
         const char* drow = nullptr;
@@ -543,25 +539,8 @@ __global__ __launch_bounds__(NTV, 4) void k_verify(TreeDev t, VerifyArgs a) {
             *over = ov;
             return wpart;
         };
-        // the maximum of the thread's elements of the segment
-        auto seg_max = [&]() -> float {
-            float mx = -INFINITY;
-#pragma unroll
-            for (int j = 0; j < JREG; ++j) {
-                if (c0 + wid + NWV * j < c1) {
-#pragma unroll
-                    for (int k = 0; k < VEC; ++k) mx = fmaxf(mx, velem<DT>(xr[j], k));
-                }
-            }
-            for (int c = c0 + wid + NWV * JREG; c < c1; c += NWV) {
-                const uint4 xv = load_vec<DT>(row, c * WAVE + lane, V);
-#pragma unroll
-                for (int k = 0; k < VEC; ++k) mx = fmaxf(mx, velem<DT>(xv, k));
-            }
-            return mx;
-        };
         float M;
-        if constexpr (!DN) {
+        {
             // ---- 1. the row maximum is guessed as the largest target logit
             //         at the special tokens and the pruned children (all of
             //         them in every block); the segment's weights, chunk
@@ -627,28 +606,6 @@ __global__ __launch_bounds__(NTV, 4) void k_verify(TreeDev t, VerifyArgs a) {
                     break;
                 }
             }
-        } else {
-            // ---- 1. row maximum over the segment ---------------------------
-            const float mx = block_max<NTV>(seg_max(), s_redf);
-            if (!team_max_exchange(tmax_x, g, G, epoch + 3 * level + 1, mx, a.spin, t.err, &s_ok,
-                                   &s_M)) {
-                failed = true;
-                break;
-            }
-            M = s_M;
-            // ---- 2. weights of the segment, chunk totals, and p's weights
-            //         at the candidates this block owns ----------------------
-            if (M > -INFINITY) {
-                bool over;
-                (void)seg_weights(M, &over);
-                if (cpos >= 0 && ctok >= lo_tok && ctok < hi_tok)
-                    __hip_atomic_store(&sp_x[nt + cpos], cweight(c_l, M, a.kT), __ATOMIC_RELAXED,
-                                       __HIP_MEMORY_SCOPE_AGENT);
-            }
-            if (!team_barrier(flags, g, G, epoch + 3 * level + 2, a.spin, t.err, &s_ok)) {
-                failed = true;
-                break;
-            }
         }
         const int nc = s_nc, spos = s_spos;
         if (!(M > -INFINITY)) {
@@ -688,40 +645,7 @@ __global__ __launch_bounds__(NTV, 4) void k_verify(TreeDev t, VerifyArgs a) {
             // latency-critical single-wave section: issue ahead of the
             // weight passes of other blocks on this compute unit
             __builtin_amdgcn_s_setprio(3);
-            uint64_t part = 0;
-            if constexpr (DN) {
-            for (int cb = 0; cb < NC; cb += 4 * WAVE) {
-                uint64_t cv[4];
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const int c = cb + q * WAVE + lane;
-                    cv[q] = (c < NC) ? __hip_atomic_load(&chunk_x[c], __ATOMIC_RELAXED,
-                                                         __HIP_MEMORY_SCOPE_AGENT) : 0ull;
-                }
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const int c = cb + q * WAVE + lane;
-                    if (c < NC) s_chunk[c] = cv[q];
-                    part += cv[q];
-                }
-            }
-            const int nsp = nt + nc;
-            for (int ib = 0; ib < nsp; ib += 4 * WAVE) {
-                uint32_t pv[4];
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const int i = ib + q * WAVE + lane;
-                    pv[q] = (i < nsp) ? __hip_atomic_load(&sp_x[i], __ATOMIC_RELAXED,
-                                                          __HIP_MEMORY_SCOPE_AGENT) : 0u;
-                }
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const int i = ib + q * WAVE + lane;
-                    if (i < nsp) s_tp[i] = pv[q];
-                }
-            }
-            }
-            Sp = DN ? wave_sum_u64(part) : s_Sp;
+            Sp = s_Sp;
             wave_sync();
 
             // RRSw (App. D.2): the leads -- the candidates before the sampled
@@ -873,7 +797,7 @@ __global__ __launch_bounds__(NTV, 4) void k_verify(TreeDev t, VerifyArgs a) {
         }
         // ---- final sample u* ~ r (one block of the team) --------------------
         if (g != 0) break;
-        if constexpr (!DN) {
+        {
             // the chunk totals, published before the sum exchange; for
             // the residual, every chunk's sum of min(P_v Zq, Q_v Z_l) over
             // the live tail tokens in it, gathered from the tail entries in

@@ -146,14 +146,15 @@ def test_edge_shapes(dev, over, row):
 
 def _root_guess_misses(w, steps):
     """Root rows (always verified) whose target maximum lies outside the
-    draft's top-S: there the row maximum is not at a special token."""
+    draft's top-S (dense mode: top-K, the children): there the row maximum
+    is not at a special token."""
     n = 0
     for step in steps:
         keys = [synth.root_key(w, b, step) for b in range(w.B)]
         d = synth.as_fp32_numpy(synth.draft_rows(w, keys))
         t = synth.as_fp32_numpy(synth.target_rows(
             w, keys, [synth.seq_sigma_t(w, b) for b in range(w.B)]))
-        S = min(w.support, w.V)
+        S = min(w.support, w.V) if w.support > 0 else w.K
         for b in range(w.B):
             n += int(t[b].argmax()) not in set(np.argsort(-d[b], kind="stable")[:S].tolist())
     return n
@@ -163,6 +164,9 @@ def _root_guess_misses(w, steps):
     dict(V=1003, dtype="bf16", support=16),
     dict(V=1001, dtype="f32", support=16),
     dict(V=4099, dtype="bf16", support=300),
+    # dense mode: the special tokens are the children
+    dict(V=1003, dtype="bf16", support=0),
+    dict(V=1001, dtype="f32", support=0),
 ])
 def test_verify_row_max_off_special_tokens(dev, over):
     """Target rows far from the draft (sigma_t = 8): the row maximum is
